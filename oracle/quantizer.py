@@ -1,0 +1,139 @@
+"""Affine asymmetric per-token group quantizer -- oracle (test infrastructure).
+
+Follows Appendix C.4, "Affine group quantization": every token is quantized on
+its own, in groups of 64 consecutive coordinates.  For ``b`` bits,
+``m = 2**b - 1`` and, per group with extrema ``xmin``, ``xmax``::
+
+    s = max(xmax - xmin, 1e-8) / m
+    z = clip(round(-xmin / s), 0, m)
+    q = clip(round(x / s + z), 0, m)
+    x_hat = s * (q - z)
+
+with round-half-to-even and no special case for constant groups.  Native
+execution keeps the stored (rounded) scale and dequantizes with it (same
+paragraph, last sentence).
+
+Readings taken where the paper leaves a choice (all listed in the design doc):
+  * inputs are bf16, widened exactly to fp32; every step is one IEEE fp32
+    operation with round-half-to-even, in the order written above (a true
+    division, then an addition: two roundings, no fused multiply-add);
+  * the constant 1e-8 is the fp32 value nearest to it;
+  * codes come from the unrounded fp32 scale ``s``; the stored scale is
+    ``fp16(s)`` (round-half-to-even, subnormals kept) and the stored zero is
+    ``fp16(z)``, which is exact;
+  * dequantization is ``fp16scale * (q - fp16zero)`` evaluated in fp32
+    (``q - z`` is exact, so this is a single rounding).
+
+Codes are packed little-endian inside a byte: for 4 bits channel ``2j`` sits in
+bits 0-3 of byte ``j`` and channel ``2j+1`` in bits 4-7; for 2 bits channel
+``4j+k`` sits in bits ``2k..2k+1`` of byte ``j``.
+
+Pure numpy; shares no code with the GPU library.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+GROUP = 64
+EPS = np.float32(1e-8)
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bit patterns (uint16) to float32."""
+    bits = np.asarray(bits, dtype=np.uint16)
+    return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def levels(bits: int) -> np.float32:
+    """``m = 2**b - 1`` as fp32 (Appendix C.4)."""
+    if bits not in (2, 4):
+        raise ValueError(f"unsupported bit width {bits}")
+    return np.float32((1 << bits) - 1)
+
+
+def quantize_groups(x: np.ndarray, bits: int):
+    """Quantize the last axis of ``x`` (float32, length 64 = one group).
+
+    Returns ``(q, s, z)``: integer codes (uint8, same shape as ``x``), the
+    unrounded fp32 scale and the fp32 zero-point per group (shape ``x.shape[:-1]``).
+    """
+    x = np.asarray(x, dtype=np.float32)
+    if x.shape[-1] != GROUP:
+        raise ValueError("last axis must be one group of 64 coordinates")
+    m = levels(bits)
+    xmin = x.min(axis=-1)
+    xmax = x.max(axis=-1)
+    r = (xmax - xmin).astype(np.float32)                       # fp32 subtraction
+    s = (np.maximum(r, EPS) / m).astype(np.float32)            # true fp32 division
+    z = np.clip(np.rint((-xmin) / s), np.float32(0), m).astype(np.float32)
+    t = (x / s[..., None]).astype(np.float32)                  # rounding 1: divide
+    t = (t + z[..., None]).astype(np.float32)                  # rounding 2: add
+    q = np.clip(np.rint(t), np.float32(0), m).astype(np.uint8)
+    return q, s, z
+
+
+def stored_meta(s: np.ndarray, z: np.ndarray):
+    """Stored fp16 scale and zero-point (round-half-to-even, subnormals kept)."""
+    return (np.asarray(s, dtype=np.float32).astype(np.float16),
+            np.asarray(z, dtype=np.float32).astype(np.float16))
+
+
+def dequantize(q: np.ndarray, scale16: np.ndarray, zero16: np.ndarray) -> np.ndarray:
+    """``x_hat = scale * (q - zero)`` in fp32 with the stored fp16 metadata.
+
+    ``q`` has a trailing group axis of 64; ``scale16``/``zero16`` one value per group.
+    """
+    sc = np.asarray(scale16, dtype=np.float16).astype(np.float32)[..., None]
+    ze = np.asarray(zero16, dtype=np.float16).astype(np.float32)[..., None]
+    d = (np.asarray(q).astype(np.float32) - ze).astype(np.float32)   # exact: small integers
+    return (sc * d).astype(np.float32)
+
+
+def pack_codes(q: np.ndarray, bits: int) -> np.ndarray:
+    """Pack integer codes along the last axis into bytes (little-endian fields)."""
+    q = np.asarray(q, dtype=np.uint8)
+    per = 8 // bits
+    if q.shape[-1] % per:
+        raise ValueError("channel count must fill whole bytes")
+    mask = np.uint8((1 << bits) - 1)
+    if np.any(q > mask):
+        raise ValueError("code out of range")
+    q = q.reshape(q.shape[:-1] + (q.shape[-1] // per, per))
+    out = np.zeros(q.shape[:-1], dtype=np.uint8)
+    for k in range(per):
+        out |= (q[..., k] & mask) << np.uint8(bits * k)
+    return out
+
+
+def unpack_codes(packed: np.ndarray, bits: int) -> np.ndarray:
+    """Inverse of :func:`pack_codes`."""
+    packed = np.asarray(packed, dtype=np.uint8)
+    per = 8 // bits
+    mask = np.uint8((1 << bits) - 1)
+    parts = [(packed >> np.uint8(bits * k)) & mask for k in range(per)]
+    out = np.stack(parts, axis=-1)
+    return out.reshape(packed.shape[:-1] + (packed.shape[-1] * per,))
+
+
+def quantize_token_path(x_bits: np.ndarray, bits: int):
+    """Quantize one cache path for a batch of tokens.
+
+    ``x_bits``: bf16 bit patterns, shape ``[n, d]`` with ``d % 64 == 0``.
+    Returns ``(packed [n, d*bits/8] uint8, scale16 [n, d/64], zero16 [n, d/64])``.
+    """
+    x = bf16_bits_to_f32(x_bits)
+    n, d = x.shape
+    if d % GROUP:
+        raise ValueError("path width must be a multiple of the group size")
+    q, s, z = quantize_groups(x.reshape(n, d // GROUP, GROUP), bits)
+    s16, z16 = stored_meta(s, z)
+    return pack_codes(q.reshape(n, d), bits), s16, z16
+
+
+def dequantize_token_path(packed: np.ndarray, scale16: np.ndarray, zero16: np.ndarray,
+                          bits: int) -> np.ndarray:
+    """Dequantize packed codes ``[n, d*bits/8]`` back to fp32 ``[n, d]``."""
+    q = unpack_codes(packed, bits)
+    n, d = q.shape
+    xh = dequantize(q.reshape(n, d // GROUP, GROUP), scale16, zero16)
+    return xh.reshape(n, d)
