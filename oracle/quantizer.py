@@ -18,6 +18,8 @@ Readings taken where the paper leaves a choice (all listed in the design doc):
     operation with round-half-to-even, in the order written above (a true
     division, then an addition: two roundings, no fused multiply-add);
   * the constant 1e-8 is the fp32 value nearest to it;
+  * the zero-point is the integer ``clip(round(-xmin/s), 0, m)``; when
+    ``-xmin/s`` rounds to -0 it is stored as +0;
   * codes come from the unrounded fp32 scale ``s``; the stored scale is
     ``fp16(s)`` (round-half-to-even, subnormals kept) and the stored zero is
     ``fp16(z)``, which is exact;
@@ -66,6 +68,7 @@ def quantize_groups(x: np.ndarray, bits: int):
     r = (xmax - xmin).astype(np.float32)                       # fp32 subtraction
     s = (np.maximum(r, EPS) / m).astype(np.float32)            # true fp32 division
     z = np.clip(np.rint((-xmin) / s), np.float32(0), m).astype(np.float32)
+    z = (z + np.float32(0)).astype(np.float32)   # the integer zero-point: +0, never -0
     t = (x / s[..., None]).astype(np.float32)                  # rounding 1: divide
     t = (t + z[..., None]).astype(np.float32)                  # rounding 2: add
     q = np.clip(np.rint(t), np.float32(0), m).astype(np.uint8)
