@@ -1,0 +1,206 @@
+"""Benchmark of the low-bit MLA decode step on one MI355X.
+
+A step is one pass of the decode hot path for one cache layer: quantize-append
+the step's new tokens, fused low-bit decode attention over the paged cache,
+and the split-KV combine.  The workload is the 128-head DeepSeek-V3-shaped
+decode batch (32 sequences x 4096 tokens, INT4 content + INT4 RoPE key).
+Successive steps cycle through 8 resident layer caches (8 x 42.5 MB), more
+than the 256 MB last-level cache holds, as a model's layer loop would.
+
+Printed: one JSON line (stdout) with whole-step decode tokens/s, the decode
+kernel's roofline (live HIP-event timing of the kernel on its stream), the
+same step over a BF16 cache (the unquantized comparison), the
+batch-64 x 32K-token target shape for both caches, and the CPU oracle timed on
+a bounded sample of the workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decode attn tokens/s + HBM GB/s & MFMA util vs peak, 128 heads, INT4/INT4 vs BF16"
+MAIN = "dsv3_b32_h128_4k_c4r4"
+TARGET = "c4r4_b64_h128_32k"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+LAYERS = 8
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(run) -> int:
+    """HBM bytes one decode launch must move: every attended key once, queries,
+    and partials (written, then read by the combine) or the output."""
+    keys = int(run.lens.astype(np.int64).sum()) * run.cache_token_bytes()
+    q = run.B * run.s_q * run.H * (512 + 64) * 2
+    rows = run.B * run.s_q * run.H
+    if run.split_tokens:
+        parts = run.num_splits * run.s_q * run.H * (512 + 2) * 4
+        return keys + q + parts
+    return keys + q + rows * 512 * 2
+
+
+def time_workload(name, kind, steps, warmup, layers, token_cache=None):
+    import torch
+
+    from paper_2609_36760_amd import _binding as mb
+    from paper_2609_36760_amd import synthetic as syn
+    from paper_2609_36760_amd.runner import DecodeRun
+    w = syn.WORKLOADS[name]
+    t0 = time.perf_counter()
+    run = DecodeRun(w, kind=kind, token_cache=token_cache)
+    caches = [run.cache] + [run.cache.clone() for _ in range(layers - 1)]
+    torch.cuda.synchronize()
+    log(f"[{name} {kind}] setup {time.perf_counter() - t0:.1f}s, cache {run.cache.numel() / 1e6:.1f} MB x {layers}")
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    dec = mb.mla_lowbit_decode_attn if kind == "lowbit" else mb.mla_bf16_decode_attn
+    app = mb.mla_lowbit_quant_append if kind == "lowbit" else mb.mla_bf16_append
+
+    def one_step(i, ev=None):
+        cache = caches[i % layers]
+        app(run.fmt, run.new_c, run.new_k, run.new_slots, cache, run.num_pages, stream=sh)
+        if ev is not None:
+            ev[0].record(stream)
+        dec(run.fmt, run.q_lat, run.q_rope, cache, run.num_pages, run.block_table, run.seq_lens, run.s_q, run.H,
+            run.tau, split_tokens=run.split_tokens, split_indptr=run.split_indptr, num_splits=run.num_splits,
+            out=run.out, lse=run.lse, part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
+        if ev is not None:
+            ev[1].record(stream)
+        if run.split_tokens:
+            mb.mla_splitkv_combine(run.part_m, run.part_s, run.part_o, run.split_indptr, run.B, run.s_q, run.H,
+                                   run.out, run.lse, stream=sh)
+
+    for i in range(warmup):
+        one_step(i)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        one_step(i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    ms_step = wall * 1e3 / steps
+    flops = run.flops()
+    nbytes = algorithmic_bytes(run)
+    res = {
+        "workload": name, "kind": kind, "ms_per_step": ms_step,
+        "decode_tokens_per_s": run.B * run.s_q / (ms_step * 1e-3),
+        "kv_tokens_per_s": float(run.lens.sum()) / (ms_step * 1e-3),
+        "decode_kernel_ms": kern_ms,
+        "decode_kernel_tflops": flops / (kern_ms * 1e-3) / 1e12,
+        "decode_kernel_gbs": nbytes / (kern_ms * 1e-3) / 1e9,
+        "flops_per_launch": flops, "bytes_per_launch": nbytes,
+        "splits": run.num_splits,
+    }
+    res["mfma_frac"] = res["decode_kernel_tflops"] / PEAK_BF16_TFLOPS
+    res["hbm_frac"] = res["decode_kernel_gbs"] / PEAK_HBM_GBS
+    log(f"[{name} {kind}] {ms_step * 1e3:.1f} us/step, decode kernel {kern_ms * 1e3:.1f} us = "
+        f"{res['decode_kernel_tflops']:.1f} TFLOP/s ({100 * res['mfma_frac']:.1f}% MFMA), "
+        f"{res['decode_kernel_gbs']:.0f} GB/s ({100 * res['hbm_frac']:.1f}% HBM)")
+    del run, caches
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(budget_s: float = 12.0):
+    """The oracle, as it stands, on whole sequences of the main workload."""
+    from oracle import attention as at
+    from oracle import paged_cache as pc
+    from paper_2609_36760_amd import synthetic as syn
+    w = syn.WORKLOADS[MAIN]
+    fmt = pc.CacheFormat(c_bits=w.layers[0][0], r_bits=w.layers[0][1])
+    lens = syn.seq_lens(w)
+    done, spent, first = 0, 0.0, None
+    while done < w.B and spent < budget_s:
+        b = done
+        c, k = syn.sequence_tokens(w, 0, b, int(lens[b]))
+        ql, qr = syn.queries(w, 0, batch=[b])
+        ts = time.perf_counter()
+        c_hat, kr_hat = pc.encode_sequence_dense(fmt, c, k)
+        at.decode_sequence(ql[0], qr[0], c_hat, kr_hat, w.tau)
+        dt = time.perf_counter() - ts
+        first = dt if first is None else first
+        spent += dt
+        done += 1
+    el = spent
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = 1
+    return {"value": done * w.s_q / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} of {w.B} sequences of {MAIN} (4096 tokens, 128 heads each): fp32 quantize + "
+                      f"dequant of every cached token and fp64 attention of all heads; oracle time {el:.1f}s "
+                      f"(input generation excluded)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-target", action="store_true", help="skip the batch-64 x 32K target shape")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no multi-GPU path; "
+              "the per-GPU kernel is the whole workload.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+
+    main_lb = time_workload(MAIN, "lowbit", args.steps, args.warmup, LAYERS)
+    main_bf = time_workload(MAIN, "bf16", args.steps, args.warmup, LAYERS)
+    extra = {}
+    if not args.no_target:
+        tc = {}
+        t_lb = time_workload(TARGET, "lowbit", max(args.steps // 5, 5), 3, 1, token_cache=tc)
+        t_bf = time_workload(TARGET, "bf16", max(args.steps // 5, 5), 3, 1, token_cache=tc)
+        del tc
+        extra[TARGET] = {"c4r4": t_lb, "bf16": t_bf,
+                         "speedup_vs_bf16": t_bf["ms_per_step"] / t_lb["ms_per_step"]}
+    cpu = None if args.no_cpu else cpu_baseline()
+
+    line = {
+        "metric": METRIC,
+        "value": main_lb["decode_tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": main_lb["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": MAIN, "batch": 32, "heads": 128, "context": 4096, "s_q": 1,
+                   "cache": "INT4 content + INT4 RoPE key, group 64, fp16 scale/zero",
+                   "split_tokens": 512, "layers_cycled": LAYERS},
+        "roofline": {"bound": "mfma", "achieved": main_lb["decode_kernel_tflops"], "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": main_lb["mfma_frac"], "traffic": None},
+        "hbm_gbs": main_lb["decode_kernel_gbs"], "hbm_frac": main_lb["hbm_frac"],
+        "bf16_cache": {"value": main_bf["decode_tokens_per_s"], "ms_per_step": main_bf["ms_per_step"],
+                       "decode_kernel_ms": main_bf["decode_kernel_ms"], "hbm_gbs": main_bf["decode_kernel_gbs"],
+                       "hbm_frac": main_bf["hbm_frac"], "mfma_frac": main_bf["mfma_frac"]},
+        "speedup_vs_bf16": main_bf["ms_per_step"] / main_lb["ms_per_step"],
+        "cpu_baseline": cpu,
+        "context": {"paper_kv_compression_128k": 3.59, "paper_serving_speedup_vs_bf16": 5.168,
+                    "paper_hardware": "unnamed NVIDIA GPUs (one for kernels, eight for serving)"},
+    }
+    line.update(extra)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,209 @@
+/*
+ * mla_lowbit.h -- C ABI of the low-bit MLA decode library for AMD MI355X (gfx950).
+ *
+ * The library computes absorbed-form Multi-head Latent Attention decode
+ * (Sec. 2.1, eq. mla_compact) directly over a packed low-bit, paged cache of
+ * the two MLA cache paths: the shared content latent C (d_c = 512 channels,
+ * 4- or 2-bit codes) and the decoupled RoPE key K_P (d_r = 64 channels, 4-bit
+ * codes).  Unpacking and dequantization are fused into attention
+ * (Sec. 3.3; Appendix C.5, "Cache update and tile reuse").  The cache holds
+ * latents already in the offline-fused coordinates, so no transformation is
+ * applied here.
+ *
+ * Conventions for every entry point
+ *   - Pointers named as device buffers must be device memory of the current
+ *     HIP device; host pointers are marked "host".  The caller owns every
+ *     buffer; the library allocates nothing and keeps no state between calls
+ *     except a per-thread copy of the last HIP error.
+ *   - bf16 tensors are passed as uint16_t bit patterns.  All tensors are dense
+ *     and row-major in the index order given, unless a stride is an argument.
+ *   - GPU work is enqueued on `stream` (0 = the null stream) and is
+ *     asynchronous; no call synchronizes.
+ *   - Arguments are validated on the host before any HIP call.  Return codes:
+ *       MLA_OK      success (work enqueued)
+ *       MLA_EINVAL  a null pointer, a negative size or an ill-formed format
+ *       MLA_ENOTSUP well-formed, but a shape this build does not implement
+ *       MLA_EHIP    a HIP launch failed; mla_last_hip_error() gives the code
+ *   - Device-resident values (page ids, sequence lengths, split offsets) are
+ *     not readable by the host without a synchronization and are preconditions:
+ *     s_q <= seq_lens[b] <= max_pages_per_seq * page_size, 0 <= page id <
+ *     num_pages, split_indptr as produced by mla_plan_splits, finite inputs.
+ *     Kernels clamp every index into its buffer, so a violated precondition
+ *     gives unspecified results but no out-of-bounds access.
+ */
+#ifndef MLA_LOWBIT_H
+#define MLA_LOWBIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { MLA_OK = 0, MLA_EINVAL = 1, MLA_ENOTSUP = 2, MLA_EHIP = 3 };
+
+/*
+ * Cache format (Appendix C.4 "Affine group quantization", Appendix C.5
+ * "Storage layout").  Supported: d_c = 512, d_r = 64, group = 64,
+ * c_bits in {4, 2}, r_bits = 4, page_size a positive multiple of 32.
+ * The BF16 cache calls read only d_c, d_r and page_size.
+ */
+typedef struct mla_cache_format {
+    int32_t d_c;        /* content latent channels                         */
+    int32_t d_r;        /* decoupled RoPE key channels                     */
+    int32_t group;      /* quantization group (consecutive channels)       */
+    int32_t c_bits;     /* content code width                              */
+    int32_t r_bits;     /* RoPE key code width                             */
+    int32_t page_size;  /* tokens per page                                 */
+} mla_cache_format;
+
+/*
+ * Packed page layout.  A page of P tokens holds four token-major regions:
+ *   codes_c[P][d_c*c_bits/8]   content codes
+ *   codes_r[P][d_r*r_bits/8]   RoPE key codes
+ *   meta_c [P][d_c/group]{fp16 scale, fp16 zero}
+ *   meta_r [P][d_r/group]{fp16 scale, fp16 zero}
+ * and the page size is rounded up to 256 bytes; the cache is num_pages such
+ * pages back to back from a 256-byte aligned base.  Inside a byte, codes are
+ * little-endian fields: 4-bit channel 2j in bits 0-3 of byte j and 2j+1 in
+ * bits 4-7; 2-bit channel 4j+k in bits 2k..2k+1.  Token t of page p is slot
+ * p*P + t.  For d_c=512, d_r=64, P=64: 20736 bytes per page with 4-bit
+ * content (324 B/token), 12544 with 2-bit content (196 B/token).
+ * A BF16 cache page holds P rows of d_c + d_r bf16 values (73728 B at P=64).
+ * Both return -1 for an invalid format.
+ */
+int64_t mla_lowbit_page_bytes(const mla_cache_format* f);
+int64_t mla_bf16_page_bytes(const mla_cache_format* f);
+
+/*
+ * Quantize-and-append (Appendix C.4 quantizer; Appendix C.5 "Cache update and
+ * tile reuse": quantization, integer packing, slot-mapped page insertion).
+ * For each of n tokens and each group of 64 consecutive channels of both
+ * paths, in IEEE fp32 with round-half-to-even:
+ *   s = max(xmax - xmin, 1e-8) / m     (m = 2^bits - 1, a true division)
+ *   z = clip(rint(-xmin / s), 0, m)
+ *   q = clip(rint(x / s + z), 0, m)    (divide, then add: two roundings)
+ * stores q packed, fp16(s) and fp16(z) (fp16 subnormals kept).
+ *   c_kv     device, bf16 [n][c_kv_stride], first d_c used
+ *   k_rope   device, bf16 [n][k_rope_stride], first d_r used (post-RoPE key)
+ *   slot_mapping device, int64 [n]: destination slot; a negative slot skips
+ *            the token; a slot >= num_pages*page_size is skipped too
+ *   cache    device, num_pages packed pages (layout above)
+ * Codes and metadata are bit-identical to the quantizer above.  n = 0 is a
+ * no-op.  Tokens with equal slots race; the last writer is unspecified.
+ */
+int mla_lowbit_quant_append(const mla_cache_format* f,
+                            const uint16_t* c_kv, int64_t c_kv_stride,
+                            const uint16_t* k_rope, int64_t k_rope_stride,
+                            const int64_t* slot_mapping, int32_t n,
+                            void* cache, int64_t num_pages, hipStream_t stream);
+
+/*
+ * Append into the BF16 comparison cache: row = [c_kv(d_c) | k_rope(d_r)],
+ * copied bit for bit.  Arguments as for mla_lowbit_quant_append.
+ */
+int mla_bf16_append(const mla_cache_format* f,
+                    const uint16_t* c_kv, int64_t c_kv_stride,
+                    const uint16_t* k_rope, int64_t k_rope_stride,
+                    const int64_t* slot_mapping, int32_t n,
+                    void* cache, int64_t num_pages, hipStream_t stream);
+
+/*
+ * Split planner (host only; no HIP call).  Split k of sequence b covers keys
+ * [k*split_tokens, min((k+1)*split_tokens, seq_lens[b])), so sequence b has
+ * ceil(seq_lens[b] / split_tokens) splits and its partials live at indices
+ * split_indptr[b] .. split_indptr[b+1]-1 (Appendix C.5, "Global attention
+ * normalization": any partition of the keys merges to the same result).
+ *   seq_lens     host, int32 [B], each >= 1
+ *   split_indptr host, int32 [B+1], written
+ * Returns the total number of splits (>= 0), or -MLA_EINVAL / -MLA_ENOTSUP
+ * (split_tokens must be a positive multiple of 32).
+ */
+int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens,
+                        int32_t* split_indptr);
+
+/*
+ * Low-bit decode attention (Sec. 2.1, eq. mla_compact, up to the latent
+ * aggregation O_h = A_h C; value/output projections stay outside).
+ * For sequence b of length L = seq_lens[b], query token i < s_q sits at
+ * position L - s_q + i and sees keys t <= L - s_q + i (causal within the
+ * s_q new tokens).  For head h:
+ *   z_t = softmax_scale * (q_lat[b,i,h,:] . C_hat[t,:] + q_rope[b,i,h,:] . K_hat[t,:])
+ *   out[b,i,h,:] = sum_t softmax(z)_t C_hat[t,:],   lse[b,i,h] = ln sum_t e^{z_t}
+ * where C_hat, K_hat are dequantized from the packed cache with the stored
+ * fp16 scale and zero: x_hat = scale * (q - zero).
+ *   q_lat   device, bf16 [B][s_q][H][d_c]  absorbed content query
+ *   q_rope  device, bf16 [B][s_q][H][d_r]  RoPE-encoded query
+ *   cache   device, packed pages; num_pages of them
+ *   block_table device, int32 [B][max_pages_per_seq]: page id of each
+ *           page_size-token block of each sequence
+ *   seq_lens    device, int32 [B]
+ *   H       heads, a positive multiple of 16; s_q in {1, 2}
+ * Unsplit (split_tokens == 0): writes out (device, bf16 [B][s_q][H][d_c]) and,
+ *   if lse != NULL, lse (device, fp32 [B][s_q][H]); split_indptr,
+ *   num_splits and part_* are ignored.
+ * Split (split_tokens > 0): split_indptr (device, int32 [B+1]) and
+ *   num_splits = split_indptr[B] come from mla_plan_splits; writes for every
+ *   split j and row (i, h) the partials of Appendix C.5 "Global attention
+ *   normalization", in natural-log units:
+ *     part_m[j][i][h]    = max_t z_t over the split's visible keys
+ *     part_s[j][i][h]    = sum_t e^{z_t - part_m}
+ *     part_o[j][i][h][:] = sum_t e^{z_t - part_m} C_hat[t,:]
+ *   (all fp32, device; a split with no visible key gives (-inf, 0, 0)); out
+ *   and lse are not touched -- call mla_splitkv_combine.
+ * Scores and latent aggregation run as bf16 matrix products with fp32
+ * accumulation; the dequantized cache is rounded to bf16 once.
+ */
+int mla_lowbit_decode_attn(const mla_cache_format* f,
+                           const uint16_t* q_lat, const uint16_t* q_rope,
+                           const void* cache, int64_t num_pages,
+                           const int32_t* block_table, int32_t max_pages_per_seq,
+                           const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
+                           float softmax_scale,
+                           int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
+                           uint16_t* out, float* lse,
+                           float* part_m, float* part_s, float* part_o,
+                           hipStream_t stream);
+
+/*
+ * Same computation over a BF16 cache (the unquantized comparison; row layout
+ * in mla_bf16_page_bytes).  Arguments as for mla_lowbit_decode_attn.
+ */
+int mla_bf16_decode_attn(const mla_cache_format* f,
+                         const uint16_t* q_lat, const uint16_t* q_rope,
+                         const void* cache, int64_t num_pages,
+                         const int32_t* block_table, int32_t max_pages_per_seq,
+                         const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
+                         float softmax_scale,
+                         int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
+                         uint16_t* out, float* lse,
+                         float* part_m, float* part_s, float* part_o,
+                         hipStream_t stream);
+
+/*
+ * Split-KV combine (Appendix C.5, "Global attention normalization"):
+ *   m = max_j part_m[j],  s = sum_j e^{part_m[j]-m} part_s[j],
+ *   out = (sum_j e^{part_m[j]-m} part_o[j]) / s  as bf16,  lse = m + ln s
+ * over the splits j of each sequence; splits with part_m = -inf are skipped.
+ *   part_*  device, as written by the decode call (num_splits = split_indptr[B])
+ *   out     device, bf16 [B][s_q][H][d_c];  lse device fp32 [B][s_q][H] or NULL
+ * Every row must have at least one split with a visible key.
+ */
+int mla_splitkv_combine(const float* part_m, const float* part_s, const float* part_o,
+                        const int32_t* split_indptr, int32_t B, int32_t s_q, int32_t H,
+                        int32_t d_c, uint16_t* out, float* lse, hipStream_t stream);
+
+/* Human-readable name of a status code (static string). */
+const char* mla_status_str(int status);
+
+/* hipError_t of this thread's last MLA_EHIP return (0 if none). */
+int mla_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MLA_LOWBIT_H */

@@ -1,0 +1,73 @@
+// Internal interface between the host ABI (mla_abi.cpp) and the HIP kernels.
+// Not part of the public C ABI.
+#pragma once
+
+#include <cstdint>
+
+#include <hip/hip_runtime_api.h>
+
+namespace mla {
+
+// Resolved byte geometry of a packed page (layout documented in mla_lowbit.h).
+struct PageGeom {
+    int32_t page_size;      // tokens per page
+    int32_t c_bits;         // 4 or 2
+    int32_t cc_bytes;       // content code bytes per token
+    int32_t cr_bytes;       // RoPE code bytes per token
+    int32_t off_cr;         // region offsets inside a page
+    int32_t off_mc;
+    int32_t off_mr;
+    int64_t page_bytes;
+};
+
+struct AppendArgs {
+    const uint16_t* c_kv;
+    int64_t c_kv_stride;
+    const uint16_t* k_rope;
+    int64_t k_rope_stride;
+    const int64_t* slot_mapping;
+    int32_t n;
+    uint8_t* cache;
+    int64_t num_slots;      // num_pages * page_size
+    PageGeom g;
+};
+
+enum CacheKind { KIND_C4R4 = 0, KIND_C2R4 = 1, KIND_BF16 = 2 };
+
+struct DecodeArgs {
+    const uint16_t* q_lat;
+    const uint16_t* q_rope;
+    const uint8_t* cache;
+    int64_t num_pages;
+    const int32_t* block_table;
+    int32_t max_pages;
+    const int32_t* seq_lens;
+    int32_t B, s_q, H;
+    float scale_log2;       // softmax_scale * log2(e)
+    int32_t split_tokens;   // 0: unsplit
+    const int32_t* split_indptr;
+    int32_t num_work;       // B (unsplit) or total splits
+    uint16_t* out;
+    float* lse;
+    float* part_m;
+    float* part_s;
+    float* part_o;
+    PageGeom g;             // for BF16: page_size and page_bytes only
+};
+
+struct CombineArgs {
+    const float* part_m;
+    const float* part_s;
+    const float* part_o;
+    const int32_t* split_indptr;
+    int32_t B, s_q, H;
+    uint16_t* out;
+    float* lse;
+};
+
+hipError_t launch_lowbit_append(const AppendArgs& a, hipStream_t stream);
+hipError_t launch_bf16_append(const AppendArgs& a, hipStream_t stream);
+hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
+hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+
+}  // namespace mla

@@ -1,0 +1,256 @@
+// Host side of the C ABI declared in include/mla_lowbit.h: argument
+// validation, page geometry, the split planner and kernel dispatch.
+//
+// This translation unit is plain C++ (it needs only the HIP runtime API
+// types); every check below runs on the host before any HIP call is made.
+#include "mla_lowbit.h"
+
+#include <cmath>
+#include <cstdint>
+
+#include "internal.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+constexpr int32_t kDc = 512;
+constexpr int32_t kDr = 64;
+constexpr int32_t kGroup = 64;
+constexpr int32_t kTile = 32;
+
+bool aligned(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+// Structural checks shared by both cache kinds.
+int check_shape(const mla_cache_format* f) {
+    if (f == nullptr) return MLA_EINVAL;
+    if (f->d_c <= 0 || f->d_r <= 0 || f->page_size <= 0) return MLA_EINVAL;
+    if (f->page_size % 16 != 0) return MLA_EINVAL;
+    if (f->d_c != kDc || f->d_r != kDr) return MLA_ENOTSUP;
+    if (f->page_size % kTile != 0) return MLA_ENOTSUP;
+    return MLA_OK;
+}
+
+int check_lowbit_format(const mla_cache_format* f) {
+    const int st = check_shape(f);
+    if (st != MLA_OK) return st;
+    if (f->group <= 0 || f->d_c % f->group != 0 || f->d_r % f->group != 0) return MLA_EINVAL;
+    if (f->c_bits != 4 && f->c_bits != 2) return MLA_EINVAL;
+    if (f->r_bits != 4) return MLA_EINVAL;
+    if (f->group != kGroup) return MLA_ENOTSUP;
+    return MLA_OK;
+}
+
+mla::PageGeom lowbit_geom(const mla_cache_format* f) {
+    mla::PageGeom g{};
+    const int32_t P = f->page_size;
+    g.page_size = P;
+    g.c_bits = f->c_bits;
+    g.cc_bytes = f->d_c * f->c_bits / 8;
+    g.cr_bytes = f->d_r * f->r_bits / 8;
+    g.off_cr = P * g.cc_bytes;
+    g.off_mc = g.off_cr + P * g.cr_bytes;
+    g.off_mr = g.off_mc + P * (f->d_c / f->group) * 4;
+    const int64_t end = g.off_mr + static_cast<int64_t>(P) * (f->d_r / f->group) * 4;
+    g.page_bytes = (end + 255) / 256 * 256;
+    return g;
+}
+
+mla::PageGeom bf16_geom(const mla_cache_format* f) {
+    mla::PageGeom g{};
+    g.page_size = f->page_size;
+    g.page_bytes = static_cast<int64_t>(f->page_size) * (f->d_c + f->d_r) * 2;
+    return g;
+}
+
+int hip_status(hipError_t e) {
+    if (e == hipSuccess) return MLA_OK;
+    g_last_hip_error = static_cast<int>(e);
+    return MLA_EHIP;
+}
+
+int check_append(const uint16_t* c_kv, int64_t c_kv_stride, const uint16_t* k_rope, int64_t k_rope_stride,
+                 const int64_t* slot_mapping, int32_t n, const void* cache, int64_t num_pages) {
+    if (n < 0 || num_pages < 0) return MLA_EINVAL;
+    if (n == 0) return MLA_OK;
+    if (c_kv == nullptr || k_rope == nullptr || slot_mapping == nullptr || cache == nullptr) return MLA_EINVAL;
+    if (num_pages == 0) return MLA_EINVAL;
+    if (c_kv_stride < kDc || k_rope_stride < kDr) return MLA_EINVAL;
+    if (!aligned(cache, 256)) return MLA_EINVAL;
+    // 16-byte vector loads of 8 channels
+    if (c_kv_stride % 8 != 0 || k_rope_stride % 8 != 0 || !aligned(c_kv, 16) || !aligned(k_rope, 16))
+        return MLA_ENOTSUP;
+    return MLA_OK;
+}
+
+int append_common(const mla_cache_format* f, bool lowbit, const uint16_t* c_kv, int64_t c_kv_stride,
+                  const uint16_t* k_rope, int64_t k_rope_stride, const int64_t* slot_mapping, int32_t n,
+                  void* cache, int64_t num_pages, hipStream_t stream) {
+    int st = lowbit ? check_lowbit_format(f) : check_shape(f);
+    if (st != MLA_OK) return st;
+    st = check_append(c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, n, cache, num_pages);
+    if (st != MLA_OK || n == 0) return st;
+    mla::AppendArgs a{};
+    a.c_kv = c_kv;
+    a.c_kv_stride = c_kv_stride;
+    a.k_rope = k_rope;
+    a.k_rope_stride = k_rope_stride;
+    a.slot_mapping = slot_mapping;
+    a.n = n;
+    a.cache = static_cast<uint8_t*>(cache);
+    a.num_slots = num_pages * f->page_size;
+    a.g = lowbit ? lowbit_geom(f) : bf16_geom(f);
+    return hip_status(lowbit ? mla::launch_lowbit_append(a, stream) : mla::launch_bf16_append(a, stream));
+}
+
+int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat, const uint16_t* q_rope,
+                  const void* cache, int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
+                  const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H, float softmax_scale,
+                  int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits, uint16_t* out,
+                  float* lse, float* part_m, float* part_s, float* part_o, hipStream_t stream) {
+    int st = lowbit ? check_lowbit_format(f) : check_shape(f);
+    if (st != MLA_OK) return st;
+    if (B < 0 || num_pages < 0 || max_pages_per_seq <= 0 || split_tokens < 0) return MLA_EINVAL;
+    if (s_q != 1 && s_q != 2) return MLA_EINVAL;
+    if (H <= 0 || H % 16 != 0) return MLA_EINVAL;
+    if (!std::isfinite(softmax_scale)) return MLA_EINVAL;
+    if (q_lat == nullptr || q_rope == nullptr || cache == nullptr || block_table == nullptr || seq_lens == nullptr)
+        return MLA_EINVAL;
+    if (num_pages == 0) return MLA_EINVAL;
+    if (!aligned(cache, 256)) return MLA_EINVAL;
+    if (!aligned(q_lat, 16) || !aligned(q_rope, 16)) return MLA_ENOTSUP;
+    if (split_tokens == 0) {
+        if (out == nullptr) return MLA_EINVAL;
+        if (!aligned(out, 8)) return MLA_ENOTSUP;
+    } else {
+        if (split_indptr == nullptr || part_m == nullptr || part_s == nullptr || part_o == nullptr || num_splits < 0)
+            return MLA_EINVAL;
+        if (split_tokens % kTile != 0) return MLA_ENOTSUP;
+        if (!aligned(part_o, 16)) return MLA_ENOTSUP;
+    }
+    if (B == 0) return MLA_OK;
+    mla::DecodeArgs a{};
+    a.q_lat = q_lat;
+    a.q_rope = q_rope;
+    a.cache = static_cast<const uint8_t*>(cache);
+    a.num_pages = num_pages;
+    a.block_table = block_table;
+    a.max_pages = max_pages_per_seq;
+    a.seq_lens = seq_lens;
+    a.B = B;
+    a.s_q = s_q;
+    a.H = H;
+    a.scale_log2 = softmax_scale * 1.4426950408889634f;
+    a.split_tokens = split_tokens;
+    a.split_indptr = split_indptr;
+    a.num_work = split_tokens == 0 ? B : num_splits;
+    a.out = out;
+    a.lse = lse;
+    a.part_m = part_m;
+    a.part_s = part_s;
+    a.part_o = part_o;
+    a.g = lowbit ? lowbit_geom(f) : bf16_geom(f);
+    const mla::CacheKind kind = !lowbit ? mla::KIND_BF16 : (f->c_bits == 4 ? mla::KIND_C4R4 : mla::KIND_C2R4);
+    return hip_status(mla::launch_decode(kind, a, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t mla_lowbit_page_bytes(const mla_cache_format* f) {
+    if (check_lowbit_format(f) != MLA_OK) return -1;
+    return lowbit_geom(f).page_bytes;
+}
+
+int64_t mla_bf16_page_bytes(const mla_cache_format* f) {
+    if (check_shape(f) != MLA_OK) return -1;
+    return bf16_geom(f).page_bytes;
+}
+
+int mla_lowbit_quant_append(const mla_cache_format* f, const uint16_t* c_kv, int64_t c_kv_stride,
+                            const uint16_t* k_rope, int64_t k_rope_stride, const int64_t* slot_mapping,
+                            int32_t n, void* cache, int64_t num_pages, hipStream_t stream) {
+    return append_common(f, true, c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, n, cache, num_pages,
+                         stream);
+}
+
+int mla_bf16_append(const mla_cache_format* f, const uint16_t* c_kv, int64_t c_kv_stride,
+                    const uint16_t* k_rope, int64_t k_rope_stride, const int64_t* slot_mapping, int32_t n,
+                    void* cache, int64_t num_pages, hipStream_t stream) {
+    return append_common(f, false, c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, n, cache, num_pages,
+                         stream);
+}
+
+int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens, int32_t* split_indptr) {
+    if (seq_lens == nullptr || split_indptr == nullptr || B < 0 || split_tokens <= 0) return -MLA_EINVAL;
+    if (split_tokens % kTile != 0) return -MLA_ENOTSUP;
+    int64_t total = 0;
+    split_indptr[0] = 0;
+    for (int32_t b = 0; b < B; ++b) {
+        if (seq_lens[b] < 1) return -MLA_EINVAL;
+        total += (static_cast<int64_t>(seq_lens[b]) + split_tokens - 1) / split_tokens;
+        if (total > INT32_MAX) return -MLA_EINVAL;
+        split_indptr[b + 1] = static_cast<int32_t>(total);
+    }
+    return static_cast<int32_t>(total);
+}
+
+int mla_lowbit_decode_attn(const mla_cache_format* f, const uint16_t* q_lat, const uint16_t* q_rope,
+                           const void* cache, int64_t num_pages, const int32_t* block_table,
+                           int32_t max_pages_per_seq, const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
+                           float softmax_scale, int32_t split_tokens, const int32_t* split_indptr,
+                           int32_t num_splits, uint16_t* out, float* lse, float* part_m, float* part_s,
+                           float* part_o, hipStream_t stream) {
+    return decode_common(f, true, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
+                         s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
+                         part_o, stream);
+}
+
+int mla_bf16_decode_attn(const mla_cache_format* f, const uint16_t* q_lat, const uint16_t* q_rope,
+                         const void* cache, int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
+                         const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H, float softmax_scale,
+                         int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits, uint16_t* out,
+                         float* lse, float* part_m, float* part_s, float* part_o, hipStream_t stream) {
+    return decode_common(f, false, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
+                         s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
+                         part_o, stream);
+}
+
+int mla_splitkv_combine(const float* part_m, const float* part_s, const float* part_o, const int32_t* split_indptr,
+                        int32_t B, int32_t s_q, int32_t H, int32_t d_c, uint16_t* out, float* lse,
+                        hipStream_t stream) {
+    if (B < 0 || d_c <= 0) return MLA_EINVAL;
+    if (s_q != 1 && s_q != 2) return MLA_EINVAL;
+    if (H <= 0 || H % 16 != 0) return MLA_EINVAL;
+    if (part_m == nullptr || part_s == nullptr || part_o == nullptr || split_indptr == nullptr || out == nullptr)
+        return MLA_EINVAL;
+    if (d_c != kDc) return MLA_ENOTSUP;
+    if (!aligned(part_o, 16) || !aligned(out, 8)) return MLA_ENOTSUP;
+    if (B == 0) return MLA_OK;
+    mla::CombineArgs a{};
+    a.part_m = part_m;
+    a.part_s = part_s;
+    a.part_o = part_o;
+    a.split_indptr = split_indptr;
+    a.B = B;
+    a.s_q = s_q;
+    a.H = H;
+    a.out = out;
+    a.lse = lse;
+    return hip_status(mla::launch_combine(a, stream));
+}
+
+const char* mla_status_str(int status) {
+    switch (status) {
+        case MLA_OK: return "MLA_OK";
+        case MLA_EINVAL: return "MLA_EINVAL: invalid argument";
+        case MLA_ENOTSUP: return "MLA_ENOTSUP: shape or alignment not supported";
+        case MLA_EHIP: return "MLA_EHIP: HIP launch failed";
+        default: return "MLA: unknown status";
+    }
+}
+
+int mla_last_hip_error(void) { return g_last_hip_error; }
+
+}  // extern "C"

@@ -1,0 +1,143 @@
+// Quantize-and-append writer for the packed dual-path cache, and the plain
+// BF16 append used by the unquantized comparison cache.
+//
+// Quantizer: Appendix C.4, "Affine group quantization" -- per token, groups of
+// 64 consecutive channels, m = 2^b - 1,
+//   s = max(xmax - xmin, 1e-8) / m,  z = clip(rint(-xmin / s), 0, m),
+//   q = clip(rint(x / s + z), 0, m),
+// round-half-to-even, constant groups not special-cased; the stored fp16
+// scale and zero are what attention dequantizes with.  Every step is one IEEE
+// fp32 operation in that order: this file is built with
+// -ffp-contract=off and correctly rounded fp32 division, so the codes and
+// fp16 metadata are bit-identical to any IEEE implementation of the formula.
+//
+// Work split: 8 lanes per group of 64 channels, each lane owning 8 channels
+// (one 16-byte load); min/max are reduced across the 8 lanes.  A token has 9
+// groups: 8 content groups (d_c = 512) and one RoPE-key group (d_r = 64).
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace mla {
+namespace {
+
+constexpr int kGroup = 64;
+constexpr int kLanesPerGroup = 8;
+constexpr int kGroupsPerToken = 9;
+constexpr int kThreads = 256;
+
+__device__ inline void widen_bf16x8(const uint4 raw, float x[8]) {
+    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        x[2 * i] = __uint_as_float(w[i] << 16);
+        x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+}
+
+__device__ inline uint16_t f16_bits(float v) {
+    const _Float16 h = static_cast<_Float16>(v);   // v_cvt_f16_f32: round-half-to-even, subnormals kept
+    return __builtin_bit_cast(uint16_t, h);
+}
+
+template <int CBITS>
+__global__ __launch_bounds__(kThreads) void lowbit_append_kernel(AppendArgs a) {
+    const int64_t tid = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    const int64_t gid = tid / kLanesPerGroup;           // the 8 lanes of a group share gid
+    const int lig = static_cast<int>(threadIdx.x % kLanesPerGroup);
+    if (gid >= static_cast<int64_t>(a.n) * kGroupsPerToken) return;
+    const int64_t token = gid / kGroupsPerToken;
+    const int g = static_cast<int>(gid % kGroupsPerToken);
+    const int64_t slot = a.slot_mapping[token];
+    if (slot < 0 || slot >= a.num_slots) return;        // skipped token
+
+    const bool rope = (g == kGroupsPerToken - 1);
+    const uint16_t* src = rope ? a.k_rope + token * a.k_rope_stride + lig * 8
+                               : a.c_kv + token * a.c_kv_stride + g * kGroup + lig * 8;
+    float x[8];
+    widen_bf16x8(*reinterpret_cast<const uint4*>(src), x);
+
+    float lo = x[0], hi = x[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) {
+        lo = fminf(lo, x[i]);
+        hi = fmaxf(hi, x[i]);
+    }
+#pragma unroll
+    for (int d = 1; d < kLanesPerGroup; d <<= 1) {
+        lo = fminf(lo, __shfl_xor(lo, d, kLanesPerGroup));
+        hi = fmaxf(hi, __shfl_xor(hi, d, kLanesPerGroup));
+    }
+
+    const int bits = rope ? 4 : CBITS;
+    const float m = static_cast<float>((1 << bits) - 1);
+    const float s = fmaxf(hi - lo, 1e-8f) / m;
+    // integer zero-point in [0, m]; "+ 0.0f" turns a -0 from rint into +0
+    const float z = fminf(fmaxf(rintf(-lo / s), 0.0f), m) + 0.0f;
+
+    uint32_t packed = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const float t = __fadd_rn(__fdiv_rn(x[i], s), z);
+        const uint32_t q = static_cast<uint32_t>(fminf(fmaxf(rintf(t), 0.0f), m));
+        packed |= q << (bits * i);
+    }
+
+    const int64_t page = slot / a.g.page_size;
+    const int64_t off = slot % a.g.page_size;
+    uint8_t* base = a.cache + page * a.g.page_bytes;
+    if (rope) {
+        *reinterpret_cast<uint32_t*>(base + a.g.off_cr + off * a.g.cr_bytes + lig * 4) = packed;
+    } else if (CBITS == 4) {
+        *reinterpret_cast<uint32_t*>(base + off * a.g.cc_bytes + g * 32 + lig * 4) = packed;
+    } else {
+        *reinterpret_cast<uint16_t*>(base + off * a.g.cc_bytes + g * 16 + lig * 2) =
+            static_cast<uint16_t>(packed);
+    }
+    if (lig == 0) {
+        const uint32_t meta = static_cast<uint32_t>(f16_bits(s)) | (static_cast<uint32_t>(f16_bits(z)) << 16);
+        uint8_t* mp = rope ? base + a.g.off_mr + off * 4 : base + a.g.off_mc + off * 32 + g * 4;
+        *reinterpret_cast<uint32_t*>(mp) = meta;
+    }
+}
+
+// BF16 comparison cache: row = [c_kv (512) | k_rope (64)] bf16; 72 lanes per
+// token, 16 bytes each.
+__global__ __launch_bounds__(kThreads) void bf16_append_kernel(AppendArgs a) {
+    constexpr int kLanesPerToken = 72;
+    const int64_t tid = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    const int64_t token = tid / kLanesPerToken;
+    const int lane = static_cast<int>(tid % kLanesPerToken);
+    if (token >= a.n) return;
+    const int64_t slot = a.slot_mapping[token];
+    if (slot < 0 || slot >= a.num_slots) return;
+    const uint16_t* src = lane < 64 ? a.c_kv + token * a.c_kv_stride + lane * 8
+                                    : a.k_rope + token * a.k_rope_stride + (lane - 64) * 8;
+    const int64_t page = slot / a.g.page_size;
+    const int64_t off = slot % a.g.page_size;
+    uint8_t* dst = a.cache + page * a.g.page_bytes + off * 1152 + lane * 16;
+    *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src);
+}
+
+}  // namespace
+
+hipError_t launch_lowbit_append(const AppendArgs& a, hipStream_t stream) {
+    if (a.n == 0) return hipSuccess;
+    const int64_t threads = static_cast<int64_t>(a.n) * kGroupsPerToken * kLanesPerGroup;
+    const dim3 grid(static_cast<unsigned>((threads + kThreads - 1) / kThreads));
+    if (a.g.c_bits == 4)
+        hipLaunchKernelGGL(lowbit_append_kernel<4>, grid, dim3(kThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL(lowbit_append_kernel<2>, grid, dim3(kThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_bf16_append(const AppendArgs& a, hipStream_t stream) {
+    if (a.n == 0) return hipSuccess;
+    const int64_t threads = static_cast<int64_t>(a.n) * 72;
+    const dim3 grid(static_cast<unsigned>((threads + kThreads - 1) / kThreads));
+    hipLaunchKernelGGL(bf16_append_kernel, grid, dim3(kThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace mla

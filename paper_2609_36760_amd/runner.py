@@ -1,0 +1,157 @@
+"""Device-side setup and decode steps for a synthetic workload.
+
+``DecodeRun`` owns the device buffers of one cache layer: the paged cache
+(packed low-bit or BF16), page table, sequence lengths, queries, the split
+plan and the partial/output buffers.  Building it prefills every sequence's
+history through the library's own writer; ``step()`` then runs one pass of
+the decode hot path: append the step's new tokens with the writer, decode
+attention over the cache, and (when split) the split-KV combine.  Only the
+binding is called; no result is computed on the host.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+from . import _binding as mb
+from . import synthetic as syn
+
+
+def _dev(a, device):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
+class DecodeRun:
+    def __init__(self, w: syn.Workload, layer: int = 0, kind: str = "lowbit", device: str = "cuda",
+                 split_tokens: int | None = None, seq_lens=None, threads: int = 16, prefill: bool = True,
+                 token_cache: dict | None = None):
+        if kind not in ("lowbit", "bf16"):
+            raise ValueError(kind)
+        self.w, self.layer, self.kind, self.device = w, layer, kind, device
+        self.c_bits, self.r_bits = w.layers[layer]
+        self.fmt = mb.cache_format(c_bits=self.c_bits)
+        self.B, self.H, self.s_q = w.B, w.H, w.s_q
+        self.tau = w.tau
+        lens = syn.seq_lens(w) if seq_lens is None else np.asarray(seq_lens, np.int32)
+        self.lens = lens
+        bt, num_pages = syn.page_table(w, lens, layer)
+        self.block_table_host = bt
+        self.num_pages = num_pages
+        self.page_bytes = (mb.mla_lowbit_page_bytes(self.fmt) if kind == "lowbit"
+                           else mb.mla_bf16_page_bytes(self.fmt))
+        self.cache = torch.empty(num_pages * self.page_bytes, dtype=torch.uint8, device=device)
+        self.block_table = _dev(bt, device)
+        self.seq_lens = _dev(lens, device)
+        ql, qr = syn.queries(w, layer)
+        self.q_lat = _dev(ql.view(np.int16), device)
+        self.q_rope = _dev(qr.view(np.int16), device)
+        self.split_tokens = w.split_tokens if split_tokens is None else split_tokens
+        if self.split_tokens:
+            indptr, total = mb.mla_plan_splits(lens, self.split_tokens)
+            self.split_indptr_host = indptr
+            self.split_indptr = _dev(indptr, device)
+            self.num_splits = total
+            R = self.s_q * self.H
+            self.part_m = torch.empty(total * R, dtype=torch.float32, device=device)
+            self.part_s = torch.empty(total * R, dtype=torch.float32, device=device)
+            self.part_o = torch.empty(total * R * 512, dtype=torch.float32, device=device)
+        else:
+            self.split_indptr = self.part_m = self.part_s = self.part_o = None
+            self.num_splits = 0
+        self.out = torch.empty((self.B, self.s_q, self.H, 512), dtype=torch.int16, device=device)
+        self.lse = torch.empty((self.B, self.s_q, self.H), dtype=torch.float32, device=device)
+        # the step's new tokens (the last s_q positions of every sequence)
+        new_c, new_k, new_slots = [], [], []
+        for b in range(self.B):
+            L = int(lens[b])
+            c, k = syn.sequence_tokens(w, layer, b, L, start=L - self.s_q)
+            new_c.append(c)
+            new_k.append(k)
+            new_slots.append(syn.slots_of(bt[b], np.arange(L - self.s_q, L)))
+        self.new_c = _dev(np.concatenate(new_c).view(np.int16), device)
+        self.new_k = _dev(np.concatenate(new_k).view(np.int16), device)
+        self.new_slots = _dev(np.concatenate(new_slots), device)
+        self.token_cache = token_cache
+        if prefill:
+            self._prefill(threads)
+
+    def _append(self, c, k, slots):
+        fn = mb.mla_lowbit_quant_append if self.kind == "lowbit" else mb.mla_bf16_append
+        fn(self.fmt, c, k, slots, self.cache, self.num_pages)
+
+    def _prefill(self, threads: int, chunk_tokens: int = 1 << 20):
+        """Write every sequence's history (all but the step's s_q new tokens)."""
+        pend_c, pend_k, pend_s, pend_n = [], [], [], 0
+
+        def flush():
+            nonlocal pend_c, pend_k, pend_s, pend_n
+            if pend_n:
+                self._append(_dev(np.concatenate(pend_c).view(np.int16), self.device),
+                             _dev(np.concatenate(pend_k).view(np.int16), self.device),
+                             _dev(np.concatenate(pend_s), self.device))
+                torch.cuda.synchronize()
+            pend_c, pend_k, pend_s, pend_n = [], [], [], 0
+
+        hist = np.maximum(self.lens.astype(np.int64) - self.s_q, 0)
+        tc = self.token_cache
+        key = (self.w.name, self.layer)
+        if tc is not None and key in tc:
+            source = ((b, c, k) for b, (c, k) in enumerate(tc[key]))
+        else:
+            source = syn.generate_sequences(self.w, self.layer, hist, threads=threads)
+            if tc is not None:
+                tc[key] = []
+        for b, c, k in source:
+            if tc is not None and len(tc[key]) == b:
+                tc[key].append((c, k))
+            n = int(hist[b])
+            if n == 0:
+                continue
+            pend_c.append(c)
+            pend_k.append(k)
+            pend_s.append(syn.slots_of(self.block_table_host[b], np.arange(n)))
+            pend_n += n
+            if pend_n >= chunk_tokens:
+                flush()
+        flush()
+
+    def append_new_tokens(self, stream=None):
+        fn = mb.mla_lowbit_quant_append if self.kind == "lowbit" else mb.mla_bf16_append
+        fn(self.fmt, self.new_c, self.new_k, self.new_slots, self.cache, self.num_pages, stream=stream)
+
+    def attend(self, stream=None):
+        """Decode attention (+ combine when split); results in ``out``/``lse``."""
+        fn = mb.mla_lowbit_decode_attn if self.kind == "lowbit" else mb.mla_bf16_decode_attn
+        fn(self.fmt, self.q_lat, self.q_rope, self.cache, self.num_pages, self.block_table, self.seq_lens,
+           self.s_q, self.H, self.tau, split_tokens=self.split_tokens, split_indptr=self.split_indptr,
+           num_splits=self.num_splits, out=self.out, lse=self.lse, part_m=self.part_m,
+           part_s=self.part_s, part_o=self.part_o, stream=stream)
+        if self.split_tokens:
+            mb.mla_splitkv_combine(self.part_m, self.part_s, self.part_o, self.split_indptr, self.B, self.s_q,
+                                   self.H, self.out, self.lse, stream=stream)
+
+    def step(self, stream=None):
+        self.append_new_tokens(stream)
+        self.attend(stream)
+
+    # ---- accounting -------------------------------------------------------
+    def visible_pairs(self) -> int:
+        """Number of valid (query row, key) pairs of one step."""
+        L = self.lens.astype(np.int64)
+        return int(self.H * sum(int(l) - self.s_q + 1 + i for l in L for i in range(self.s_q)))
+
+    def flops(self) -> int:
+        """Algorithmic flops of one step: 2 * (576 + 512) per valid (row, key) pair."""
+        return 2 * (576 + 512) * self.visible_pairs()
+
+    def cache_token_bytes(self) -> int:
+        if self.kind == "bf16":
+            return 1152
+        return (512 * self.c_bits + 64 * self.r_bits) // 8 + 9 * 4
+
+    def cache_bytes_read(self) -> int:
+        """Cache bytes attention reads per step (every key once per 128-row block)."""
+        row_blocks = math.ceil(self.s_q * self.H / 128)
+        return int(self.lens.astype(np.int64).sum()) * self.cache_token_bytes() * row_blocks

@@ -1,0 +1,111 @@
+"""Host-side checks of the C ABI (CPU only; no GPU work is launched).
+
+The library must load, export every function include/mla_lowbit.h declares,
+report the page geometry of the documented layout, plan splits as documented,
+and reject invalid arguments on the host before any HIP call.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mla_lowbit.h")
+
+
+@pytest.fixture(scope="module")
+def mb():
+    from paper_2609_36760_amd import _binding
+    if not os.path.exists(_binding.LIB_PATH):
+        pytest.skip("libmla_lowbit.so not built (run __graft_entry__.build())")
+    _binding.library()
+    return _binding
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mla_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(mb):
+    names = declared_functions()
+    assert len(names) == 10
+    lib = ctypes.CDLL(mb.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(mb.SYMBOLS) == names
+
+
+def test_page_geometry(mb):
+    assert mb.mla_lowbit_page_bytes(mb.cache_format(c_bits=4)) == 20736
+    assert mb.mla_lowbit_page_bytes(mb.cache_format(c_bits=2)) == 12544
+    assert mb.mla_bf16_page_bytes(mb.cache_format()) == 73728
+    assert mb.mla_lowbit_page_bytes(mb.cache_format(c_bits=4, page_size=32)) == 10496   # 10368 -> 256-aligned
+    assert mb.mla_lowbit_page_bytes(mb.cache_format(c_bits=3)) == -1
+    assert mb.mla_lowbit_page_bytes(mb.cache_format(page_size=48)) == -1
+    assert mb.mla_bf16_page_bytes(mb.cache_format(d_c=256)) == -1
+
+
+def test_planner(mb):
+    lens = np.array([1, 2048, 2049, 131072, 4095], np.int32)
+    indptr, total = mb.mla_plan_splits(lens, 2048)
+    assert indptr.tolist() == [0, 1, 2, 4, 68, 70]
+    assert total == 70
+    with pytest.raises(mb.MlaError):
+        mb.mla_plan_splits(lens, 100)               # not a multiple of 32
+    with pytest.raises(mb.MlaError):
+        mb.mla_plan_splits(np.array([0], np.int32), 64)
+
+
+def _decode_status(mb, **over):
+    lib = mb.library()
+    fmt = over.pop("fmt", mb.cache_format())
+    args = dict(q_lat=16, q_rope=16, cache=256, num_pages=4, block_table=16, max_pages=2, seq_lens=16,
+                B=1, s_q=1, H=128, scale=0.07, split_tokens=0, split_indptr=None, num_splits=0, out=16,
+                lse=None, part_m=None, part_s=None, part_o=None)
+    args.update(over)
+    return lib.mla_lowbit_decode_attn(ctypes.byref(fmt), args["q_lat"], args["q_rope"], args["cache"],
+                                      args["num_pages"], args["block_table"], args["max_pages"], args["seq_lens"],
+                                      args["B"], args["s_q"], args["H"], args["scale"], args["split_tokens"],
+                                      args["split_indptr"], args["num_splits"], args["out"], args["lse"],
+                                      args["part_m"], args["part_s"], args["part_o"], None)
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(q_lat=None), 1), (dict(cache=None), 1), (dict(out=None), 1), (dict(s_q=3), 1), (dict(s_q=0), 1),
+    (dict(H=24), 1), (dict(H=0), 1), (dict(B=-1), 1), (dict(max_pages=0), 1), (dict(num_pages=0), 1),
+    (dict(cache=272), 1), (dict(q_lat=8), 2), (dict(scale=float("inf")), 1),
+    (dict(split_tokens=64, split_indptr=16, part_m=16, part_s=16, part_o=None), 1),
+    (dict(split_tokens=48, split_indptr=16, part_m=16, part_s=16, part_o=16), 2),
+    (dict(fmt="c3"), 1), (dict(fmt="r2"), 1), (dict(fmt="g32"), 2), (dict(fmt="p48"), 2), (dict(fmt="p40"), 1), (dict(fmt="dc256"), 2),
+    (dict(B=0), 0),
+])
+def test_decode_rejects_before_any_hip_call(mb, over, status):
+    fmts = {"c3": mb.cache_format(c_bits=3), "r2": mb.cache_format(r_bits=2),
+            "g32": mb.cache_format(group=32), "p48": mb.cache_format(page_size=48),
+            "p40": mb.cache_format(page_size=40),
+            "dc256": mb.cache_format(d_c=256)}
+    if "fmt" in over:
+        over = dict(over, fmt=fmts[over["fmt"]])
+    assert _decode_status(mb, **over) == status
+    assert mb.mla_status_str(status).startswith("MLA_")
+
+
+def test_append_and_combine_validation(mb):
+    lib = mb.library()
+    fmt = mb.cache_format()
+    f = ctypes.byref(fmt)
+    assert lib.mla_lowbit_quant_append(f, None, 512, 16, 64, 16, 4, 256, 1, None) == 1
+    assert lib.mla_lowbit_quant_append(f, 16, 500, 16, 64, 16, 4, 256, 1, None) == 1     # stride < 512
+    assert lib.mla_lowbit_quant_append(f, 16, 516, 16, 64, 16, 4, 256, 1, None) == 2     # stride % 8
+    assert lib.mla_lowbit_quant_append(f, 18, 512, 16, 64, 16, 4, 256, 1, None) == 2     # misaligned rows
+    assert lib.mla_lowbit_quant_append(f, 16, 512, 16, 64, 16, -1, 256, 1, None) == 1
+    assert lib.mla_lowbit_quant_append(f, None, 512, None, 64, None, 0, None, 0, None) == 0   # n = 0
+    assert lib.mla_bf16_append(f, 16, 512, 16, 64, 16, 4, 256, 0, None) == 1             # no pages
+    assert lib.mla_splitkv_combine(16, 16, 16, 16, 1, 3, 128, 512, 16, None, None) == 1
+    assert lib.mla_splitkv_combine(16, 16, 16, 16, 1, 1, 128, 256, 16, None, None) == 2
+    assert lib.mla_splitkv_combine(16, 16, 16, 16, 0, 1, 128, 512, 16, None, None) == 0
+    assert lib.mla_last_hip_error() == 0
