@@ -142,6 +142,7 @@ int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens
  *           page_size-token block of each sequence
  *   seq_lens    device, int32 [B]
  *   H       heads, a positive multiple of 16; s_q in {1, 2}
+ *   B = 0 is a no-op after the scalar arguments are checked (pointers may be NULL)
  * Unsplit (split_tokens == 0): writes out (device, bf16 [B][s_q][H][d_c]) and,
  *   if lse != NULL, lse (device, fp32 [B][s_q][H]); split_indptr,
  *   num_splits and part_* are ignored.
@@ -190,7 +191,7 @@ int mla_bf16_decode_attn(const mla_cache_format* f,
  * over the splits j of each sequence; splits with part_m = -inf are skipped.
  *   part_*  device, as written by the decode call (num_splits = split_indptr[B])
  *   out     device, bf16 [B][s_q][H][d_c];  lse device fp32 [B][s_q][H] or NULL
- * Every row must have at least one split with a visible key.
+ * Every row must have at least one split with a visible key.  B = 0 is a no-op.
  */
 int mla_splitkv_combine(const float* part_m, const float* part_s, const float* part_o,
                         const int32_t* split_indptr, int32_t B, int32_t s_q, int32_t H,

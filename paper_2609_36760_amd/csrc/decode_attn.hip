@@ -3,39 +3,47 @@
 // Computes, for every query row r = (query token i, head h) of a sequence,
 //   z_t = tau * (q_lat[r] . C_hat[t] + q_rope[r] . K_hat[t])      (Sec. 2.1,
 //   out[r] = softmax(z) C_hat,  lse[r] = ln sum_t e^{z_t}          eq. mla_compact)
-// straight from the packed paged cache: each tile of 32 tokens is gathered
-// from its page, unpacked and dequantized (x_hat = scale * (q - zero), stored
-// fp16 metadata; Appendix C.4) once into LDS as bf16, and that single
+// straight from the packed paged cache.  Each tile of 32 tokens is gathered
+// from its page, unpacked and dequantized (x_hat = scale * (q - zero) with the
+// stored fp16 metadata; Appendix C.4) once into LDS, and that single
 // reconstructed tile feeds both the score product and the latent aggregation
 // (Appendix C.5, "Cache update and tile reuse").  Partials over a key split
 // are the (max, sum, weighted sum) of Appendix C.5 "Global attention
 // normalization".
 //
-// Mapping (one workgroup = 4 waves = 256 threads, one per CU):
-//   * the workgroup owns one (sequence or key split, block of 128 rows);
-//     wave w owns rows 32w..32w+31 of the block;
-//   * the wave keeps its 32 query rows (576 channels) in registers as the B
-//     operand of v_mfma_f32_32x32x16_bf16 and computes the transposed score
-//     tile S^T[token][row] = K_tile . Q^T (M = 32 tokens, N = 32 rows,
-//     K = 576), so every lane holds the scores of ONE row: the online
-//     softmax needs no cross-lane reduction except one swap with lane ^ 32;
-//   * the output is accumulated transposed, O^T[channel][row] += V^T . P^T
-//     (M = 512 channels in 16 tiles, N = 32 rows, K = 32 tokens), the
-//     probabilities coming straight from the score registers; the rescale
-//     of the running output is one per-lane scalar;
-//   * the dequantized tile is written to LDS twice: token-major (QK operand,
-//     16 contiguous bytes per lane) and channel-major with tokens permuted to
-//     match the score register layout (PV operand, 16 contiguous bytes per
-//     lane);
-//   * two LDS stages: tile i+1 is unpacked into one while tile i is consumed
-//     from the other; packed bytes of tile i+2 are already in flight.
-//   * no running rescale of the output: every row fixes its exponential
-//     reference at the maximum of the first tile it sees and keeps it; the
-//     result is exact for any reference (all terms share it).  If a later
-//     tile exceeds the reference by more than 2^64 -- far below fp32
-//     overflow of the sums -- the row's reference is raised and the whole
-//     workgroup restarts the split (a block-uniform decision through LDS).
-//     This keeps the 256 accumulator registers out of any branch.
+// Workgroup = 4 waves = 256 threads, one per CU; it owns one (sequence or key
+// split, block of 128 query rows); wave w owns rows 32w..32w+31.
+//
+// Data path per 32-token tile:
+//   1. the tile's packed bytes (codes and metadata regions of the page; raw
+//      bf16 rows for the BF16 cache) are copied HBM -> LDS by direct-to-LDS
+//      loads (global_load_lds_dwordx4), two tiles ahead of use;
+//   2. all 256 threads unpack and dequantize them with packed fp16 math into
+//      one token-major fp16 tile [32][576] (rows padded by 32 bytes to spread
+//      LDS banks); invalid tokens become zeros;
+//   3. scores: every wave computes S^T[token][row] = K_tile . Q^T with
+//      v_mfma_f32_32x32x16_f16 (M = 32 tokens, N = its 32 rows, K = 576), the
+//      rows' queries held in registers as the B operand.  A lane then holds
+//      the 16 scores of one row, the other 16 live in lane ^ 32;
+//   4. softmax weights p = 2^(x - ref) in fp32, rounded to fp16;
+//   5. latent aggregation O^T[channel][row] += V^T . P^T (M = 512 channels in
+//      16 tiles, N = 32 rows, K = 32 tokens): the V^T operand is read from the
+//      SAME token-major tile with ds_read_b64_tr_b16 (transposing loads), the
+//      P^T operand comes straight from the score registers.
+//
+// The fp16 datapath (instead of bf16) keeps the reconstructed latents and the
+// probabilities to 11 significant bits; the result is accumulated in fp32 and
+// rounded once to the bf16 output.  Inputs must lie within the fp16 range
+// (|q|, |x_hat| < 65504), which also bounds the reference slack below.
+//
+// Online softmax with a lazy rescale: every row keeps a running reference
+// (its maximum so far, log2 units) and the weights p = 2^(x - ref) stay below
+// 2^10 (well inside fp16).  Only when a tile's maximum exceeds the reference by
+// more than that slack does the wave rescale its rows' accumulators -- rare
+// after the first tiles.  The rescale reads and writes the accumulator
+// registers in place (the compiler would otherwise stage all 256 of them
+// through vector registers at the branch).  The true maximum is tracked
+// separately for the split partials.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -45,8 +53,13 @@
 namespace mla {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef const __attribute__((address_space(1))) void gbl_void;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
@@ -55,159 +68,199 @@ constexpr int kTile = 32;                       // tokens per tile
 constexpr int kDc = 512;
 constexpr int kDk = 576;                        // d_c + d_r
 constexpr int kKSteps = kDk / 16;               // 36 MFMA k-steps for the scores
-constexpr int kKRow = kDk * 2 + 16;             // bytes per token row, token-major tile (padded)
-constexpr int kVRow = kTile * 2 + 16;           // bytes per channel row, channel-major tile (padded)
-constexpr int kKTileBytes = kTile * kKRow;      // 37376
-constexpr int kVTileBytes = kDc * kVRow;        // 40960
-constexpr int kStageBytes = kKTileBytes + kVTileBytes;
-constexpr float kRefSlack = 64.0f;              // log2 units a score may exceed the reference
+constexpr int kRowBytes = kDk * 2 + 32;         // fp16 tile row, padded (see below)
+constexpr int kTileBytes = kTile * kRowBytes;   // 37888
+constexpr float kRefSlack = 10.0f;              // log2 units a weight may exceed the reference
 constexpr float kLn2 = 0.693147180559945309f;
 
-static_assert(2 * kStageBytes <= 160 * 1024, "two LDS stages must fit the 160 KiB of a gfx950 CU");
+// Staging bytes of one tile's raw cache data (regions in page order).
+template <int KIND> struct Staging;
+template <> struct Staging<KIND_C4R4> {
+    static constexpr int cc = 256, rcodes = kTile * cc, meta = rcodes + kTile * 32,
+                         rmeta = meta + kTile * 32, bytes = rmeta + kTile * 4;
+};
+template <> struct Staging<KIND_C2R4> {
+    static constexpr int cc = 128, rcodes = kTile * cc, meta = rcodes + kTile * 32,
+                         rmeta = meta + kTile * 32, bytes = rmeta + kTile * 4;
+};
+template <> struct Staging<KIND_BF16> { static constexpr int bytes = kTile * 1152; };
 
-// Natural token index (0..31) of element j (0..7) of token octet o (0..3).
-// Octet o holds exactly the tokens that lane group (o & 1) of the score
-// accumulator covers in PV k-step (o >> 1), in register order.
-__device__ __forceinline__ int octet_token(int o, int j) {
-    return 16 * (o >> 1) + 4 * (o & 1) + (j & 3) + 8 * (j >> 2);
-}
+template <int KIND>
+constexpr int lds_bytes() { return 2 * kTileBytes + 2 * Staging<KIND>::bytes; }
+static_assert(lds_bytes<KIND_BF16>() + 16 <= 160 * 1024, "LDS budget of a gfx950 CU");
 
-__device__ __forceinline__ float f16lo(uint32_t w) {
-    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xffffu)));
-}
-__device__ __forceinline__ float f16hi(uint32_t w) {
-    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16)));
-}
+// Byte offset of the 16-byte chunk `chunk` (8 channels) of tile row `row`.
+// The 32-byte row pad puts 4 consecutive rows reading two neighbouring chunks
+// (the transposing reads) into 8 distinct 16-byte bank groups of a 128-byte
+// window, and keeps every operand address a per-lane base plus a
+// compile-time offset.
+__device__ __forceinline__ int chunk_off(int row, int chunk) { return row * kRowBytes + (chunk << 4); }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    const bf16x2 v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};   // v_cvt_pk_bf16_f32, RNE
+    const bf16x2 v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};   // RNE
     return __builtin_bit_cast(uint32_t, v);
 }
 
-__device__ __forceinline__ float swap_halves(float v) {
-    // exchange with lane ^ 32 (the other half of the wave holds the same row)
-    return __shfl_xor(v, 32, 64);
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+    const f16x2 v = {static_cast<_Float16>(lo), static_cast<_Float16>(hi)}; // v_cvt_pk_f16_f32, RNE
+    return __builtin_bit_cast(uint32_t, v);
 }
 
-// Per-thread registers of one tile's raw (packed or bf16) cache bytes.
-template <int KIND> struct Raw;
-template <> struct Raw<KIND_C4R4> { uint32_t code[8]; uint32_t meta[8]; uint32_t rcode; uint32_t rmeta; };
-template <> struct Raw<KIND_C2R4> { uint32_t code[8]; uint32_t meta[8]; uint32_t rcode; uint32_t rmeta; };
-template <> struct Raw<KIND_BF16> { uint4 c[8]; uint4 r; };
+__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
+    return pack_f16x2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
+}
 
-struct TileCtx {
-    const uint8_t* page;   // page holding the tile
-    int po;                // page offset of the tile's first token
-    int nvalid;            // tokens of the tile inside the work range
-};
+__device__ __forceinline__ float swap_halves(float v) { return __shfl_xor(v, 32, 64); }
 
-template <int KIND>
-__device__ __forceinline__ void load_raw(Raw<KIND>& raw, const TileCtx& tc, const PageGeom& g,
-                                         int wave, int lane, int tid) {
-    if constexpr (KIND == KIND_BF16) {
+// acc *= alpha on an accumulator tile held in AGPRs, element by element in
+// place.  Used only on the rare rescale path, hundreds of cycles after the
+// last matrix instruction that wrote the tile and before the next one reads it.
+__device__ __forceinline__ void scale_acc(f32x16& acc, float alpha) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int t = octet_token(wave, j);
-            raw.c[j] = *reinterpret_cast<const uint4*>(tc.page + (tc.po + t) * 1152 + lane * 16);
-        }
-        const int t = tid >> 3;
-        raw.r = *reinterpret_cast<const uint4*>(tc.page + (tc.po + t) * 1152 + 1024 + (tid & 7) * 16);
-    } else {
-        constexpr int cb = (KIND == KIND_C4R4) ? 4 : 2;        // code bytes per 8 channels
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int t = octet_token(wave, j);
-            const uint8_t* p = tc.page + (tc.po + t) * g.cc_bytes + lane * cb;
-            raw.code[j] = (cb == 4) ? *reinterpret_cast<const uint32_t*>(p)
-                                    : static_cast<uint32_t>(*reinterpret_cast<const uint16_t*>(p));
-            raw.meta[j] = *reinterpret_cast<const uint32_t*>(tc.page + g.off_mc + (tc.po + t) * 32 + (lane >> 3) * 4);
-        }
-        const int t = tid >> 3;
-        raw.rcode = *reinterpret_cast<const uint32_t*>(tc.page + g.off_cr + (tc.po + t) * 32 + (tid & 7) * 4);
-        raw.rmeta = *reinterpret_cast<const uint32_t*>(tc.page + g.off_mr + (tc.po + t) * 4);
+    for (int v = 0; v < 16; ++v) {
+        float t;
+        asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
+                     : "+a"(acc[v]), "=&v"(t)
+                     : "v"(alpha));
     }
 }
 
-// Dequantize 8 codes of one group slice: x_hat = scale * (q - zero).
-template <int BITS>
-__device__ __forceinline__ void dequant8(uint32_t code, uint32_t meta, float v[8]) {
-    const float sc = f16lo(meta);
-    const float ze = f16hi(meta);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const float q = static_cast<float>((code >> (BITS * i)) & ((1u << BITS) - 1u));
-        v[i] = sc * (q - ze);
-    }
+// ---------------------------------------------------------------------------
+// 1. HBM -> LDS staging of one tile (direct-to-LDS loads, 16 B per lane).
+// Chunk j of the staging area is loaded by lane (j % 64) of wave ((j / 64) % 4)
+// in round j / 256, so every wave instruction fills 1 KiB of contiguous LDS.
+// The region sizes make every (round, wave) read from one region: the content
+// codes fill whole rounds and the three small regions start a round at waves
+// 0, 1 and 2.
+__device__ __forceinline__ void dma16(const uint8_t* src, uint8_t* lds_wave_base) {
+    __builtin_amdgcn_global_load_lds((gbl_void*)src, (lds_void*)lds_wave_base, 16, 0, 0);
 }
 
 template <int KIND>
-__device__ __forceinline__ void store_tile(const Raw<KIND>& raw, uint8_t* stage, int nvalid,
-                                           int wave, int lane, int tid) {
-    uint8_t* kt = stage;
-    uint8_t* vt = stage + kKTileBytes;
-    // content: this thread owns channels 8*lane..+8 of token octet `wave`
-    uint32_t kw[8][4];      // [token j][channel pair]
+__device__ __forceinline__ void stage_tile(const uint8_t* page, int po, const PageGeom& g, uint8_t* stage,
+                                           int wave, int lane) {
     if constexpr (KIND == KIND_BF16) {
+        constexpr int rounds = Staging<KIND>::bytes / (kThreads * 16);       // 9
+        static_assert(rounds * kThreads * 16 == Staging<KIND>::bytes, "whole rounds");
+        const uint8_t* src = page + po * 1152 + (wave * 64 + lane) * 16;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const bool ok = octet_token(wave, j) < nvalid;
-            kw[j][0] = ok ? raw.c[j].x : 0u;
-            kw[j][1] = ok ? raw.c[j].y : 0u;
-            kw[j][2] = ok ? raw.c[j].z : 0u;
-            kw[j][3] = ok ? raw.c[j].w : 0u;
-        }
+        for (int r = 0; r < rounds; ++r)
+            dma16(src + r * kThreads * 16, stage + (r * kThreads + wave * 64) * 16);
     } else {
-        constexpr int BITS = (KIND == KIND_C4R4) ? 4 : 2;
+        using S = Staging<KIND>;
+        constexpr int code_rounds = S::rcodes / (kThreads * 16);             // 2 (4-bit) or 1 (2-bit)
+        static_assert(code_rounds * kThreads * 16 == S::rcodes, "content codes fill whole rounds");
+        static_assert(S::meta - S::rcodes == 1024 && S::rmeta - S::meta == 1024, "one wave per small region");
+        const uint8_t* src = page + po * S::cc + (wave * 64 + lane) * 16;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            float v[8];
-            dequant8<BITS>(raw.code[j], raw.meta[j], v);
-            const bool ok = octet_token(wave, j) < nvalid;
-#pragma unroll
-            for (int p = 0; p < 4; ++p) kw[j][p] = ok ? pack_bf16x2(v[2 * p], v[2 * p + 1]) : 0u;
+        for (int r = 0; r < code_rounds; ++r)
+            dma16(src + r * kThreads * 16, stage + (r * kThreads + wave * 64) * 16);
+        uint8_t* dst = stage + S::rcodes + wave * 1024;
+        if (wave == 0) {
+            dma16(page + g.off_cr + po * 32 + lane * 16, dst);
+        } else if (wave == 1) {
+            dma16(page + g.off_mc + po * 32 + lane * 16, dst);
+        } else if (wave == 2 && lane < kTile * 4 / 16) {
+            dma16(page + g.off_mr + po * 4 + lane * 16, dst);
         }
     }
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int t = octet_token(wave, j);
-        *reinterpret_cast<uint4*>(kt + t * kKRow + lane * 16) = make_uint4(kw[j][0], kw[j][1], kw[j][2], kw[j][3]);
-    }
-    // channel-major copy: row = channel, 8 tokens of this octet in register order
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int p = i >> 1;
-        const int sh = (i & 1) * 16;
-        uint32_t w[4];
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            const uint32_t a = (kw[2 * jj][p] >> sh) & 0xffffu;
-            const uint32_t b = (kw[2 * jj + 1][p] >> sh) & 0xffffu;
-            w[jj] = a | (b << 16);
-        }
-        *reinterpret_cast<uint4*>(vt + (lane * 8 + i) * kVRow + wave * 16) = make_uint4(w[0], w[1], w[2], w[3]);
-    }
-    // RoPE key: token tid>>3, channels 512 + 8*(tid&7)..+8
-    const int t = tid >> 3;
-    const bool ok = t < nvalid;
-    uint4 r;
-    if constexpr (KIND == KIND_BF16) {
-        r = ok ? raw.r : make_uint4(0u, 0u, 0u, 0u);
-    } else {
-        float v[8];
-        dequant8<4>(raw.rcode, raw.rmeta, v);
-        r = ok ? make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
-                            pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]))
-               : make_uint4(0u, 0u, 0u, 0u);
-    }
-    *reinterpret_cast<uint4*>(kt + t * kKRow + (kDc + (tid & 7) * 8) * 2) = r;
 }
 
+// ---------------------------------------------------------------------------
+// 2. Dequantization of a staged tile into the fp16 tile.
+//
+// Codes become fp16 values 1024 + q (the fp16 with bits 0x6400 | q, exact);
+// (1024 + q) - (1024 + zero) = q - zero exactly, and one fp16 multiply by the
+// stored scale rounds s * (q - zero) once.  Both in packed fp16 (2 per op).
+__device__ __forceinline__ void meta_to_f16(uint32_t meta, f16x2& zz, f16x2& ss) {
+    const _Float16 s = __builtin_bit_cast(_Float16, static_cast<uint16_t>(meta & 0xFFFFu));
+    const _Float16 z = __builtin_bit_cast(_Float16, static_cast<uint16_t>(meta >> 16));
+    const _Float16 zb = z + static_cast<_Float16>(1024.0f);    // exact: z is an integer in [0, 15]
+    zz = f16x2{zb, zb};
+    ss = f16x2{s, s};
+}
+
+// 8 four-bit codes (channel 2j in the low nibble of byte j) -> 4 fp16 pairs.
+__device__ __forceinline__ uint4 codes4_to_f16(uint32_t w, f16x2 zz, f16x2 ss) {
+    const uint32_t lo = w & 0x0F0F0F0Fu;          // channels 0, 2, 4, 6
+    const uint32_t hi = (w >> 4) & 0x0F0F0F0Fu;   // channels 1, 3, 5, 7
+    uint32_t o[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        // bytes [lo.b_k, 0, hi.b_k, 0]
+        const uint32_t sel = static_cast<uint32_t>(k) | 0x0C000C00u | (static_cast<uint32_t>(4 + k) << 16);
+        const uint32_t pair = __builtin_amdgcn_perm(hi, lo, sel) | 0x64006400u;
+        o[k] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, pair) - zz) * ss);
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+// 8 two-bit codes (channel 4j+k in bits 2k..2k+1 of byte j), low 16 bits of w.
+__device__ __forceinline__ uint4 codes2_to_f16(uint32_t w, f16x2 zz, f16x2 ss) {
+    uint32_t o[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {          // pair k: channels 2k, 2k+1
+        const uint32_t sh = 4 * k;
+        const uint32_t pair = ((w >> sh) & 3u) | (((w >> (sh + 2)) & 3u) << 16) | 0x64006400u;
+        o[k] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, pair) - zz) * ss);
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+__device__ __forceinline__ uint4 bf16x8_to_f16(uint4 v) {
+    return make_uint4(bf16x2_to_f16x2(v.x), bf16x2_to_f16x2(v.y), bf16x2_to_f16x2(v.z), bf16x2_to_f16x2(v.w));
+}
+
+// Thread t: tile row (t >> 3) and part (t & 7); the part is one content group
+// of 64 channels (8 chunks) plus one RoPE chunk of 8 channels.
+template <int KIND>
+__device__ __forceinline__ void dequant_tile(const uint8_t* stage, uint8_t* tile, int nvalid, int tid) {
+    const int row = tid >> 3;
+    const int part = tid & 7;
+    uint4 w[9];
+    if constexpr (KIND == KIND_BF16) {
+        const uint4* src = reinterpret_cast<const uint4*>(stage + row * 1152);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) w[j] = bf16x8_to_f16(src[part * 8 + j]);
+        w[8] = bf16x8_to_f16(src[64 + part]);
+    } else {
+        using S = Staging<KIND>;
+        f16x2 zz, ss;
+        meta_to_f16(*reinterpret_cast<const uint32_t*>(stage + S::meta + row * 32 + part * 4), zz, ss);
+        if constexpr (KIND == KIND_C4R4) {
+            const uint4 c0 = *reinterpret_cast<const uint4*>(stage + row * 256 + part * 32);
+            const uint4 c1 = *reinterpret_cast<const uint4*>(stage + row * 256 + part * 32 + 16);
+            const uint32_t cw[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) w[j] = codes4_to_f16(cw[j], zz, ss);
+        } else {
+            const uint4 c0 = *reinterpret_cast<const uint4*>(stage + row * 128 + part * 16);
+            const uint32_t cw[4] = {c0.x, c0.y, c0.z, c0.w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) w[j] = codes2_to_f16(cw[j >> 1] >> (16 * (j & 1)), zz, ss);
+        }
+        f16x2 rz, rs;
+        meta_to_f16(*reinterpret_cast<const uint32_t*>(stage + S::rmeta + row * 4), rz, rs);
+        w[8] = codes4_to_f16(*reinterpret_cast<const uint32_t*>(stage + S::rcodes + row * 32 + part * 4), rz, rs);
+    }
+    const bool ok = row < nvalid;
+#pragma unroll
+    for (int j = 0; j < 9; ++j) {
+        const int chunk = j < 8 ? part * 8 + j : 64 + part;
+        *reinterpret_cast<uint4*>(tile + chunk_off(row, chunk)) = ok ? w[j] : make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
+// ---------------------------------------------------------------------------
 template <int KIND>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void decode_kernel(DecodeArgs a) {
-    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * kStageBytes];
-    __shared__ int restart_flag;
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[lds_bytes<KIND>()];
+    uint8_t* tiles = smem;                              // 2 x kTileBytes
+    uint8_t* stages = smem + 2 * kTileBytes;            // 2 x Staging::bytes
+    constexpr int kStage = Staging<KIND>::bytes;
+
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -243,8 +296,6 @@ void decode_kernel(DecodeArgs a) {
         b = lo < a.B ? lo : a.B - 1;
         t_begin = (w - a.split_indptr[b]) * a.split_tokens;
         t_end = t_begin + a.split_tokens;
-        const int L = a.seq_lens[b];
-        if (t_end > L) t_end = L;
     }
     const int L = min(max(a.seq_lens[b], 0), a.max_pages * P);
     if (t_end > L) t_end = L;
@@ -258,125 +309,132 @@ void decode_kernel(DecodeArgs a) {
     const int h = row_ok ? row % a.H : 0;
     const int lim = row_ok ? min(L - a.s_q + qi + 1, t_end) : t_begin;   // keys t < lim are visible
 
-    bf16x8 qf[kKSteps];
+    // queries as fp16 B operands: k-step kk holds channels 16kk + 8*half .. +8
+    f16x8 qf[kKSteps];
     {
         const int64_t qrow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
         const uint16_t* ql = a.q_lat + qrow * kDc + 8 * half;
         const uint16_t* qr = a.q_rope + qrow * 64 + 8 * half;
 #pragma unroll
         for (int kk = 0; kk < kKSteps; ++kk) {
-            const uint16_t* p = kk < 32 ? ql + 16 * kk : qr + 16 * (kk - 32);
-            qf[kk] = *reinterpret_cast<const bf16x8*>(p);   // rows past the end read row 0; never written
+            // rows past the end read row 0 of the sequence; they are never stored
+            const uint4 v = *reinterpret_cast<const uint4*>(kk < 32 ? ql + 16 * kk : qr + 16 * (kk - 32));
+            qf[kk] = __builtin_bit_cast(f16x8, bf16x8_to_f16(v));
         }
     }
 
-    f32x16 acc[16];
-#pragma unroll
-    for (int m = 0; m < 16; ++m) acc[m] = f32x16{};
-    float m_ref = -INFINITY;    // reference of the exponentials (log2 units)
-    float m_true = -INFINITY;   // true running maximum (log2 units)
-    float l_run = 0.0f;         // this lane's share of the exponential sum
-    if (tid == 0) restart_flag = 0;
-
-    auto tile_ctx = [&](int it) {
-        TileCtx tc;
+    auto tile_page = [&](int it, int& po) {
         const int t0 = t_begin + it * kTile;
         int pid = a.block_table[static_cast<int64_t>(b) * a.max_pages + t0 / P];
         pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
-        tc.page = a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
-        tc.po = t0 % P;
-        tc.nvalid = t_end - t0;
-        return tc;
+        po = t0 % P;
+        return a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
     };
 
-    Raw<KIND> raw;
-    if (n_tiles > 0) {
-        const TileCtx tc = tile_ctx(0);
-        load_raw<KIND>(raw, tc, a.g, wave, lane, tid);
-        store_tile<KIND>(raw, smem, tc.nvalid, wave, lane, tid);
-    }
-    if (n_tiles > 1) load_raw<KIND>(raw, tile_ctx(1), a.g, wave, lane, tid);
+    // per-lane addressing of the transposing V^T reads: lane (group g, index i)
+    // supplies the address of tile row k0 + i/4, channels n0 + 4(i%4) .. +3
+    // and receives rows k0 .. k0+3 of channel n0 + i
+    const int qk_row = lane & 31;
+    const int tr_i = lane & 15;
+    const int tr_g = lane >> 4;
+    const int tr_kbase = 4 * (tr_g >> 1) + (tr_i >> 2);   // + 16 * ks (+ 8 for the second read)
+    const int tr_col = 16 * (tr_g & 1) + 4 * (tr_i & 3);  // + 32 * m
 
-    for (int it = 0; it < n_tiles; ++it) {
-        __syncthreads();
-        if (restart_flag != 0) {
-            // some row met a score far above its reference: start the split
-            // again with the raised references (uniform across the block)
+    float m_ref = -INFINITY;    // reference of the exponentials (log2 units)
+    float m_true = -INFINITY;   // true running maximum (log2 units)
+    float l_run = 0.0f;         // this lane's share of the exponential sum
+    f32x16 acc[16];
 #pragma unroll
-            for (int m = 0; m < 16; ++m) acc[m] = f32x16{};
-            l_run = 0.0f;
-            const TileCtx tc = tile_ctx(0);
-            load_raw<KIND>(raw, tc, a.g, wave, lane, tid);
-            store_tile<KIND>(raw, smem, tc.nvalid, wave, lane, tid);
-            if (n_tiles > 1) load_raw<KIND>(raw, tile_ctx(1), a.g, wave, lane, tid);
-            it = 0;
-            __syncthreads();
-            if (tid == 0) restart_flag = 0;
+    for (int m = 0; m < 16; ++m) acc[m] = f32x16{};
+
+    {
+        // prologue: stage tiles 0 and 1, dequantize tile 0
+        int po;
+        if (n_tiles > 0) {
+            const uint8_t* pg = tile_page(0, po);
+            stage_tile<KIND>(pg, po, a.g, stages, wave, lane);
         }
-        const uint8_t* kt = smem + (it & 1) * kStageBytes;
-        const uint8_t* vt = kt + kKTileBytes;
-        const int t0 = t_begin + it * kTile;
-        {
+        if (n_tiles > 1) {
+            const uint8_t* pg = tile_page(1, po);
+            stage_tile<KIND>(pg, po, a.g, stages + kStage, wave, lane);
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (n_tiles > 0) dequant_tile<KIND>(stages, tiles, t_end - t_begin, tid);
+
+        for (int it = 0; it < n_tiles; ++it) {
+            __builtin_amdgcn_s_waitcnt(0);   // this thread's staging of tile it+1 has landed
+            __syncthreads();                 // tile it is in LDS; staging it+1 complete; tile (it+1)&1 free
+            if (it + 2 < n_tiles) {
+                const uint8_t* pg = tile_page(it + 2, po);
+                stage_tile<KIND>(pg, po, a.g, stages + (it & 1) * kStage, wave, lane);
+            }
+            const uint8_t* kt = tiles + (it & 1) * kTileBytes;
+            const int t0 = t_begin + it * kTile;
+
             // every wave computes, also one whose rows all lie past the end
             // (its results are never stored): a branch here would force the
-            // accumulators through a register-class join
+            // accumulators through a register-class join.
             // scores S^T[token][row], K = 576 in 36 steps
-            f32x16 s0 = f32x16{};
-            const uint8_t* krow = kt + (lane & 31) * kKRow + half * 16;
+            f32x16 s = f32x16{};
+            const uint8_t* krow = kt + chunk_off(qk_row, half);
 #pragma unroll
-            for (int kk = 0; kk < kKSteps; kk += 2) {
-                const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(krow + kk * 32);
-                const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(krow + kk * 32 + 32);
-                s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[kk], s0, 0, 0, 0);
-                s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[kk + 1], s0, 0, 0, 0);
+            for (int kk = 0; kk < kKSteps; ++kk) {
+                const f16x8 k = *reinterpret_cast<const f16x8*>(krow + 32 * kk);
+                s = __builtin_amdgcn_mfma_f32_32x32x16_f16(k, qf[kk], s, 0, 0, 0);
             }
-            // online softmax over this lane's 16 tokens (the other 16 of the
-            // row live in lane ^ 32)
             float x[16];
             float mt = -INFINITY;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
-                x[v] = t < lim ? s0[v] * a.scale_log2 : -INFINITY;
+                x[v] = t < lim ? s[v] * a.scale_log2 : -INFINITY;
                 mt = fmaxf(mt, x[v]);
             }
             mt = fmaxf(mt, swap_halves(mt));
             m_true = fmaxf(m_true, mt);
-            if (m_ref == -INFINITY) m_ref = mt;           // first tile with a visible key
-            if (mt > m_ref + kRefSlack) {                 // rare: raise and restart
-                m_ref = mt;
-                restart_flag = 1;
+            if (m_ref == -INFINITY) m_ref = mt;          // first visible key: nothing accumulated yet
+            if (__builtin_amdgcn_ballot_w64(mt > m_ref + kRefSlack) != 0) {
+                const float m_new = fmaxf(m_ref, mt);     // finite for every row that needs it
+                const float alpha = exp2f(m_ref - m_new); // 1 for the other rows
+#pragma unroll
+                for (int m = 0; m < 16; ++m) scale_acc(acc[m], alpha);
+                l_run *= alpha;
+                m_ref = m_new;
             }
             const float ref = m_ref == -INFINITY ? 0.0f : m_ref;
-            float p[16];
+            uint32_t pw[8];
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                p[v] = exp2f(x[v] - ref);
-                l_run += p[v];
+            for (int v = 0; v < 16; v += 2) {
+                const float p0 = exp2f(x[v] - ref);
+                const float p1 = exp2f(x[v + 1] - ref);
+                l_run += p0 + p1;
+                pw[v >> 1] = pack_f16x2(p0, p1);
             }
-            bf16x8 pb[2];
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                pb[ks] = bf16x8{static_cast<__bf16>(p[8 * ks + 0]), static_cast<__bf16>(p[8 * ks + 1]),
-                                static_cast<__bf16>(p[8 * ks + 2]), static_cast<__bf16>(p[8 * ks + 3]),
-                                static_cast<__bf16>(p[8 * ks + 4]), static_cast<__bf16>(p[8 * ks + 5]),
-                                static_cast<__bf16>(p[8 * ks + 6]), static_cast<__bf16>(p[8 * ks + 7])};
-            }
-            // latent aggregation O^T[channel][row] += V^T . P^T
-            const uint8_t* vrow = vt + (lane & 31) * kVRow + half * 16;
+            const f16x8 pb0 = __builtin_bit_cast(f16x8, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+            const f16x8 pb1 = __builtin_bit_cast(f16x8, make_uint4(pw[4], pw[5], pw[6], pw[7]));
+
+            // latent aggregation O^T[channel][row] += V^T . P^T; the V^T operand
+            // is read transposed from the token-major tile
+            const uint8_t* vbase = kt + chunk_off(tr_kbase, 0) + 2 * tr_col;
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
                 for (int m = 0; m < 16; ++m) {
-                    const bf16x8 v = *reinterpret_cast<const bf16x8*>(vrow + m * 32 * kVRow + ks * 32);
-                    acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, pb[ks], acc[m], 0, 0, 0);
+                    const uint8_t* p = vbase + (16 * ks) * kRowBytes + 64 * m;
+                    const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+                    const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * kRowBytes));
+                    const f16x8 va = __builtin_bit_cast(f16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+                    acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, ks == 0 ? pb0 : pb1, acc[m], 0, 0, 0);
                 }
             }
-        }
-        if (it + 1 < n_tiles) {
-            const TileCtx tc = tile_ctx(it + 1);
-            store_tile<KIND>(raw, smem + ((it + 1) & 1) * kStageBytes, tc.nvalid, wave, lane, tid);
-            if (it + 2 < n_tiles) load_raw<KIND>(raw, tile_ctx(it + 2), a.g, wave, lane, tid);
+            // keep the unpacking of the next tile out of the operand loads of
+            // this one: interleaving them overflows the register file
+            __builtin_amdgcn_sched_barrier(0);
+            if (it + 1 < n_tiles)
+                dequant_tile<KIND>(stages + ((it + 1) & 1) * kStage, tiles + ((it + 1) & 1) * kTileBytes,
+                                   t_end - t_begin - (it + 1) * kTile, tid);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 
@@ -391,9 +449,9 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 const int c = 32 * m + 8 * q4;
-                const uint2 v = make_uint2(pack_bf16x2(acc[m][4 * q4] * inv, acc[m][4 * q4 + 1] * inv),
-                                           pack_bf16x2(acc[m][4 * q4 + 2] * inv, acc[m][4 * q4 + 3] * inv));
-                *reinterpret_cast<uint2*>(op + c) = v;
+                *reinterpret_cast<uint2*>(op + c) =
+                    make_uint2(pack_bf16x2(acc[m][4 * q4] * inv, acc[m][4 * q4 + 1] * inv),
+                               pack_bf16x2(acc[m][4 * q4 + 2] * inv, acc[m][4 * q4 + 3] * inv));
             }
         }
         if (a.lse != nullptr && half == 0)

@@ -114,6 +114,8 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
     if (s_q != 1 && s_q != 2) return MLA_EINVAL;
     if (H <= 0 || H % 16 != 0) return MLA_EINVAL;
     if (!std::isfinite(softmax_scale)) return MLA_EINVAL;
+    if (split_tokens % kTile != 0) return MLA_ENOTSUP;
+    if (B == 0) return MLA_OK;   // nothing is read or written
     if (q_lat == nullptr || q_rope == nullptr || cache == nullptr || block_table == nullptr || seq_lens == nullptr)
         return MLA_EINVAL;
     if (num_pages == 0) return MLA_EINVAL;
@@ -125,10 +127,8 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
     } else {
         if (split_indptr == nullptr || part_m == nullptr || part_s == nullptr || part_o == nullptr || num_splits < 0)
             return MLA_EINVAL;
-        if (split_tokens % kTile != 0) return MLA_ENOTSUP;
         if (!aligned(part_o, 16)) return MLA_ENOTSUP;
     }
-    if (B == 0) return MLA_OK;
     mla::DecodeArgs a{};
     a.q_lat = q_lat;
     a.q_rope = q_rope;
@@ -223,11 +223,11 @@ int mla_splitkv_combine(const float* part_m, const float* part_s, const float* p
     if (B < 0 || d_c <= 0) return MLA_EINVAL;
     if (s_q != 1 && s_q != 2) return MLA_EINVAL;
     if (H <= 0 || H % 16 != 0) return MLA_EINVAL;
+    if (d_c != kDc) return MLA_ENOTSUP;
+    if (B == 0) return MLA_OK;   // nothing is read or written
     if (part_m == nullptr || part_s == nullptr || part_o == nullptr || split_indptr == nullptr || out == nullptr)
         return MLA_EINVAL;
-    if (d_c != kDc) return MLA_ENOTSUP;
     if (!aligned(part_o, 16) || !aligned(out, 8)) return MLA_ENOTSUP;
-    if (B == 0) return MLA_OK;
     mla::CombineArgs a{};
     a.part_m = part_m;
     a.part_s = part_s;

@@ -3,12 +3,15 @@ tolerance checks.
 
 Tolerances (attention, floating point):
   * output: mean |gpu - oracle| <= 2e-3 * RMS(oracle) over all compared
-    outputs, and for every latent channel c, max over rows |gpu - oracle| <=
-    2e-2 * RMS over rows of the oracle's channel c.  The max rule is read per
-    channel: the synthetic latents carry 10x outlier channels, so a few
-    channels' outputs are an order of magnitude above the global RMS, and the
-    bf16 rounding of those outputs alone (2^-9 |out|) exceeds 2e-2 of the
-    global RMS -- for the BF16-cache kernel as much as for the low-bit one;
+    outputs, and for every latent channel c and row r,
+    |gpu - oracle|_rc <= 2e-2 * RMS_c + u_rc, where RMS_c is the RMS over
+    rows of the oracle's channel c and u_rc half a bf16 ulp of the oracle
+    value (the representation error of the bf16 output format).  The max
+    rule is read this way because the synthetic latents carry 10x outlier
+    channels: those channels' outputs sit an order of magnitude above the
+    global RMS, and rounding the exact result to bf16 alone moves them by
+    more than 2e-2 of the global RMS (and of their own channel RMS), for any
+    kernel;
   * lse: |gpu - oracle| <= d_r + 1e-5 * |lse| per row, with
     d_r = tau * 2^-8 * max_t sum_c |q_rc| |k_hat_tc|.  The kernel rounds the
     reconstructed keys to bf16 once (relative error <= 2^-9 per element) and
@@ -85,7 +88,10 @@ class AttnStats:
         wo = np.asarray(want_out, np.float64)
         self.sq_sum += float((wo ** 2).sum())
         self.n += d.size
-        d2 = d.reshape(-1, D_C)
+        # error beyond the bf16 output's own half-ulp representation error
+        ay = np.abs(wo) * (1 + 2.0 ** -7)
+        half_ulp = np.where(ay > 0, np.exp2(np.floor(np.log2(np.maximum(ay, 1e-300))) - 8), 0.0)
+        d2 = np.maximum(d - half_ulp, 0.0).reshape(-1, D_C)
         if not hasattr(self, "ch_max"):
             self.ch_max = np.zeros(D_C)
             self.ch_sq = np.zeros(D_C)
@@ -100,13 +106,15 @@ class AttnStats:
             self.lse_max_err = max(self.lse_max_err, float(e.max()))
 
     def check(self, label="", rms_max=True):
-        """Assert the bounds.  ``rms_max`` applies the per-channel max-abs rule."""
+        """Assert the bounds.  ``rms_max`` applies the per-channel max-abs rule
+        (small edge-case batches, whose channel RMS is dominated by a few rows,
+        rely on the per-element bound instead)."""
         rms = np.sqrt(self.sq_sum / self.n)
         mean = self.abs_sum / self.n
         ch_rms = np.sqrt(self.ch_sq / self.ch_n)
         ch_ratio = float((self.ch_max / ch_rms).max())
         msg = (f"{label}: n={self.n} rms={rms:.4g} max_abs={self.abs_max:.4g} ({self.abs_max / rms:.2e} rms) "
-               f"mean_abs={mean:.4g} ({mean / rms:.2e} rms) max_abs/channel_rms={ch_ratio:.3g} "
+               f"mean_abs={mean:.4g} ({mean / rms:.2e} rms) max_excess/channel_rms={ch_ratio:.3g} "
                f"lse_max_err={self.lse_max_err:.3g} "
                f"elem_err/bound={getattr(self, 'elem_ratio', float('nan')):.3g}")
         print(msg, flush=True)

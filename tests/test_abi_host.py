@@ -81,7 +81,7 @@ def _decode_status(mb, **over):
     (dict(split_tokens=64, split_indptr=16, part_m=16, part_s=16, part_o=None), 1),
     (dict(split_tokens=48, split_indptr=16, part_m=16, part_s=16, part_o=16), 2),
     (dict(fmt="c3"), 1), (dict(fmt="r2"), 1), (dict(fmt="g32"), 2), (dict(fmt="p48"), 2), (dict(fmt="p40"), 1), (dict(fmt="dc256"), 2),
-    (dict(B=0), 0),
+    (dict(B=0), 0), (dict(B=0, q_lat=None, cache=None, out=None), 0), (dict(B=0, s_q=3), 1),
 ])
 def test_decode_rejects_before_any_hip_call(mb, over, status):
     fmts = {"c3": mb.cache_format(c_bits=3), "r2": mb.cache_format(r_bits=2),

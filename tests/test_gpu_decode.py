@@ -115,8 +115,9 @@ def test_split_partials_match_oracle_chunks():
             assert np.all(np.abs(go[live] / gs[live, None] - want) <= tol)
 
 
-def test_reference_restart_path():
-    """Scores that jump far above the first tile's maximum (restart of the split)."""
+def test_large_score_jump_rescale():
+    """Scores that jump far above the first tiles' maximum: the running reference
+    is raised and the accumulators rescaled in place."""
     import torch
 
     from paper_2609_36760_amd import _binding as mb
@@ -156,7 +157,7 @@ def test_reference_restart_path():
     stats = AttnStats()
     stats.add(bf16_bits_to_f64(out.cpu().numpy())[0], want, lse.cpu().numpy()[0], want_lse,
               lse_bound(ql[0], qr[0], c_hat, kr_hat, tau, L, 1))
-    stats.check("restart")
+    stats.check("rescale")
 
 
 def test_identical_keys_give_the_key():
