@@ -141,7 +141,7 @@ int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens
  *   block_table device, int32 [B][max_pages_per_seq]: page id of each
  *           page_size-token block of each sequence
  *   seq_lens    device, int32 [B]
- *   H       heads, a positive multiple of 16; s_q in {1, 2}
+ *   H       heads, a positive multiple of 16; s_q in {1, 2}; softmax_scale > 0
  *   B = 0 is a no-op after the scalar arguments are checked (pointers may be NULL)
  * Unsplit (split_tokens == 0): writes out (device, bf16 [B][s_q][H][d_c]) and,
  *   if lse != NULL, lse (device, fp32 [B][s_q][H]); split_indptr,

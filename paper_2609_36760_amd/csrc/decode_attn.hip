@@ -308,6 +308,7 @@ void decode_kernel(DecodeArgs a) {
     const int qi = row_ok ? row / a.H : 0;
     const int h = row_ok ? row % a.H : 0;
     const int lim = row_ok ? min(L - a.s_q + qi + 1, t_end) : t_begin;   // keys t < lim are visible
+    const int full_lim = min(L - a.s_q + 1, t_end);    // every valid row sees keys t < full_lim
 
     // queries as fp16 B operands: k-step kk holds channels 16kk + 8*half .. +8
     f16x8 qf[kKSteps];
@@ -376,22 +377,39 @@ void decode_kernel(DecodeArgs a) {
             // (its results are never stored): a branch here would force the
             // accumulators through a register-class join.
             // scores S^T[token][row], K = 576 in 36 steps
+            // The operand reads run kAhead steps ahead of the matrix
+            // instructions; the group barriers pin that order (left alone, the
+            // scheduler issues each read right before its use and the chain
+            // waits on LDS latency at every step).
             f32x16 s = f32x16{};
             const uint8_t* krow = kt + chunk_off(qk_row, half);
+            constexpr int kAhead = 3;
+            f16x8 kb[kAhead];
+#pragma unroll
+            for (int j = 0; j < kAhead; ++j) kb[j] = *reinterpret_cast<const f16x8*>(krow + 32 * j);
+            __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);             // LDS reads
 #pragma unroll
             for (int kk = 0; kk < kKSteps; ++kk) {
-                const f16x8 k = *reinterpret_cast<const f16x8*>(krow + 32 * kk);
+                const f16x8 k = kb[kk % kAhead];
+                if (kk + kAhead < kKSteps) kb[kk % kAhead] = *reinterpret_cast<const f16x8*>(krow + 32 * (kk + kAhead));
                 s = __builtin_amdgcn_mfma_f32_32x32x16_f16(k, qf[kk], s, 0, 0, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // one MFMA
+                if (kk + kAhead < kKSteps) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             }
-            float x[16];
-            float mt = -INFINITY;
+            // rows see every key of the tile except in the last tile of the
+            // range or the tile holding the newest key (block-uniform test)
+            if (t0 + kTile > full_lim) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
-                x[v] = t < lim ? s[v] * a.scale_log2 : -INFINITY;
-                mt = fmaxf(mt, x[v]);
+                for (int v = 0; v < 16; ++v) {
+                    const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
+                    s[v] = t < lim ? s[v] : -INFINITY;
+                }
             }
-            mt = fmaxf(mt, swap_halves(mt));
+            float mr = s[0];
+#pragma unroll
+            for (int v = 1; v < 16; ++v) mr = fmaxf(mr, s[v]);
+            mr = fmaxf(mr, swap_halves(mr));
+            const float mt = mr * a.scale_log2;           // scale > 0: max commutes
             m_true = fmaxf(m_true, mt);
             if (m_ref == -INFINITY) m_ref = mt;          // first visible key: nothing accumulated yet
             if (__builtin_amdgcn_ballot_w64(mt > m_ref + kRefSlack) != 0) {
@@ -402,12 +420,12 @@ void decode_kernel(DecodeArgs a) {
                 l_run *= alpha;
                 m_ref = m_new;
             }
-            const float ref = m_ref == -INFINITY ? 0.0f : m_ref;
+            const float nref = m_ref == -INFINITY ? 0.0f : -m_ref;
             uint32_t pw[8];
 #pragma unroll
             for (int v = 0; v < 16; v += 2) {
-                const float p0 = exp2f(x[v] - ref);
-                const float p1 = exp2f(x[v + 1] - ref);
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(s[v], a.scale_log2, nref));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(s[v + 1], a.scale_log2, nref));
                 l_run += p0 + p1;
                 pw[v >> 1] = pack_f16x2(p0, p1);
             }
@@ -417,16 +435,26 @@ void decode_kernel(DecodeArgs a) {
             // latent aggregation O^T[channel][row] += V^T . P^T; the V^T operand
             // is read transposed from the token-major tile
             const uint8_t* vbase = kt + chunk_off(tr_kbase, 0) + 2 * tr_col;
+            auto vread = [&](int step) __attribute__((always_inline)) {
+                const int ks = step >> 4, m = step & 15;
+                const uint8_t* p = vbase + (16 * ks) * kRowBytes + 64 * m;
+                const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+                const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * kRowBytes));
+                return __builtin_bit_cast(f16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+            };
+            constexpr int kVAhead = 2;
+            f16x8 vb[kVAhead];
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
+            for (int j = 0; j < kVAhead; ++j) vb[j] = vread(j);
+            __builtin_amdgcn_sched_group_barrier(0x100, 2 * kVAhead, 0);
 #pragma unroll
-                for (int m = 0; m < 16; ++m) {
-                    const uint8_t* p = vbase + (16 * ks) * kRowBytes + 64 * m;
-                    const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
-                    const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * kRowBytes));
-                    const f16x8 va = __builtin_bit_cast(f16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
-                    acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, ks == 0 ? pb0 : pb1, acc[m], 0, 0, 0);
-                }
+            for (int step = 0; step < 32; ++step) {
+                const f16x8 va = vb[step % kVAhead];
+                if (step + kVAhead < 32) vb[step % kVAhead] = vread(step + kVAhead);
+                const int m = step & 15;
+                acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, step < 16 ? pb0 : pb1, acc[m], 0, 0, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                if (step + kVAhead < 32) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
             }
             // keep the unpacking of the next tile out of the operand loads of
             // this one: interleaving them overflows the register file

@@ -113,7 +113,7 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
     if (B < 0 || num_pages < 0 || max_pages_per_seq <= 0 || split_tokens < 0) return MLA_EINVAL;
     if (s_q != 1 && s_q != 2) return MLA_EINVAL;
     if (H <= 0 || H % 16 != 0) return MLA_EINVAL;
-    if (!std::isfinite(softmax_scale)) return MLA_EINVAL;
+    if (!std::isfinite(softmax_scale) || !(softmax_scale > 0.0f)) return MLA_EINVAL;
     if (split_tokens % kTile != 0) return MLA_ENOTSUP;
     if (B == 0) return MLA_OK;   // nothing is read or written
     if (q_lat == nullptr || q_rope == nullptr || cache == nullptr || block_table == nullptr || seq_lens == nullptr)

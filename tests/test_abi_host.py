@@ -77,7 +77,7 @@ def _decode_status(mb, **over):
 @pytest.mark.parametrize("over,status", [
     (dict(q_lat=None), 1), (dict(cache=None), 1), (dict(out=None), 1), (dict(s_q=3), 1), (dict(s_q=0), 1),
     (dict(H=24), 1), (dict(H=0), 1), (dict(B=-1), 1), (dict(max_pages=0), 1), (dict(num_pages=0), 1),
-    (dict(cache=272), 1), (dict(q_lat=8), 2), (dict(scale=float("inf")), 1),
+    (dict(cache=272), 1), (dict(q_lat=8), 2), (dict(scale=float("inf")), 1), (dict(scale=0.0), 1), (dict(scale=-0.1), 1),
     (dict(split_tokens=64, split_indptr=16, part_m=16, part_s=16, part_o=None), 1),
     (dict(split_tokens=48, split_indptr=16, part_m=16, part_s=16, part_o=16), 2),
     (dict(fmt="c3"), 1), (dict(fmt="r2"), 1), (dict(fmt="g32"), 2), (dict(fmt="p48"), 2), (dict(fmt="p40"), 1), (dict(fmt="dc256"), 2),

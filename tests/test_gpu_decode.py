@@ -246,3 +246,26 @@ def test_decode_full_size_sampled(case):
     stats.check(f"{name} layer {layer} {kind}")
     del run
     torch.cuda.empty_cache()
+
+
+def test_repeated_launches_are_deterministic():
+    """Back-to-back launches of the same decode give bit-identical partials and output."""
+    import torch
+
+    from paper_2609_36760_amd import _binding as mb
+    from paper_2609_36760_amd.runner import DecodeRun
+    w = syn.WORKLOADS["dsv3_b32_h128_4k_c4r4"]
+    run = DecodeRun(w)
+    run.attend()
+    torch.cuda.synchronize()
+    ref_o, ref_m, ref_out = run.part_o.clone(), run.part_m.clone(), run.out.clone()
+    for _ in range(3):
+        for _ in range(10):
+            mb.mla_lowbit_decode_attn(run.fmt, run.q_lat, run.q_rope, run.cache, run.num_pages, run.block_table,
+                                      run.seq_lens, run.s_q, run.H, run.tau, split_tokens=run.split_tokens,
+                                      split_indptr=run.split_indptr, num_splits=run.num_splits, part_m=run.part_m,
+                                      part_s=run.part_s, part_o=run.part_o)
+        run.attend()
+        torch.cuda.synchronize()
+        assert torch.equal(run.part_o, ref_o) and torch.equal(run.part_m, ref_m)
+        assert torch.equal(run.out, ref_out)
