@@ -11,16 +11,20 @@
 // are the (max, sum, weighted sum) of Appendix C.5 "Global attention
 // normalization".
 //
-// Workgroup = 4 waves = 256 threads, one per CU; it owns one (sequence or key
-// split, block of 128 query rows); wave w owns rows 32w..32w+31.
+// Workgroup = 4 waves = 256 threads, one per CU (one wave per SIMD); it owns
+// one (sequence or key split, block of 128 query rows); wave w owns rows
+// 32w..32w+31.
 //
 // Data path per 32-token tile:
-//   1. the tile's packed bytes (codes and metadata regions of the page; raw
-//      bf16 rows for the BF16 cache) are copied HBM -> LDS by direct-to-LDS
-//      loads (global_load_lds_dwordx4), two tiles ahead of use;
-//   2. all 256 threads unpack and dequantize them with packed fp16 math into
-//      one token-major fp16 tile [32][576] (rows padded by 32 bytes to spread
-//      LDS banks); invalid tokens become zeros;
+//   1. its packed bytes (code and metadata regions of the page) are copied
+//      HBM -> LDS by direct-to-LDS loads (global_load_lds_dwordx4) three tiles
+//      ahead of use, every wave issuing the same number of loads so that one
+//      counted wait covers a tile; the page id comes from a load issued one
+//      tile earlier.  Rows past the end of the range re-read the range's last
+//      token, so every staged row decodes to finite values;
+//   2. all 256 threads unpack and dequantize them with packed fp16 math into a
+//      token-major fp16 tile [32][576] (rows padded by 32 bytes to spread LDS
+//      banks);
 //   3. scores: every wave computes S^T[token][row] = K_tile . Q^T with
 //      v_mfma_f32_32x32x16_f16 (M = 32 tokens, N = its 32 rows, K = 576), the
 //      rows' queries held in registers as the B operand.  A lane then holds
@@ -31,22 +35,36 @@
 //      SAME token-major tile with ds_read_b64_tr_b16 (transposing loads), the
 //      P^T operand comes straight from the score registers.
 //
-// The fp16 datapath (instead of bf16) keeps the reconstructed latents and the
-// probabilities to 11 significant bits; the result is accumulated in fp32 and
-// rounded once to the bf16 output.  Inputs must lie within the fp16 range
+// Software pipeline.  With one wave per SIMD no other wave hides a wave's
+// latencies, so every step interleaves independent work explicitly:
+//   step j:  scores of tile j   ||  dequantization of tile j+1
+//            softmax of tile j  ||  latent aggregation of tile j-1
+// (the aggregation trails the scores by one tile: three fp16 tile buffers,
+// three staging buffers).  Group barriers pin the interleaving.
+//
+// The BF16-cache kernel stages raw bf16 rows straight into padded tile
+// buffers (four of them; staging distance two tiles) and runs the same steps
+// on bf16 matrix instructions, the weights rounded to bf16 (cache values and
+// queries are exact in bf16, so the weights are the only rounded operand).
+//
+// The fp16 datapath of the low-bit kernel keeps the reconstructed latents and
+// the probabilities to 11 significant bits; the result is accumulated in fp32
+// and rounded once to the bf16 output.  Inputs must lie within the fp16 range
 // (|q|, |x_hat| < 65504), which also bounds the reference slack below.
 //
 // Online softmax with a lazy rescale: every row keeps a running reference
 // (its maximum so far, log2 units) and the weights p = 2^(x - ref) stay below
 // 2^10 (well inside fp16).  Only when a tile's maximum exceeds the reference by
-// more than that slack does the wave rescale its rows' accumulators -- rare
-// after the first tiles.  The rescale reads and writes the accumulator
-// registers in place (the compiler would otherwise stage all 256 of them
-// through vector registers at the branch).  The true maximum is tracked
-// separately for the split partials.
+// more than that slack does the wave move its rows to a new reference -- rare
+// after the first tiles.  The accumulators are then rescaled once the trailing
+// aggregation (still on the old reference) has been added, in place in their
+// registers (the compiler would otherwise stage all 256 of them through vector
+// registers at the branch).  The true maximum is tracked separately for the
+// split partials.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <type_traits>
 
 #include "internal.h"
 
@@ -54,6 +72,7 @@ namespace mla {
 namespace {
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -68,33 +87,61 @@ constexpr int kTile = 32;                       // tokens per tile
 constexpr int kDc = 512;
 constexpr int kDk = 576;                        // d_c + d_r
 constexpr int kKSteps = kDk / 16;               // 36 MFMA k-steps for the scores
-constexpr int kRowBytes = kDk * 2 + 32;         // fp16 tile row, padded (see below)
-constexpr int kTileBytes = kTile * kRowBytes;   // 37888
 constexpr float kRefSlack = 10.0f;              // log2 units a weight may exceed the reference
 constexpr float kLn2 = 0.693147180559945309f;
 
-// Staging bytes of one tile's raw cache data (regions in page order).
-template <int KIND> struct Staging;
-template <> struct Staging<KIND_C4R4> {
-    static constexpr int cc = 256, rcodes = kTile * cc, meta = rcodes + kTile * 32,
-                         rmeta = meta + kTile * 32, bytes = rmeta + kTile * 4;
+// Per cache kind: NT tile buffers, NS staging buffers, staging distance D
+// (tiles ahead), direct-to-LDS loads per wave per tile.
+template <int KIND> struct Cfg;
+template <> struct Cfg<KIND_C4R4> {
+    static constexpr bool lowbit = true;
+    static constexpr int cc = 256;                      // content code bytes per token
+    static constexpr int code_rounds = 2;               // content codes: 2 x 256 chunks
+    static constexpr int rcodes = kTile * cc, meta = rcodes + 1024, rmeta = meta + 1024,
+                         spare = rmeta + 128, stage_bytes = spare + 128;
+    static constexpr int NT = 3, NS = 3, D = 3, loads = code_rounds + 1;
+    static constexpr int SC = 84;                       // tile row stride in 16-byte chunks
+    static constexpr bool grouped = true;               // a pad chunk after every 8 content chunks
 };
-template <> struct Staging<KIND_C2R4> {
-    static constexpr int cc = 128, rcodes = kTile * cc, meta = rcodes + kTile * 32,
-                         rmeta = meta + kTile * 32, bytes = rmeta + kTile * 4;
+template <> struct Cfg<KIND_C2R4> {
+    static constexpr bool lowbit = true;
+    static constexpr int cc = 128;
+    static constexpr int code_rounds = 1;
+    static constexpr int rcodes = kTile * cc, meta = rcodes + 1024, rmeta = meta + 1024,
+                         spare = rmeta + 128, stage_bytes = spare + 128;
+    static constexpr int NT = 3, NS = 3, D = 3, loads = code_rounds + 1;
+    static constexpr int SC = 84;
+    static constexpr bool grouped = true;
 };
-template <> struct Staging<KIND_BF16> { static constexpr int bytes = kTile * 1152; };
+template <> struct Cfg<KIND_BF16> {
+    static constexpr bool lowbit = false;
+    static constexpr int stage_bytes = 0;
+    static constexpr int NT = 4, NS = 0, D = 2, loads = 10;   // 2432 chunks: 9 rounds of 256 + 128
+    static constexpr int SC = 76;
+    static constexpr bool grouped = false;
+};
+
+// Tile layout.  Row r (token) starts at 16 * (SC * r + ((r >> 2) & 3)) bytes;
+// logical 16-byte chunk c (8 channels) sits at chunk c + c / 8 of the row in
+// the grouped layout (low-bit tiles: a pad chunk after each 64-channel group,
+// 80 chunks in all) and at chunk c otherwise (72 chunks).  With SC = 84 (or
+// 76), the score operand reads (16 rows, one chunk each), the transposing reads
+// (4 aligned rows, 4 consecutive chunks each) and the dequantization stores
+// (8 consecutive groups of two rows r, r + 2) touch 16 distinct 16-byte bank
+// groups per 256-byte access, i.e. no bank conflicts.
+template <int KIND>
+constexpr int tile_bytes() { return kTile * Cfg<KIND>::SC * 16; }
+__host__ __device__ constexpr int row_off(int sc, int r) { return 16 * (sc * r + ((r >> 2) & 3)); }
+__host__ __device__ constexpr int phys_chunk(bool grouped, int c) { return grouped ? c + (c >> 3) : c; }
+static_assert(row_off(84, 31) + 16 * 80 <= 32 * 84 * 16, "grouped rows fit the tile");
+static_assert(row_off(84, 16) - row_off(84, 15) >= 16 * 80, "grouped rows do not overlap");
+static_assert(row_off(76, 31) + 16 * 72 <= 32 * 76 * 16, "plain rows fit the tile");
+static_assert(row_off(76, 16) - row_off(76, 15) >= 16 * 72, "plain rows do not overlap");
 
 template <int KIND>
-constexpr int lds_bytes() { return 2 * kTileBytes + 2 * Staging<KIND>::bytes; }
-static_assert(lds_bytes<KIND_BF16>() + 16 <= 160 * 1024, "LDS budget of a gfx950 CU");
-
-// Byte offset of the 16-byte chunk `chunk` (8 channels) of tile row `row`.
-// The 32-byte row pad puts 4 consecutive rows reading two neighbouring chunks
-// (the transposing reads) into 8 distinct 16-byte bank groups of a 128-byte
-// window, and keeps every operand address a per-lane base plus a
-// compile-time offset.
-__device__ __forceinline__ int chunk_off(int row, int chunk) { return row * kRowBytes + (chunk << 4); }
+constexpr int lds_bytes() { return Cfg<KIND>::NT * tile_bytes<KIND>() + Cfg<KIND>::NS * Cfg<KIND>::stage_bytes; }
+static_assert(lds_bytes<KIND_C4R4>() <= 160 * 1024, "LDS budget of a gfx950 CU");
+static_assert(lds_bytes<KIND_BF16>() <= 160 * 1024, "LDS budget of a gfx950 CU");
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -113,9 +160,25 @@ __device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
 
 __device__ __forceinline__ float swap_halves(float v) { return __shfl_xor(v, 32, 64); }
 
+// Byte offset of buffer (j mod n) of `bytes` bytes, as an opaque scalar: the
+// compiler then forms every LDS address as one per-lane base plus this offset
+// plus an immediate, instead of keeping a per-lane address for every buffer.
+__device__ __forceinline__ int slot_offset(int j, int n, int bytes) {
+    int off = (j % n) * bytes;
+    asm volatile("" : "+s"(off));
+    return off;
+}
+
+__device__ __forceinline__ f32x16 mfma(f16x8 a, f16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
 // acc *= alpha on an accumulator tile held in AGPRs, element by element in
-// place.  Used only on the rare rescale path, hundreds of cycles after the
-// last matrix instruction that wrote the tile and before the next one reads it.
+// place.  Used only on the rare rescale path; the caller first waits out the
+// latency of the matrix instructions that last wrote the tiles.
 __device__ __forceinline__ void scale_acc(f32x16& acc, float alpha) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
@@ -127,43 +190,108 @@ __device__ __forceinline__ void scale_acc(f32x16& acc, float alpha) {
 }
 
 // ---------------------------------------------------------------------------
-// 1. HBM -> LDS staging of one tile (direct-to-LDS loads, 16 B per lane).
-// Chunk j of the staging area is loaded by lane (j % 64) of wave ((j / 64) % 4)
-// in round j / 256, so every wave instruction fills 1 KiB of contiguous LDS.
-// The region sizes make every (round, wave) read from one region: the content
-// codes fill whole rounds and the three small regions start a round at waves
-// 0, 1 and 2.
-__device__ __forceinline__ void dma16(const uint8_t* src, uint8_t* lds_wave_base) {
-    __builtin_amdgcn_global_load_lds((gbl_void*)src, (lds_void*)lds_wave_base, 16, 0, 0);
+// 1. HBM -> LDS staging.
+//
+// Direct-to-LDS load of 16 bytes per lane: lane l copies base + voff into LDS
+// bytes [lds + 16 l, lds + 16 l + 16) (base and lds wave-uniform).  Written as
+// inline assembly so that the compiler does not track it: it would otherwise
+// wait for every such load in flight before any LDS read of the same array.
+// Every read of staged data instead follows an explicit counted wait and a
+// barrier (step_barrier).  M0 is saved and restored around the load.
+__device__ __forceinline__ void dma16(const uint8_t* base, uint32_t voff, uint32_t lds) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(voff), "s"(base), "s"(lds)
+        : "memory");
 }
 
+// 32-bit LDS address of a pointer into shared memory (uniform).
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
+    return __builtin_amdgcn_readfirstlane(
+        static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint8_t*)p)));
+}
+
+// Wait until at most N direct-to-LDS loads of this wave are in flight and all
+// of its LDS accesses are done, then synchronize the workgroup.
+template <int N>
+__device__ __forceinline__ void step_barrier() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+// A page-table entry through the scalar cache (one cache line holds the ids
+// of 16 consecutive pages), waited for on the spot.
+__device__ __forceinline__ int load_page_id(const int32_t* table, int index) {
+    int v;
+    asm volatile("s_load_dword %0, %1, %2\n\ts_waitcnt lgkmcnt(0)"
+                 : "=s"(v)
+                 : "s"(table), "s"(__builtin_amdgcn_readfirstlane(index * 4))
+                 : "memory");
+    return v;
+}
+
+// Packed tile: the content codes in whole rounds (chunk i of the region by
+// lane i % 64 of wave (i / 64) % 4), then one load per wave for the small
+// regions: wave 0 the RoPE codes, wave 1 the content metadata, wave 2 the RoPE
+// metadata, wave 3 the RoPE metadata again into a spare area (every wave
+// issues Cfg::loads loads).  Tokens at or past `nvalid` re-read token
+// nvalid - 1 (per-token regions; a RoPE metadata chunk holds four tokens and
+// is read as it is -- such a token's score is masked and its RoPE channels
+// never enter the aggregation).
 template <int KIND>
-__device__ __forceinline__ void stage_tile(const uint8_t* page, int po, const PageGeom& g, uint8_t* stage,
-                                           int wave, int lane) {
-    if constexpr (KIND == KIND_BF16) {
-        constexpr int rounds = Staging<KIND>::bytes / (kThreads * 16);       // 9
-        static_assert(rounds * kThreads * 16 == Staging<KIND>::bytes, "whole rounds");
-        const uint8_t* src = page + po * 1152 + (wave * 64 + lane) * 16;
+__device__ __forceinline__ void stage_lowbit(const uint8_t* page, int po, int nvalid, const PageGeom& g,
+                                             uint8_t* st, int wave, int lane) {
+    using C = Cfg<KIND>;
+    constexpr int cpt = C::cc / 16;                     // chunks per token
+    static_assert(C::code_rounds * kThreads * 16 == C::rcodes, "content codes fill whole rounds");
+    const uint32_t st_lds = lds_addr(st);
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
 #pragma unroll
-        for (int r = 0; r < rounds; ++r)
-            dma16(src + r * kThreads * 16, stage + (r * kThreads + wave * 64) * 16);
+    for (int r = 0; r < C::code_rounds; ++r) {
+        const int i = r * kThreads + wave * 64 + lane;
+        const int tok = min(i / cpt, nvalid - 1);
+        dma16(page, (po + tok) * C::cc + (i % cpt) * 16, st_lds + (r * kThreads + wave_u * 64) * 16);
+    }
+    const int tok2 = min(lane >> 1, nvalid - 1);
+    int src_off, dst_off;
+    if (wave_u == 0) {
+        src_off = g.off_cr + (po + tok2) * 32 + (lane & 1) * 16;
+        dst_off = C::rcodes;
+    } else if (wave_u == 1) {
+        src_off = g.off_mc + (po + tok2) * 32 + (lane & 1) * 16;
+        dst_off = C::meta;
     } else {
-        using S = Staging<KIND>;
-        constexpr int code_rounds = S::rcodes / (kThreads * 16);             // 2 (4-bit) or 1 (2-bit)
-        static_assert(code_rounds * kThreads * 16 == S::rcodes, "content codes fill whole rounds");
-        static_assert(S::meta - S::rcodes == 1024 && S::rmeta - S::meta == 1024, "one wave per small region");
-        const uint8_t* src = page + po * S::cc + (wave * 64 + lane) * 16;
+        src_off = g.off_mr + po * 4 + (lane & 7) * 16;
+        dst_off = wave_u == 2 ? C::rmeta : C::spare;
+    }
+    if (wave_u < 2 || lane < 8) dma16(page, src_off, st_lds + dst_off);
+}
+
+// Raw bf16 rows into a tile of the plain layout (SC = 76): LDS chunk i of the
+// tile belongs to row r (the last row starting at or before i) and column
+// i - start(r); columns 72.. are padding and receive column 71 again.  Tokens
+// at or past `nvalid` re-read token nvalid - 1.  Rounds 0..8 cover chunks
+// 0..2303 (chunk i by lane i % 64 of wave (i / 64) % 4); round 9 covers
+// 2304..2431 with waves 0/2 and 1/3 loading the same chunks (same data to the
+// same place), so that all waves issue the same number of loads.
+__device__ __forceinline__ void stage_bf16(const uint8_t* page, int po, int nvalid, uint8_t* tile, int wave,
+                                           int lane) {
+    constexpr int sc = 76;
+    const uint32_t tile_lds = lds_addr(tile);
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
 #pragma unroll
-        for (int r = 0; r < code_rounds; ++r)
-            dma16(src + r * kThreads * 16, stage + (r * kThreads + wave * 64) * 16);
-        uint8_t* dst = stage + S::rcodes + wave * 1024;
-        if (wave == 0) {
-            dma16(page + g.off_cr + po * 32 + lane * 16, dst);
-        } else if (wave == 1) {
-            dma16(page + g.off_mc + po * 32 + lane * 16, dst);
-        } else if (wave == 2 && lane < kTile * 4 / 16) {
-            dma16(page + g.off_mr + po * 4 + lane * 16, dst);
-        }
+    for (int r = 0; r < 10; ++r) {
+        const int base = r < 9 ? r * kThreads + wave * 64 : 2304 + 64 * (wave & 1);
+        const int i = base + lane;
+        int row = static_cast<int>((static_cast<unsigned>(i) * 3450u) >> 18);   // i / 76 for i < 2432
+        if (i < row_off(sc, row) / 16) --row;
+        const int col = min(i - row_off(sc, row) / 16, 71);
+        const int tok = min(row, nvalid - 1);
+        const int base_u = r < 9 ? r * kThreads + wave_u * 64 : 2304 + 64 * (wave_u & 1);
+        dma16(page, (po + tok) * 1152 + col * 16, tile_lds + base_u * 16);
     }
 }
 
@@ -208,58 +336,76 @@ __device__ __forceinline__ uint4 codes2_to_f16(uint32_t w, f16x2 zz, f16x2 ss) {
     return make_uint4(o[0], o[1], o[2], o[3]);
 }
 
-__device__ __forceinline__ uint4 bf16x8_to_f16(uint4 v) {
-    return make_uint4(bf16x2_to_f16x2(v.x), bf16x2_to_f16x2(v.y), bf16x2_to_f16x2(v.z), bf16x2_to_f16x2(v.w));
+// Thread t dequantizes part (t & 7) -- one content group of 64 channels (8
+// chunks) plus one RoPE chunk of 8 channels -- of tile row dq_row(t); the
+// eight threads of a row and the row two further on share a 16-lane store
+// group (conflict-free in the grouped layout).  Split in two: the staged bytes
+// a thread needs (read at the start of a step) and nine chunk steps
+// (arithmetic plus one 16-byte store each) spread over the score products.
+__device__ __forceinline__ int dq_row(int tid) {
+    const int g16 = tid >> 4;
+    return 4 * (g16 >> 1) + (g16 & 1) + 2 * ((tid >> 3) & 1);
+}
+template <int KIND> struct Held { uint4 c0, c1; uint32_t meta, rcode, rmeta; };
+
+template <int KIND>
+__device__ __forceinline__ Held<KIND> read_staged(const uint8_t* st, int tid) {
+    using C = Cfg<KIND>;
+    const int row = dq_row(tid), part = tid & 7;
+    Held<KIND> h;
+    if constexpr (KIND == KIND_C4R4) {
+        h.c0 = *reinterpret_cast<const uint4*>(st + row * 256 + part * 32);
+        h.c1 = *reinterpret_cast<const uint4*>(st + row * 256 + part * 32 + 16);
+    } else {
+        h.c0 = *reinterpret_cast<const uint4*>(st + row * 128 + part * 16);
+        h.c1 = make_uint4(0u, 0u, 0u, 0u);
+    }
+    h.meta = *reinterpret_cast<const uint32_t*>(st + C::meta + row * 32 + part * 4);
+    h.rcode = *reinterpret_cast<const uint32_t*>(st + C::rcodes + row * 32 + part * 4);
+    h.rmeta = *reinterpret_cast<const uint32_t*>(st + C::rmeta + row * 4);
+    return h;
 }
 
-// Thread t: tile row (t >> 3) and part (t & 7); the part is one content group
-// of 64 channels (8 chunks) plus one RoPE chunk of 8 channels.
 template <int KIND>
-__device__ __forceinline__ void dequant_tile(const uint8_t* stage, uint8_t* tile, int nvalid, int tid) {
-    const int row = tid >> 3;
-    const int part = tid & 7;
-    uint4 w[9];
-    if constexpr (KIND == KIND_BF16) {
-        const uint4* src = reinterpret_cast<const uint4*>(stage + row * 1152);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) w[j] = bf16x8_to_f16(src[part * 8 + j]);
-        w[8] = bf16x8_to_f16(src[64 + part]);
-    } else {
-        using S = Staging<KIND>;
-        f16x2 zz, ss;
-        meta_to_f16(*reinterpret_cast<const uint32_t*>(stage + S::meta + row * 32 + part * 4), zz, ss);
+__device__ __forceinline__ void dequant_chunk(const Held<KIND>& h, int j, uint8_t* tile, int tid) {
+    const int row = dq_row(tid), part = tid & 7;
+    f16x2 zz, ss;
+    uint4 w;
+    if (j < 8) {
+        meta_to_f16(h.meta, zz, ss);
         if constexpr (KIND == KIND_C4R4) {
-            const uint4 c0 = *reinterpret_cast<const uint4*>(stage + row * 256 + part * 32);
-            const uint4 c1 = *reinterpret_cast<const uint4*>(stage + row * 256 + part * 32 + 16);
-            const uint32_t cw[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
-#pragma unroll
-            for (int j = 0; j < 8; ++j) w[j] = codes4_to_f16(cw[j], zz, ss);
+            const uint32_t cw[8] = {h.c0.x, h.c0.y, h.c0.z, h.c0.w, h.c1.x, h.c1.y, h.c1.z, h.c1.w};
+            w = codes4_to_f16(cw[j], zz, ss);
         } else {
-            const uint4 c0 = *reinterpret_cast<const uint4*>(stage + row * 128 + part * 16);
-            const uint32_t cw[4] = {c0.x, c0.y, c0.z, c0.w};
-#pragma unroll
-            for (int j = 0; j < 8; ++j) w[j] = codes2_to_f16(cw[j >> 1] >> (16 * (j & 1)), zz, ss);
+            const uint32_t cw[4] = {h.c0.x, h.c0.y, h.c0.z, h.c0.w};
+            w = codes2_to_f16(cw[j >> 1] >> (16 * (j & 1)), zz, ss);
         }
-        f16x2 rz, rs;
-        meta_to_f16(*reinterpret_cast<const uint32_t*>(stage + S::rmeta + row * 4), rz, rs);
-        w[8] = codes4_to_f16(*reinterpret_cast<const uint32_t*>(stage + S::rcodes + row * 32 + part * 4), rz, rs);
+    } else {
+        meta_to_f16(h.rmeta, zz, ss);
+        w = codes4_to_f16(h.rcode, zz, ss);
     }
-    const bool ok = row < nvalid;
+    const int chunk = j < 8 ? part * 8 + j : 64 + part;
+    *reinterpret_cast<uint4*>(tile + row_off(Cfg<KIND>::SC, row) + 16 * phys_chunk(true, chunk)) = w;
+}
+
+template <int KIND>
+__device__ __forceinline__ void dequant_tile(const uint8_t* st, uint8_t* tile, int tid) {
+    const Held<KIND> h = read_staged<KIND>(st, tid);
 #pragma unroll
-    for (int j = 0; j < 9; ++j) {
-        const int chunk = j < 8 ? part * 8 + j : 64 + part;
-        *reinterpret_cast<uint4*>(tile + chunk_off(row, chunk)) = ok ? w[j] : make_uint4(0u, 0u, 0u, 0u);
-    }
+    for (int j = 0; j < 9; ++j) dequant_chunk<KIND>(h, j, tile, tid);
 }
 
 // ---------------------------------------------------------------------------
 template <int KIND>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void decode_kernel(DecodeArgs a) {
+    using C = Cfg<KIND>;
+    using OpT = std::conditional_t<C::lowbit, f16x8, bf16x8>;
+    constexpr int kDqKind = C::lowbit ? KIND : KIND_C4R4;     // unused by the BF16 kernel
     __shared__ __attribute__((aligned(1024))) uint8_t smem[lds_bytes<KIND>()];
-    uint8_t* tiles = smem;                              // 2 x kTileBytes
-    uint8_t* stages = smem + 2 * kTileBytes;            // 2 x Staging::bytes
-    constexpr int kStage = Staging<KIND>::bytes;
+    constexpr int kTileBytes = tile_bytes<KIND>();
+    uint8_t* tiles = smem;                              // NT x kTileBytes
+    uint8_t* stages = smem + C::NT * kTileBytes;        // NS x stage_bytes (low-bit only)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -310,8 +456,27 @@ void decode_kernel(DecodeArgs a) {
     const int lim = row_ok ? min(L - a.s_q + qi + 1, t_end) : t_begin;   // keys t < lim are visible
     const int full_lim = min(L - a.s_q + 1, t_end);    // every valid row sees keys t < full_lim
 
-    // queries as fp16 B operands: k-step kk holds channels 16kk + 8*half .. +8
-    f16x8 qf[kKSteps];
+    // page of tile j (the table entry clamped into the pool; uniform)
+    const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_pages;
+    auto stage = [&](int j) {
+        int pid = load_page_id(bt, (t_begin + j * kTile) / P);
+        pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
+        const uint8_t* page = a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
+        const int t0 = t_begin + j * kTile;
+        const int nvalid = min(t_end - t0, kTile);
+        if constexpr (C::lowbit)
+            stage_lowbit<KIND>(page, t0 % P, nvalid, a.g, stages + slot_offset(j, C::NS, C::stage_bytes), wave, lane);
+        else
+            stage_bf16(page, t0 % P, nvalid, tiles + slot_offset(j, C::NT, kTileBytes), wave, lane);
+    };
+
+    // prologue part 1: staging of the first D tiles
+#pragma unroll
+    for (int j = 0; j < C::D; ++j)
+        if (j < n_tiles) stage(j);
+
+    // queries as B operands: k-step kk holds channels 16kk + 8*half .. +8
+    OpT qf[kKSteps];
     {
         const int64_t qrow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
         const uint16_t* ql = a.q_lat + qrow * kDc + 8 * half;
@@ -320,17 +485,13 @@ void decode_kernel(DecodeArgs a) {
         for (int kk = 0; kk < kKSteps; ++kk) {
             // rows past the end read row 0 of the sequence; they are never stored
             const uint4 v = *reinterpret_cast<const uint4*>(kk < 32 ? ql + 16 * kk : qr + 16 * (kk - 32));
-            qf[kk] = __builtin_bit_cast(f16x8, bf16x8_to_f16(v));
+            if constexpr (C::lowbit)
+                qf[kk] = __builtin_bit_cast(f16x8, make_uint4(bf16x2_to_f16x2(v.x), bf16x2_to_f16x2(v.y),
+                                                              bf16x2_to_f16x2(v.z), bf16x2_to_f16x2(v.w)));
+            else
+                qf[kk] = __builtin_bit_cast(bf16x8, v);
         }
     }
-
-    auto tile_page = [&](int it, int& po) {
-        const int t0 = t_begin + it * kTile;
-        int pid = a.block_table[static_cast<int64_t>(b) * a.max_pages + t0 / P];
-        pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
-        po = t0 % P;
-        return a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
-    };
 
     // per-lane addressing of the transposing V^T reads: lane (group g, index i)
     // supplies the address of tile row k0 + i/4, channels n0 + 4(i%4) .. +3
@@ -347,57 +508,57 @@ void decode_kernel(DecodeArgs a) {
     f32x16 acc[16];
 #pragma unroll
     for (int m = 0; m < 16; ++m) acc[m] = f32x16{};
+    OpT pb_prev[2] = {OpT{}, OpT{}};   // weights of the previous tile (P^T operands)
 
-    {
-        // prologue: stage tiles 0 and 1, dequantize tile 0
-        int po;
-        if (n_tiles > 0) {
-            const uint8_t* pg = tile_page(0, po);
-            stage_tile<KIND>(pg, po, a.g, stages, wave, lane);
-        }
-        if (n_tiles > 1) {
-            const uint8_t* pg = tile_page(1, po);
-            stage_tile<KIND>(pg, po, a.g, stages + kStage, wave, lane);
-        }
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (n_tiles > 0) dequant_tile<KIND>(stages, tiles, t_end - t_begin, tid);
+    // One pipeline step.  QK: scores and softmax of tile `it` (low-bit: plus
+    // the dequantization of tile it+1); PV: aggregation of tile it-1.
+    auto step = [&](const int it, auto QK, auto PV) __attribute__((always_inline)) {
+        constexpr bool kQK = decltype(QK)::value, kPV = decltype(PV)::value;
+        // the previous step issued Cfg::loads staging loads iff it staged;
+        // everything older must have landed
+        if (it > 0 && it + C::D - 1 < n_tiles) step_barrier<C::loads>();
+        else step_barrier<0>();
+        if (it + C::D < n_tiles) stage(it + C::D);
 
-        for (int it = 0; it < n_tiles; ++it) {
-            __builtin_amdgcn_s_waitcnt(0);   // this thread's staging of tile it+1 has landed
-            __syncthreads();                 // tile it is in LDS; staging it+1 complete; tile (it+1)&1 free
-            if (it + 2 < n_tiles) {
-                const uint8_t* pg = tile_page(it + 2, po);
-                stage_tile<KIND>(pg, po, a.g, stages + (it & 1) * kStage, wave, lane);
-            }
-            const uint8_t* kt = tiles + (it & 1) * kTileBytes;
-            const int t0 = t_begin + it * kTile;
-
+        f32x16 s = f32x16{};
+        float nref = 0.0f;
+        if constexpr (kQK) {
+            const uint8_t* kt = tiles + slot_offset(it, C::NT, kTileBytes);
             // every wave computes, also one whose rows all lie past the end
             // (its results are never stored): a branch here would force the
             // accumulators through a register-class join.
-            // scores S^T[token][row], K = 576 in 36 steps
-            // The operand reads run kAhead steps ahead of the matrix
-            // instructions; the group barriers pin that order (left alone, the
-            // scheduler issues each read right before its use and the chain
-            // waits on LDS latency at every step).
-            f32x16 s = f32x16{};
-            const uint8_t* krow = kt + chunk_off(qk_row, half);
+            // Scores S^T[token][row], K = 576 in 36 steps, the operand reads
+            // kAhead steps ahead of the matrix instructions.  Low-bit: the nine
+            // chunk steps of the next tile's dequantization (reading staging
+            // buffer (it+1) % NS, writing tile buffer (it+1) % NT, which the
+            // aggregation of tile it-2 released before this step's barrier)
+            // fill the matrix pipe's shadow.
+            Held<kDqKind> held{};
+            uint8_t* next_tile = tiles + slot_offset(it + 1, C::NT, kTileBytes);
+            if constexpr (C::lowbit) held = read_staged<kDqKind>(stages + slot_offset(it + 1, C::NS, C::stage_bytes), tid);
+            // k-step kk reads logical chunk 2kk + half: physical 2kk + half (+ kk/4 grouped)
+            const uint8_t* krow = kt + row_off(C::SC, qk_row) + 16 * half;
+            auto kread_off = [](int kk) { return 16 * (2 * kk + (C::grouped ? kk >> 2 : 0)); };
             constexpr int kAhead = 3;
-            f16x8 kb[kAhead];
+            OpT kb[kAhead];
 #pragma unroll
-            for (int j = 0; j < kAhead; ++j) kb[j] = *reinterpret_cast<const f16x8*>(krow + 32 * j);
-            __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);             // LDS reads
+            for (int j = 0; j < kAhead; ++j) kb[j] = *reinterpret_cast<const OpT*>(krow + kread_off(j));
+            // Scheduling barriers after every k-step keep this order (left
+            // free, the scheduler trades the read-ahead for registers and every
+            // product then waits on LDS latency).
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kk = 0; kk < kKSteps; ++kk) {
-                const f16x8 k = kb[kk % kAhead];
-                if (kk + kAhead < kKSteps) kb[kk % kAhead] = *reinterpret_cast<const f16x8*>(krow + 32 * (kk + kAhead));
-                s = __builtin_amdgcn_mfma_f32_32x32x16_f16(k, qf[kk], s, 0, 0, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // one MFMA
-                if (kk + kAhead < kKSteps) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                s = mfma(kb[kk % kAhead], qf[kk], s);
+                if (kk + kAhead < kKSteps) kb[kk % kAhead] = *reinterpret_cast<const OpT*>(krow + kread_off(kk + kAhead));
+                if constexpr (C::lowbit) {
+                    if (kk % 4 == 2) dequant_chunk<kDqKind>(held, kk / 4, next_tile, tid);
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
             // rows see every key of the tile except in the last tile of the
             // range or the tile holding the newest key (block-uniform test)
+            const int t0 = t_begin + it * kTile;
             if (t0 + kTile > full_lim) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
@@ -405,6 +566,9 @@ void decode_kernel(DecodeArgs a) {
                     s[v] = t < lim ? s[v] : -INFINITY;
                 }
             }
+            // softmax of tile it: the reference first (and, rarely, the move of
+            // the accumulators to a new one), then the weights, which are
+            // interleaved below with the aggregation of tile it-1
             float mr = s[0];
 #pragma unroll
             for (int v = 1; v < 16; ++v) mr = fmaxf(mr, s[v]);
@@ -412,58 +576,83 @@ void decode_kernel(DecodeArgs a) {
             const float mt = mr * a.scale_log2;           // scale > 0: max commutes
             m_true = fmaxf(m_true, mt);
             if (m_ref == -INFINITY) m_ref = mt;          // first visible key: nothing accumulated yet
-            if (__builtin_amdgcn_ballot_w64(mt > m_ref + kRefSlack) != 0) {
-                const float m_new = fmaxf(m_ref, mt);     // finite for every row that needs it
-                const float alpha = exp2f(m_ref - m_new); // 1 for the other rows
+            if constexpr (kPV) {
+                if (__builtin_amdgcn_ballot_w64(mt > m_ref + kRefSlack) != 0) {
+                    // the accumulators and the pending weights of tile it-1
+                    // move to the new reference (a second fp16 rounding of
+                    // those weights; alpha < 2^-10 for the rows that move)
+                    const float m_new = fmaxf(m_ref, mt);     // finite for every row that needs it
+                    const float alpha = __builtin_amdgcn_exp2f(m_ref - m_new);   // 1 for the other rows
 #pragma unroll
-                for (int m = 0; m < 16; ++m) scale_acc(acc[m], alpha);
-                l_run *= alpha;
-                m_ref = m_new;
+                    for (int m = 0; m < 16; ++m) scale_acc(acc[m], alpha);
+                    const OpT av = OpT{} + static_cast<typename std::remove_reference_t<decltype(pb_prev[0][0])>>(alpha);
+                    pb_prev[0] *= av;
+                    pb_prev[1] *= av;
+                    l_run *= alpha;
+                    m_ref = m_new;
+                }
             }
-            const float nref = m_ref == -INFINITY ? 0.0f : -m_ref;
-            uint32_t pw[8];
+            nref = m_ref == -INFINITY ? 0.0f : -m_ref;
+        }
+        // weights of tile it, two per piece: spread over the aggregation of
+        // tile it-1 when there is one
+        uint32_t pw[8];
+        auto weights = [&](int v2) __attribute__((always_inline)) {
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2], a.scale_log2, nref));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2 + 1], a.scale_log2, nref));
+            l_run += p0 + p1;
+            pw[v2] = C::lowbit ? pack_f16x2(p0, p1) : pack_bf16x2(p0, p1);
+        };
+        if constexpr (kQK && !kPV) {
 #pragma unroll
-            for (int v = 0; v < 16; v += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(fmaf(s[v], a.scale_log2, nref));
-                const float p1 = __builtin_amdgcn_exp2f(fmaf(s[v + 1], a.scale_log2, nref));
-                l_run += p0 + p1;
-                pw[v >> 1] = pack_f16x2(p0, p1);
-            }
-            const f16x8 pb0 = __builtin_bit_cast(f16x8, make_uint4(pw[0], pw[1], pw[2], pw[3]));
-            const f16x8 pb1 = __builtin_bit_cast(f16x8, make_uint4(pw[4], pw[5], pw[6], pw[7]));
-
-            // latent aggregation O^T[channel][row] += V^T . P^T; the V^T operand
-            // is read transposed from the token-major tile
-            const uint8_t* vbase = kt + chunk_off(tr_kbase, 0) + 2 * tr_col;
-            auto vread = [&](int step) __attribute__((always_inline)) {
-                const int ks = step >> 4, m = step & 15;
-                const uint8_t* p = vbase + (16 * ks) * kRowBytes + 64 * m;
+            for (int v2 = 0; v2 < 8; ++v2) weights(v2);
+        }
+        if constexpr (kPV) {
+            // latent aggregation of tile it-1: O^T[channel][row] += V^T . P^T;
+            // the V^T operand is read transposed from the token-major tile
+            const uint8_t* vt = tiles + slot_offset(it + C::NT - 1, C::NT, kTileBytes);
+            // rows tr_kbase + 16 ks (+ 8): the row shift term of row + 8 is that of
+            // row + 2 (tr_kbase < 8), of row + 16 that of the row itself;
+            // channels 32 m + tr_col .. : logical chunk 4m + (0..3), physical
+            // + m/2 in the grouped layout
+            const uint8_t* vbase = vt + row_off(C::SC, tr_kbase) + 2 * tr_col;
+            auto vread = [&](int stp) __attribute__((always_inline)) {
+                const int ks = stp >> 4, m = stp & 15;
+                const uint8_t* p = vbase + 16 * C::SC * 16 * ks + 64 * m + (C::grouped ? 16 * (m >> 1) : 0);
                 const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
-                const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * kRowBytes));
-                return __builtin_bit_cast(f16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+                const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 16 * C::SC * 8 + 32));
+                return __builtin_bit_cast(OpT, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
             };
             constexpr int kVAhead = 2;
-            f16x8 vb[kVAhead];
+            OpT vb[kVAhead];
 #pragma unroll
             for (int j = 0; j < kVAhead; ++j) vb[j] = vread(j);
-            __builtin_amdgcn_sched_group_barrier(0x100, 2 * kVAhead, 0);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int step = 0; step < 32; ++step) {
-                const f16x8 va = vb[step % kVAhead];
-                if (step + kVAhead < 32) vb[step % kVAhead] = vread(step + kVAhead);
-                const int m = step & 15;
-                acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, step < 16 ? pb0 : pb1, acc[m], 0, 0, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                if (step + kVAhead < 32) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            for (int stp = 0; stp < 32; ++stp) {
+                const int m = stp & 15;
+                acc[m] = mfma(vb[stp % kVAhead], pb_prev[stp >> 4], acc[m]);
+                if (stp + kVAhead < 32) vb[stp % kVAhead] = vread(stp + kVAhead);
+                if constexpr (kQK) {
+                    if (stp % 2 == 1 && stp < 16) weights(stp >> 1);
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
-            // keep the unpacking of the next tile out of the operand loads of
-            // this one: interleaving them overflows the register file
-            __builtin_amdgcn_sched_barrier(0);
-            if (it + 1 < n_tiles)
-                dequant_tile<KIND>(stages + ((it + 1) & 1) * kStage, tiles + ((it + 1) & 1) * kTileBytes,
-                                   t_end - t_begin - (it + 1) * kTile, tid);
-            __builtin_amdgcn_sched_barrier(0);
         }
+        if constexpr (kQK) {
+            pb_prev[0] = __builtin_bit_cast(OpT, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+            pb_prev[1] = __builtin_bit_cast(OpT, make_uint4(pw[4], pw[5], pw[6], pw[7]));
+        }
+    };
+    if (n_tiles > 0) {
+        // prologue part 2: tile 0 decoded (low-bit) before the first step
+        if constexpr (C::lowbit) {
+            step_barrier<0>();
+            dequant_tile<kDqKind>(stages, tiles, tid);
+        }
+        step(0, std::true_type{}, std::false_type{});
+        for (int it = 1; it < n_tiles; ++it) step(it, std::true_type{}, std::true_type{});
+        step(n_tiles, std::false_type{}, std::true_type{});
     }
 
     if (!row_ok) return;
