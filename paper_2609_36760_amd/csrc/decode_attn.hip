@@ -19,12 +19,13 @@
 //   1. its packed bytes (code and metadata regions of the page) are copied
 //      HBM -> LDS by direct-to-LDS loads (global_load_lds_dwordx4) three tiles
 //      ahead of use, every wave issuing the same number of loads so that one
-//      counted wait covers a tile; the page id comes from a load issued one
-//      tile earlier.  Rows past the end of the range re-read the range's last
-//      token, so every staged row decodes to finite values;
+//      counted wait covers a tile; the page id is fetched through the scalar
+//      cache while the workgroup waits at the step barrier.  Rows past the
+//      end of the range re-read the range's last token, so every staged row
+//      decodes to finite values;
 //   2. all 256 threads unpack and dequantize them with packed fp16 math into a
-//      token-major fp16 tile [32][576] (rows padded by 32 bytes to spread LDS
-//      banks);
+//      token-major fp16 tile [32][576] (the bank-conflict-free layout of
+//      tile_bytes below);
 //   3. scores: every wave computes S^T[token][row] = K_tile . Q^T with
 //      v_mfma_f32_32x32x16_f16 (M = 32 tokens, N = its 32 rows, K = 576), the
 //      rows' queries held in registers as the B operand.  A lane then holds
@@ -38,9 +39,11 @@
 // Software pipeline.  With one wave per SIMD no other wave hides a wave's
 // latencies, so every step interleaves independent work explicitly:
 //   step j:  scores of tile j   ||  dequantization of tile j+1
-//            softmax of tile j  ||  latent aggregation of tile j-1
+//            softmax of tile j  ||  latent aggregation of tile j-1 (and the
+//                                   staging of tile j+3)
 // (the aggregation trails the scores by one tile: three fp16 tile buffers,
-// three staging buffers).  Group barriers pin the interleaving.
+// three staging buffers).  Scheduling barriers after every matrix
+// instruction pin the interleaving.
 //
 // The BF16-cache kernel stages raw bf16 rows straight into padded tile
 // buffers (four of them; staging distance two tiles) and runs the same steps
@@ -56,9 +59,11 @@
 // (its maximum so far, log2 units) and the weights p = 2^(x - ref) stay below
 // 2^10 (well inside fp16).  Only when a tile's maximum exceeds the reference by
 // more than that slack does the wave move its rows to a new reference -- rare
-// after the first tiles.  The accumulators are then rescaled once the trailing
-// aggregation (still on the old reference) has been added, in place in their
-// registers (the compiler would otherwise stage all 256 of them through vector
+// after the first tiles.  The tile's weights are then computed on the new
+// reference, and the accumulators follow in the next step, just before that
+// tile is aggregated (after the aggregation of the previous tile, still on the
+// old reference).  The rescale reads and writes the accumulator registers in
+// place (the compiler would otherwise stage all 256 of them through vector
 // registers at the branch).  The true maximum is tracked separately for the
 // split partials.
 #include <hip/hip_runtime.h>
@@ -158,7 +163,16 @@ __device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
     return pack_f16x2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
 }
 
-__device__ __forceinline__ float swap_halves(float v) { return __shfl_xor(v, 32, 64); }
+// max / sum of a value and its copy in lane ^ 32 (v_permlane32_swap hands each
+// lane the pair {own value, partner's value} in its two results)
+__device__ __forceinline__ float max_halves(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 // Byte offset of buffer (j mod n) of `bytes` bytes, as an opaque scalar: the
 // compiler then forms every LDS address as one per-lane base plus this offset
@@ -215,19 +229,26 @@ __device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
 }
 
 // Wait until at most N direct-to-LDS loads of this wave are in flight and all
-// of its LDS accesses are done, then synchronize the workgroup.
+// of its LDS accesses are done, then synchronize the workgroup.  Also fetches
+// a page-table entry through the scalar cache (one cache line holds the ids
+// of 16 consecutive pages): its latency hides behind the barrier, and the
+// value is complete when the statement ends.
 template <int N>
-__device__ __forceinline__ void step_barrier() {
+__device__ __forceinline__ int step_barrier(const int32_t* table, int index) {
     static_assert(N >= 0 && N < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+    int v;
+    asm volatile("s_load_dword %0, %1, %2\n\ts_waitcnt vmcnt(%3) lgkmcnt(0)\n\ts_barrier"
+                 : "=&s"(v)
+                 : "s"(table), "s"(__builtin_amdgcn_readfirstlane(index * 4)), "n"(N)
+                 : "memory");
+    return v;
 }
 
-// A page-table entry through the scalar cache (one cache line holds the ids
-// of 16 consecutive pages), waited for on the spot.
+// The same entry, waited for on the spot.
 __device__ __forceinline__ int load_page_id(const int32_t* table, int index) {
     int v;
     asm volatile("s_load_dword %0, %1, %2\n\ts_waitcnt lgkmcnt(0)"
-                 : "=s"(v)
+                 : "=&s"(v)
                  : "s"(table), "s"(__builtin_amdgcn_readfirstlane(index * 4))
                  : "memory");
     return v;
@@ -240,20 +261,18 @@ __device__ __forceinline__ int load_page_id(const int32_t* table, int index) {
 // issues Cfg::loads loads).  Tokens at or past `nvalid` re-read token
 // nvalid - 1 (per-token regions; a RoPE metadata chunk holds four tokens and
 // is read as it is -- such a token's score is masked and its RoPE channels
-// never enter the aggregation).
+// never enter the aggregation).  Load `k` of the Cfg::loads.
 template <int KIND>
-__device__ __forceinline__ void stage_lowbit(const uint8_t* page, int po, int nvalid, const PageGeom& g,
-                                             uint8_t* st, int wave, int lane) {
+__device__ __forceinline__ void stage_lowbit(int k, const uint8_t* page, int po, int nvalid, const PageGeom& g,
+                                             uint32_t st_lds, int wave, int wave_u, int lane) {
     using C = Cfg<KIND>;
     constexpr int cpt = C::cc / 16;                     // chunks per token
     static_assert(C::code_rounds * kThreads * 16 == C::rcodes, "content codes fill whole rounds");
-    const uint32_t st_lds = lds_addr(st);
-    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-#pragma unroll
-    for (int r = 0; r < C::code_rounds; ++r) {
-        const int i = r * kThreads + wave * 64 + lane;
+    if (k < C::code_rounds) {
+        const int i = k * kThreads + wave * 64 + lane;
         const int tok = min(i / cpt, nvalid - 1);
-        dma16(page, (po + tok) * C::cc + (i % cpt) * 16, st_lds + (r * kThreads + wave_u * 64) * 16);
+        dma16(page, (po + tok) * C::cc + (i % cpt) * 16, st_lds + (k * kThreads + wave_u * 64) * 16);
+        return;
     }
     const int tok2 = min(lane >> 1, nvalid - 1);
     int src_off, dst_off;
@@ -273,26 +292,21 @@ __device__ __forceinline__ void stage_lowbit(const uint8_t* page, int po, int nv
 // Raw bf16 rows into a tile of the plain layout (SC = 76): LDS chunk i of the
 // tile belongs to row r (the last row starting at or before i) and column
 // i - start(r); columns 72.. are padding and receive column 71 again.  Tokens
-// at or past `nvalid` re-read token nvalid - 1.  Rounds 0..8 cover chunks
-// 0..2303 (chunk i by lane i % 64 of wave (i / 64) % 4); round 9 covers
+// at or past `nvalid` re-read token nvalid - 1.  Loads 0..8 cover chunks
+// 0..2303 (chunk i by lane i % 64 of wave (i / 64) % 4); load 9 covers
 // 2304..2431 with waves 0/2 and 1/3 loading the same chunks (same data to the
 // same place), so that all waves issue the same number of loads.
-__device__ __forceinline__ void stage_bf16(const uint8_t* page, int po, int nvalid, uint8_t* tile, int wave,
-                                           int lane) {
+__device__ __forceinline__ void stage_bf16(int k, const uint8_t* page, int po, int nvalid, uint32_t tile_lds,
+                                           int wave, int wave_u, int lane) {
     constexpr int sc = 76;
-    const uint32_t tile_lds = lds_addr(tile);
-    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-#pragma unroll
-    for (int r = 0; r < 10; ++r) {
-        const int base = r < 9 ? r * kThreads + wave * 64 : 2304 + 64 * (wave & 1);
-        const int i = base + lane;
-        int row = static_cast<int>((static_cast<unsigned>(i) * 3450u) >> 18);   // i / 76 for i < 2432
-        if (i < row_off(sc, row) / 16) --row;
-        const int col = min(i - row_off(sc, row) / 16, 71);
-        const int tok = min(row, nvalid - 1);
-        const int base_u = r < 9 ? r * kThreads + wave_u * 64 : 2304 + 64 * (wave_u & 1);
-        dma16(page, (po + tok) * 1152 + col * 16, tile_lds + base_u * 16);
-    }
+    const int base = k < 9 ? k * kThreads + wave * 64 : 2304 + 64 * (wave & 1);
+    const int i = base + lane;
+    int row = static_cast<int>((static_cast<unsigned>(i) * 3450u) >> 18);   // i / 76 for i < 2432
+    if (i < row_off(sc, row) / 16) --row;
+    const int col = min(i - row_off(sc, row) / 16, 71);
+    const int tok = min(row, nvalid - 1);
+    const int base_u = k < 9 ? k * kThreads + wave_u * 64 : 2304 + 64 * (wave_u & 1);
+    dma16(page, (po + tok) * 1152 + col * 16, tile_lds + base_u * 16);
 }
 
 // ---------------------------------------------------------------------------
@@ -309,90 +323,119 @@ __device__ __forceinline__ void meta_to_f16(uint32_t meta, f16x2& zz, f16x2& ss)
     ss = f16x2{s, s};
 }
 
-// 8 four-bit codes (channel 2j in the low nibble of byte j) -> 4 fp16 pairs.
-__device__ __forceinline__ uint4 codes4_to_f16(uint32_t w, f16x2 zz, f16x2 ss) {
-    const uint32_t lo = w & 0x0F0F0F0Fu;          // channels 0, 2, 4, 6
-    const uint32_t hi = (w >> 4) & 0x0F0F0F0Fu;   // channels 1, 3, 5, 7
-    uint32_t o[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        // bytes [lo.b_k, 0, hi.b_k, 0]
-        const uint32_t sel = static_cast<uint32_t>(k) | 0x0C000C00u | (static_cast<uint32_t>(4 + k) << 16);
-        const uint32_t pair = __builtin_amdgcn_perm(hi, lo, sel) | 0x64006400u;
-        o[k] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, pair) - zz) * ss);
-    }
-    return make_uint4(o[0], o[1], o[2], o[3]);
-}
-
-// 8 two-bit codes (channel 4j+k in bits 2k..2k+1 of byte j), low 16 bits of w.
-__device__ __forceinline__ uint4 codes2_to_f16(uint32_t w, f16x2 zz, f16x2 ss) {
-    uint32_t o[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {          // pair k: channels 2k, 2k+1
-        const uint32_t sh = 4 * k;
-        const uint32_t pair = ((w >> sh) & 3u) | (((w >> (sh + 2)) & 3u) << 16) | 0x64006400u;
-        o[k] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, pair) - zz) * ss);
-    }
-    return make_uint4(o[0], o[1], o[2], o[3]);
-}
-
 // Thread t dequantizes part (t & 7) -- one content group of 64 channels (8
 // chunks) plus one RoPE chunk of 8 channels -- of tile row dq_row(t); the
 // eight threads of a row and the row two further on share a 16-lane store
-// group (conflict-free in the grouped layout).  Split in two: the staged bytes
-// a thread needs (read at the start of a step) and nine chunk steps
-// (arithmetic plus one 16-byte store each) spread over the score products.
+// group (conflict-free in the grouped layout).
+//
+// The 36 fp16 pairs (chunk j, pair p; task 4j + p) go through four stages --
+// A unpack, B bias, C subtract the biased zero, D scale (and store the chunk
+// after its last pair) -- one stage per k-step of the score products, task t
+// in stage A at step t: a step runs four independent operations (stages of
+// four different tasks), which issue without waiting on each other while the
+// matrix pipe works.  Steps 0..38; the staged bytes are read, and chunk 0's
+// code word split, before step 0.
 __device__ __forceinline__ int dq_row(int tid) {
     const int g16 = tid >> 4;
     return 4 * (g16 >> 1) + (g16 & 1) + 2 * ((tid >> 3) & 1);
 }
-template <int KIND> struct Held { uint4 c0, c1; uint32_t meta, rcode, rmeta; };
+
+template <int KIND> struct Dq {
+    uint4 c0, c1;                   // content codes of the group (c1: 4-bit only)
+    uint32_t meta, rcode, rmeta;    // content {scale, zero}, RoPE codes, RoPE {scale, zero}
+    f16x2 zz, ss, rz, rs;           // metadata as fp16 (zero + 1024, scale)
+    uint32_t lo[2], hi[2];          // nibbles of the 4-bit code words of chunks j (index j & 1)
+    uint32_t pr[4];                 // pairs in flight (index task & 3)
+    uint32_t o[4];                  // finished pairs of the chunk being stored
+};
 
 template <int KIND>
-__device__ __forceinline__ Held<KIND> read_staged(const uint8_t* st, int tid) {
+__device__ __forceinline__ void dq_read(Dq<KIND>& d, const uint8_t* st, int tid) {
     using C = Cfg<KIND>;
     const int row = dq_row(tid), part = tid & 7;
-    Held<KIND> h;
     if constexpr (KIND == KIND_C4R4) {
-        h.c0 = *reinterpret_cast<const uint4*>(st + row * 256 + part * 32);
-        h.c1 = *reinterpret_cast<const uint4*>(st + row * 256 + part * 32 + 16);
+        d.c0 = *reinterpret_cast<const uint4*>(st + row * 256 + part * 32);
+        d.c1 = *reinterpret_cast<const uint4*>(st + row * 256 + part * 32 + 16);
     } else {
-        h.c0 = *reinterpret_cast<const uint4*>(st + row * 128 + part * 16);
-        h.c1 = make_uint4(0u, 0u, 0u, 0u);
+        d.c0 = *reinterpret_cast<const uint4*>(st + row * 128 + part * 16);
+        d.c1 = make_uint4(0u, 0u, 0u, 0u);
     }
-    h.meta = *reinterpret_cast<const uint32_t*>(st + C::meta + row * 32 + part * 4);
-    h.rcode = *reinterpret_cast<const uint32_t*>(st + C::rcodes + row * 32 + part * 4);
-    h.rmeta = *reinterpret_cast<const uint32_t*>(st + C::rmeta + row * 4);
-    return h;
+    d.meta = *reinterpret_cast<const uint32_t*>(st + C::meta + row * 32 + part * 4);
+    d.rcode = *reinterpret_cast<const uint32_t*>(st + C::rcodes + row * 32 + part * 4);
+    d.rmeta = *reinterpret_cast<const uint32_t*>(st + C::rmeta + row * 4);
+}
+
+// chunk j holds 4-bit codes (channel 2i in the low nibble of byte i)?
+template <int KIND>
+__device__ __forceinline__ constexpr bool dq_is4(int j) { return KIND == KIND_C4R4 || j == 8; }
+
+template <int KIND>
+__device__ __forceinline__ uint32_t dq_word(const Dq<KIND>& d, int j) {
+    if constexpr (KIND == KIND_C4R4) {
+        const uint32_t cw[9] = {d.c0.x, d.c0.y, d.c0.z, d.c0.w, d.c1.x, d.c1.y, d.c1.z, d.c1.w, d.rcode};
+        return cw[j];
+    } else {
+        // 2-bit codes: 8 per 16 bits
+        const uint32_t cw[4] = {d.c0.x, d.c0.y, d.c0.z, d.c0.w};
+        return j < 8 ? cw[j >> 1] >> (16 * (j & 1)) : d.rcode;
+    }
 }
 
 template <int KIND>
-__device__ __forceinline__ void dequant_chunk(const Held<KIND>& h, int j, uint8_t* tile, int tid) {
-    const int row = dq_row(tid), part = tid & 7;
-    f16x2 zz, ss;
-    uint4 w;
-    if (j < 8) {
-        meta_to_f16(h.meta, zz, ss);
-        if constexpr (KIND == KIND_C4R4) {
-            const uint32_t cw[8] = {h.c0.x, h.c0.y, h.c0.z, h.c0.w, h.c1.x, h.c1.y, h.c1.z, h.c1.w};
-            w = codes4_to_f16(cw[j], zz, ss);
-        } else {
-            const uint32_t cw[4] = {h.c0.x, h.c0.y, h.c0.z, h.c0.w};
-            w = codes2_to_f16(cw[j >> 1] >> (16 * (j & 1)), zz, ss);
-        }
-    } else {
-        meta_to_f16(h.rmeta, zz, ss);
-        w = codes4_to_f16(h.rcode, zz, ss);
+__device__ __forceinline__ void dq_split(Dq<KIND>& d, int j) {
+    if (dq_is4<KIND>(j)) {
+        const uint32_t w = dq_word<KIND>(d, j);
+        d.lo[j & 1] = w & 0x0F0F0F0Fu;          // channels 0, 2, 4, 6
+        d.hi[j & 1] = (w >> 4) & 0x0F0F0F0Fu;   // channels 1, 3, 5, 7
     }
-    const int chunk = j < 8 ? part * 8 + j : 64 + part;
-    *reinterpret_cast<uint4*>(tile + row_off(Cfg<KIND>::SC, row) + 16 * phys_chunk(true, chunk)) = w;
+}
+
+template <int KIND>
+__device__ __forceinline__ void dq_step(Dq<KIND>& d, int s, uint8_t* tile, int tid) {
+    if (s == 0) {
+        meta_to_f16(d.meta, d.zz, d.ss);
+        meta_to_f16(d.rmeta, d.rz, d.rs);
+    }
+    if (s >= 3 && s - 3 < 36) {                 // D: scale; store a finished chunk
+        const int t = s - 3, j = t >> 2, p = t & 3;
+        d.o[p] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, d.pr[t & 3]) * (j < 8 ? d.ss : d.rs));
+        if (p == 3) {
+            const int row = dq_row(tid), part = tid & 7;
+            const int chunk = j < 8 ? part * 8 + j : 64 + part;
+            *reinterpret_cast<uint4*>(tile + row_off(Cfg<KIND>::SC, row) + 16 * phys_chunk(true, chunk)) =
+                make_uint4(d.o[0], d.o[1], d.o[2], d.o[3]);
+        }
+    }
+    if (s >= 2 && s - 2 < 36) {                 // C: (1024 + q) - (1024 + zero) = q - zero, exact
+        const int t = s - 2, j = t >> 2;
+        d.pr[t & 3] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, d.pr[t & 3]) - (j < 8 ? d.zz : d.rz));
+    }
+    if (s >= 1 && s - 1 < 36) {                 // B: fp16 bits 0x6400 | q = 1024 + q
+        const int t = s - 1, j = t >> 2;
+        if (dq_is4<KIND>(j)) d.pr[t & 3] |= 0x64006400u;
+    }
+    if (s < 36) {                               // A: unpack pair p of chunk j
+        const int t = s, j = t >> 2, p = t & 3;
+        if (dq_is4<KIND>(j)) {
+            // bytes [lo.b_p, 0, hi.b_p, 0]: channels 2p, 2p+1
+            const uint32_t sel = static_cast<uint32_t>(p) | 0x0C000C00u | (static_cast<uint32_t>(4 + p) << 16);
+            d.pr[t & 3] = __builtin_amdgcn_perm(d.hi[j & 1], d.lo[j & 1], sel);
+        } else {
+            // channel 4i+k in bits 2k..2k+1 of byte i; pair p: channels 2p, 2p+1
+            const uint32_t w = dq_word<KIND>(d, j);
+            d.pr[t & 3] = ((w >> (4 * p)) & 3u) | (((w >> (4 * p + 2)) & 3u) << 16) | 0x64006400u;
+        }
+        if (p == 3 && j + 1 < 9) dq_split<KIND>(d, j + 1);
+    }
 }
 
 template <int KIND>
 __device__ __forceinline__ void dequant_tile(const uint8_t* st, uint8_t* tile, int tid) {
-    const Held<KIND> h = read_staged<KIND>(st, tid);
+    Dq<KIND> d;
+    dq_read<KIND>(d, st, tid);
+    dq_split<KIND>(d, 0);
 #pragma unroll
-    for (int j = 0; j < 9; ++j) dequant_chunk<KIND>(h, j, tile, tid);
+    for (int s = 0; s < 39; ++s) dq_step<KIND>(d, s, tile, tid);
 }
 
 // ---------------------------------------------------------------------------
@@ -456,25 +499,6 @@ void decode_kernel(DecodeArgs a) {
     const int lim = row_ok ? min(L - a.s_q + qi + 1, t_end) : t_begin;   // keys t < lim are visible
     const int full_lim = min(L - a.s_q + 1, t_end);    // every valid row sees keys t < full_lim
 
-    // page of tile j (the table entry clamped into the pool; uniform)
-    const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_pages;
-    auto stage = [&](int j) {
-        int pid = load_page_id(bt, (t_begin + j * kTile) / P);
-        pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
-        const uint8_t* page = a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
-        const int t0 = t_begin + j * kTile;
-        const int nvalid = min(t_end - t0, kTile);
-        if constexpr (C::lowbit)
-            stage_lowbit<KIND>(page, t0 % P, nvalid, a.g, stages + slot_offset(j, C::NS, C::stage_bytes), wave, lane);
-        else
-            stage_bf16(page, t0 % P, nvalid, tiles + slot_offset(j, C::NT, kTileBytes), wave, lane);
-    };
-
-    // prologue part 1: staging of the first D tiles
-#pragma unroll
-    for (int j = 0; j < C::D; ++j)
-        if (j < n_tiles) stage(j);
-
     // queries as B operands: k-step kk holds channels 16kk + 8*half .. +8
     OpT qf[kKSteps];
     {
@@ -493,6 +517,39 @@ void decode_kernel(DecodeArgs a) {
         }
     }
 
+    // Staging.  Tile j is staged into staging slot j % NS (low-bit) or tile
+    // slot j % NT (BF16).  Step it stages tile it + D -- clamped to the last
+    // tile, whose bytes then land once more in a free slot -- so that every
+    // step issues Cfg::loads loads.  Cursor: first token and page-table index
+    // of that tile (uniform).
+    const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_pages;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    auto slot_lds = [&](int j) {
+        return C::lowbit ? lds_addr(stages + slot_offset(j, C::NS, C::stage_bytes))
+                         : lds_addr(tiles + slot_offset(j, C::NT, kTileBytes));
+    };
+    auto issue = [&](int k, int pid, int t0, int j) __attribute__((always_inline)) {
+        pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
+        const uint8_t* page = a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
+        const int nvalid = min(t_end - t0, kTile);
+        if constexpr (C::lowbit)
+            stage_lowbit<KIND>(k, page, t0 % P, nvalid, a.g, slot_lds(j), wave, wave_u, lane);
+        else
+            stage_bf16(k, page, t0 % P, nvalid, slot_lds(j), wave, wave_u, lane);
+    };
+    // prologue: the first D tiles
+#pragma unroll
+    for (int j = 0; j < C::D; ++j) {
+        if (j < n_tiles) {
+            const int t0 = t_begin + j * kTile;
+            const int pid = load_page_id(bt, t0 / P);
+#pragma unroll
+            for (int k = 0; k < C::loads; ++k) issue(k, pid, t0, j);
+        }
+    }
+    int cur_t0 = t_begin + min(C::D, n_tiles - 1) * kTile;     // tile staged by the current step
+    int cur_page = cur_t0 / P;
+
     // per-lane addressing of the transposing V^T reads: lane (group g, index i)
     // supplies the address of tile row k0 + i/4, channels n0 + 4(i%4) .. +3
     // and receives rows k0 .. k0+3 of channel n0 + i
@@ -509,33 +566,39 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
     for (int m = 0; m < 16; ++m) acc[m] = f32x16{};
     OpT pb_prev[2] = {OpT{}, OpT{}};   // weights of the previous tile (P^T operands)
+    bool move_pending = false;         // the previous tile moved the reference:
+    float alpha_pending = 1.0f;        // accumulators *= alpha before its aggregation
 
     // One pipeline step.  QK: scores and softmax of tile `it` (low-bit: plus
-    // the dequantization of tile it+1); PV: aggregation of tile it-1.
+    // the dequantization of tile it+1) and the staging of tile it+D; PV:
+    // aggregation of tile it-1.
     auto step = [&](const int it, auto QK, auto PV) __attribute__((always_inline)) {
         constexpr bool kQK = decltype(QK)::value, kPV = decltype(PV)::value;
-        // the previous step issued Cfg::loads staging loads iff it staged;
-        // everything older must have landed
-        if (it > 0 && it + C::D - 1 < n_tiles) step_barrier<C::loads>();
-        else step_barrier<0>();
-        if (it + C::D < n_tiles) stage(it + C::D);
+        // The previous step issued Cfg::loads staging loads (none before step
+        // 0: the prologue's must all land); everything older must have landed.
+        int pid = 0;
+        if (it == 0) pid = step_barrier<0>(bt, cur_page);
+        else pid = step_barrier<C::loads>(bt, cur_page);
+        const int stage_j = it + C::D;
 
         f32x16 s = f32x16{};
-        float nref = 0.0f;
         if constexpr (kQK) {
             const uint8_t* kt = tiles + slot_offset(it, C::NT, kTileBytes);
             // every wave computes, also one whose rows all lie past the end
             // (its results are never stored): a branch here would force the
             // accumulators through a register-class join.
             // Scores S^T[token][row], K = 576 in 36 steps, the operand reads
-            // kAhead steps ahead of the matrix instructions.  Low-bit: the nine
-            // chunk steps of the next tile's dequantization (reading staging
-            // buffer (it+1) % NS, writing tile buffer (it+1) % NT, which the
-            // aggregation of tile it-2 released before this step's barrier)
-            // fill the matrix pipe's shadow.
-            Held<kDqKind> held{};
+            // kAhead steps ahead of the matrix instructions.  Low-bit: the 36
+            // pieces of the next tile's dequantization (reading staging slot
+            // (it+1) % NS, writing tile slot (it+1) % NT, which the aggregation
+            // of tile it-2 released before this step's barrier) fill the
+            // matrix pipe's shadow, one per k-step.
+            Dq<kDqKind> dq;
             uint8_t* next_tile = tiles + slot_offset(it + 1, C::NT, kTileBytes);
-            if constexpr (C::lowbit) held = read_staged<kDqKind>(stages + slot_offset(it + 1, C::NS, C::stage_bytes), tid);
+            if constexpr (C::lowbit) {
+                dq_read<kDqKind>(dq, stages + slot_offset(it + 1, C::NS, C::stage_bytes), tid);
+                dq_split<kDqKind>(dq, 0);
+            }
             // k-step kk reads logical chunk 2kk + half: physical 2kk + half (+ kk/4 grouped)
             const uint8_t* krow = kt + row_off(C::SC, qk_row) + 16 * half;
             auto kread_off = [](int kk) { return 16 * (2 * kk + (C::grouped ? kk >> 2 : 0)); };
@@ -551,10 +614,12 @@ void decode_kernel(DecodeArgs a) {
             for (int kk = 0; kk < kKSteps; ++kk) {
                 s = mfma(kb[kk % kAhead], qf[kk], s);
                 if (kk + kAhead < kKSteps) kb[kk % kAhead] = *reinterpret_cast<const OpT*>(krow + kread_off(kk + kAhead));
-                if constexpr (C::lowbit) {
-                    if (kk % 4 == 2) dequant_chunk<kDqKind>(held, kk / 4, next_tile, tid);
-                }
+                if constexpr (C::lowbit) dq_step<kDqKind>(dq, kk, next_tile, tid);
                 __builtin_amdgcn_sched_barrier(0);
+            }
+            if constexpr (C::lowbit) {
+#pragma unroll
+                for (int s = kKSteps; s < kKSteps + 3; ++s) dq_step<kDqKind>(dq, s, next_tile, tid);
             }
             // rows see every key of the tile except in the last tile of the
             // range or the tile holding the newest key (block-uniform test)
@@ -566,55 +631,68 @@ void decode_kernel(DecodeArgs a) {
                     s[v] = t < lim ? s[v] : -INFINITY;
                 }
             }
-            // softmax of tile it: the reference first (and, rarely, the move of
-            // the accumulators to a new one), then the weights, which are
-            // interleaved below with the aggregation of tile it-1
-            float mr = s[0];
-#pragma unroll
-            for (int v = 1; v < 16; ++v) mr = fmaxf(mr, s[v]);
-            mr = fmaxf(mr, swap_halves(mr));
-            const float mt = mr * a.scale_log2;           // scale > 0: max commutes
-            m_true = fmaxf(m_true, mt);
-            if (m_ref == -INFINITY) m_ref = mt;          // first visible key: nothing accumulated yet
-            if constexpr (kPV) {
-                if (__builtin_amdgcn_ballot_w64(mt > m_ref + kRefSlack) != 0) {
-                    // the accumulators and the pending weights of tile it-1
-                    // move to the new reference (a second fp16 rounding of
-                    // those weights; alpha < 2^-10 for the rows that move)
-                    const float m_new = fmaxf(m_ref, mt);     // finite for every row that needs it
-                    const float alpha = __builtin_amdgcn_exp2f(m_ref - m_new);   // 1 for the other rows
-#pragma unroll
-                    for (int m = 0; m < 16; ++m) scale_acc(acc[m], alpha);
-                    const OpT av = OpT{} + static_cast<typename std::remove_reference_t<decltype(pb_prev[0][0])>>(alpha);
-                    pb_prev[0] *= av;
-                    pb_prev[1] *= av;
-                    l_run *= alpha;
-                    m_ref = m_new;
-                }
-            }
-            nref = m_ref == -INFINITY ? 0.0f : -m_ref;
-        }
-        // weights of tile it, two per piece: spread over the aggregation of
-        // tile it-1 when there is one
-        uint32_t pw[8];
-        auto weights = [&](int v2) __attribute__((always_inline)) {
-            const float p0 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2], a.scale_log2, nref));
-            const float p1 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2 + 1], a.scale_log2, nref));
-            l_run += p0 + p1;
-            pw[v2] = C::lowbit ? pack_f16x2(p0, p1) : pack_bf16x2(p0, p1);
-        };
-        if constexpr (kQK && !kPV) {
-#pragma unroll
-            for (int v2 = 0; v2 < 8; ++v2) weights(v2);
         }
         if constexpr (kPV) {
+            if (move_pending) {
+                // the previous tile moved the reference: its weights are on the
+                // new one, the accumulators follow before they are added
+#pragma unroll
+                for (int m = 0; m < 16; ++m) scale_acc(acc[m], alpha_pending);
+            }
+        }
+
+        // Softmax of tile it in pieces (interleaved with the aggregation of
+        // tile it-1 when there is one): 0-1 the tile maximum, 2 the reference
+        // (a move reaches the accumulators in the next step), 3-10 the
+        // weights, two per piece.
+        float mr = -INFINITY, nref = 0.0f;
+        bool move = false;
+        float alpha = 1.0f;
+        uint32_t pw[8];
+        // (The empty statements pin each piece's results where it is computed:
+        // the compiler would otherwise sink the work next to its first use,
+        // after the aggregation.)
+        auto softmax_piece = [&](int q) __attribute__((always_inline)) {
+            if (q == 0) {
+                mr = s[0];
+#pragma unroll
+                for (int v = 1; v < 8; ++v) mr = fmaxf(mr, s[v]);
+                asm volatile("" : "+v"(mr));
+            } else if (q == 1) {
+#pragma unroll
+                for (int v = 8; v < 16; ++v) mr = fmaxf(mr, s[v]);
+                mr = max_halves(mr);
+                asm volatile("" : "+v"(mr));
+            } else if (q == 2) {
+                const float mt = mr * a.scale_log2;           // scale > 0: max commutes
+                m_true = fmaxf(m_true, mt);
+                if (m_ref == -INFINITY) m_ref = mt;          // first visible key: nothing accumulated yet
+                move = __builtin_amdgcn_ballot_w64(mt > m_ref + kRefSlack) != 0;
+                const float m_new = move ? fmaxf(m_ref, mt) : m_ref;   // finite for a row that moves
+                alpha = m_new == m_ref ? 1.0f : __builtin_amdgcn_exp2f(m_ref - m_new);
+                m_ref = m_new;
+                l_run *= alpha;
+                nref = m_ref == -INFINITY ? 0.0f : -m_ref;
+                asm volatile("" : "+v"(nref), "+v"(l_run), "+v"(m_ref), "+v"(m_true), "+v"(alpha));
+            } else if (q < 11) {
+                const int v2 = q - 3;
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2], a.scale_log2, nref));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2 + 1], a.scale_log2, nref));
+                l_run += p0 + p1;
+                pw[v2] = C::lowbit ? pack_f16x2(p0, p1) : pack_bf16x2(p0, p1);
+                asm volatile("" : "+v"(pw[v2]), "+v"(l_run));
+            }
+        };
+        constexpr int kStageSlot0 = 12, kStageGap = C::lowbit ? 4 : 2;
+
+        if constexpr (kPV) {
             // latent aggregation of tile it-1: O^T[channel][row] += V^T . P^T;
-            // the V^T operand is read transposed from the token-major tile
-            const uint8_t* vt = tiles + slot_offset(it + C::NT - 1, C::NT, kTileBytes);
-            // rows tr_kbase + 16 ks (+ 8): the row shift term of row + 8 is that of
-            // row + 2 (tr_kbase < 8), of row + 16 that of the row itself;
-            // channels 32 m + tr_col .. : logical chunk 4m + (0..3), physical
+            // the V^T operand is read transposed from the token-major tile.
+            // Rows tr_kbase + 16 ks (+ 8): the row shift term of row + 8 is
+            // that of row + 2 (tr_kbase < 8), of row + 16 that of the row;
+            // channels 32 m + tr_col ..: logical chunk 4m + (0..3), physical
             // + m/2 in the grouped layout
+            const uint8_t* vt = tiles + slot_offset(it + C::NT - 1, C::NT, kTileBytes);
             const uint8_t* vbase = vt + row_off(C::SC, tr_kbase) + 2 * tr_col;
             auto vread = [&](int stp) __attribute__((always_inline)) {
                 const int ks = stp >> 4, m = stp & 15;
@@ -634,29 +712,48 @@ void decode_kernel(DecodeArgs a) {
                 acc[m] = mfma(vb[stp % kVAhead], pb_prev[stp >> 4], acc[m]);
                 if (stp + kVAhead < 32) vb[stp % kVAhead] = vread(stp + kVAhead);
                 if constexpr (kQK) {
-                    if (stp % 2 == 1 && stp < 16) weights(stp >> 1);
+                    softmax_piece(stp);
+                    // the staging of tile it+D, one load per kStageGap k-steps
+                    const int k = (stp - kStageSlot0) / kStageGap;
+                    if (stp >= kStageSlot0 && (stp - kStageSlot0) % kStageGap == 0 && k < C::loads)
+                        issue(k, pid, cur_t0, stage_j);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
+        } else if constexpr (kQK) {
+#pragma unroll
+            for (int q = 0; q < 11; ++q) softmax_piece(q);
+#pragma unroll
+            for (int k = 0; k < C::loads; ++k) issue(k, pid, cur_t0, stage_j);
         }
         if constexpr (kQK) {
             pb_prev[0] = __builtin_bit_cast(OpT, make_uint4(pw[0], pw[1], pw[2], pw[3]));
             pb_prev[1] = __builtin_bit_cast(OpT, make_uint4(pw[4], pw[5], pw[6], pw[7]));
+            move_pending = move;
+            alpha_pending = alpha;
+            // advance the staging cursor (it stays on the last tile)
+            if (stage_j + 1 < n_tiles) {
+                cur_t0 += kTile;
+                if (cur_t0 % P == 0) ++cur_page;
+            }
         }
     };
+
     if (n_tiles > 0) {
         // prologue part 2: tile 0 decoded (low-bit) before the first step
         if constexpr (C::lowbit) {
-            step_barrier<0>();
+            (void)step_barrier<0>(bt, cur_page);
             dequant_tile<kDqKind>(stages, tiles, tid);
         }
         step(0, std::true_type{}, std::false_type{});
         for (int it = 1; it < n_tiles; ++it) step(it, std::true_type{}, std::true_type{});
         step(n_tiles, std::false_type{}, std::true_type{});
+        // no direct-to-LDS load may outlive the workgroup's LDS
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     }
 
     if (!row_ok) return;
-    const float l_tot = l_run + swap_halves(l_run);
+    const float l_tot = sum_halves(l_run);
     const int64_t orow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
     if (a.split_tokens == 0) {
         const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
