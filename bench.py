@@ -147,6 +147,28 @@ def cpu_baseline(budget_s: float = 12.0):
                       f"(input generation excluded)"}
 
 
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the low-bit decode kernel from the recorded
+    FETCH_SIZE / WRITE_SIZE counter runs, each scaled by what the same counter
+    read for a plain 256 MiB copy; None when the kernel sources changed since
+    (or the record is for another workload)."""
+    import hashlib
+    pkg = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2609_36760_amd")
+    try:
+        rec = json.load(open(os.path.join(pkg, "measured_traffic.json")))
+        h = hashlib.sha256()
+        for f in rec["kernel_sources"]:
+            h.update(open(os.path.join(pkg, f), "rb").read())
+    except (OSError, KeyError, ValueError):
+        return None
+    if h.hexdigest() != rec["kernel_sources_sha256"] or rec["workload"] != workload:
+        return None
+    kib = rec["copy_bytes"] / 1024.0
+    fetch = rec["fetch_kib_per_dispatch"] * kib / rec["copy_fetch_kib"] * 1024.0
+    write = rec["write_kib_per_dispatch"] * kib / rec["copy_write_kib"] * 1024.0
+    return fetch + write
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -203,7 +225,8 @@ def main():
                    "cache": "INT4 content + INT4 RoPE key, group 64, fp16 scale/zero",
                    "split_tokens": 512, "layers_cycled": LAYERS},
         "roofline": {"bound": "mfma", "achieved": main_lb["decode_kernel_tflops"], "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": main_lb["mfma_frac"], "traffic": None},
+                     "unit": "TFLOP/s", "frac": main_lb["mfma_frac"], "traffic": measured_traffic(MAIN),
+                     "algorithmic_bytes": main_lb["bytes_per_launch"]},
         "hbm_gbs": main_lb["decode_kernel_gbs"], "hbm_frac": main_lb["hbm_frac"],
         "bf16_cache": {"value": main_bf["decode_tokens_per_s"], "ms_per_step": main_bf["ms_per_step"],
                        "decode_kernel_ms": main_bf["decode_kernel_ms"], "hbm_gbs": main_bf["decode_kernel_gbs"],

@@ -27,7 +27,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
-    const int64_t row = blockIdx.x;                  // (b * s_q + i) * H + h
+    // rows (b * s_q + i) * H + h in 8 contiguous ranges, range x on XCD x
+    // (block id mod 8), the XCD whose decode workgroups wrote most of them
+    const int64_t rows_all = static_cast<int64_t>(a.B) * a.s_q * a.H;
+    const int64_t per_xcd = (rows_all + 7) / 8;
+    const int64_t row = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (row >= rows_all) return;
     const int rows_per_seq = a.s_q * a.H;
     const int b = static_cast<int>(row / rows_per_seq);
     const int r = static_cast<int>(row % rows_per_seq);
@@ -62,7 +67,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
     const int64_t rows = static_cast<int64_t>(a.B) * a.s_q * a.H;
     if (rows == 0) return hipSuccess;
-    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>(rows)), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((rows + 7) / 8 * 8)), dim3(kThreads), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -457,17 +457,15 @@ void decode_kernel(DecodeArgs a) {
     const int rows_total = a.s_q * a.H;
     const int RB = (rows_total + kRowsPerBlock - 1) / kRowsPerBlock;
 
-    // Block -> (work item, row block).  Row blocks of one work item read the
-    // same tiles, so they are placed on the same XCD (block id = XCD mod 8).
-    int w, rb;
-    if (RB == 1) {
-        w = blockIdx.x;
-        rb = 0;
-    } else {
-        const int slot = blockIdx.x >> 3;
-        w = (slot / RB) * 8 + (blockIdx.x & 7);
-        rb = slot % RB;
-    }
+    // Block -> (work item, row block).  Workgroups are dispatched to the 8
+    // XCDs round-robin (XCD = block id mod 8); each XCD gets a contiguous range
+    // of work items -- the key splits of whole sequences, which share their
+    // queries through that XCD's L2 -- and all row blocks of its work items
+    // (which read the same tiles).
+    const int per_xcd = (a.num_work + 7) / 8;
+    const int slot = blockIdx.x >> 3;
+    const int w = (blockIdx.x & 7) * per_xcd + slot / RB;
+    const int rb = slot % RB;
     if (w >= a.num_work) return;
 
     const int P = a.g.page_size;
@@ -796,7 +794,7 @@ hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream
     if (a.num_work == 0) return hipSuccess;
     const int rows = a.s_q * a.H;
     const int RB = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
-    const int blocks = RB == 1 ? a.num_work : ((a.num_work + 7) / 8) * 8 * RB;
+    const int blocks = ((a.num_work + 7) / 8) * 8 * RB;
     const dim3 grid(static_cast<unsigned>(blocks)), block(kThreads);
     switch (kind) {
         case KIND_C4R4: hipLaunchKernelGGL(decode_kernel<KIND_C4R4>, grid, block, 0, stream, a); break;
