@@ -155,8 +155,10 @@ int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens
  *     part_o[j][i][h][:] = sum_t e^{z_t - part_m} C_hat[t,:]
  *   (all fp32, device; a split with no visible key gives (-inf, 0, 0)); out
  *   and lse are not touched -- call mla_splitkv_combine.
- * Scores and latent aggregation run as bf16 matrix products with fp32
- * accumulation; the dequantized cache is rounded to bf16 once.
+ * Scores and latent aggregation run as fp16 matrix products with fp32
+ * accumulation: the dequantized cache (x_hat, one fp16 rounding) and the
+ * softmax weights are fp16 operands, so queries and x_hat must lie within the
+ * fp16 range.  The output is rounded to bf16 once.
  */
 int mla_lowbit_decode_attn(const mla_cache_format* f,
                            const uint16_t* q_lat, const uint16_t* q_rope,
@@ -171,7 +173,9 @@ int mla_lowbit_decode_attn(const mla_cache_format* f,
 
 /*
  * Same computation over a BF16 cache (the unquantized comparison; row layout
- * in mla_bf16_page_bytes).  Arguments as for mla_lowbit_decode_attn.
+ * in mla_bf16_page_bytes).  Arguments as for mla_lowbit_decode_attn.  The
+ * products run in bf16 (cache rows and queries exact), the softmax weights
+ * rounded to bf16.
  */
 int mla_bf16_decode_attn(const mla_cache_format* f,
                          const uint16_t* q_lat, const uint16_t* q_rope,

@@ -6,11 +6,13 @@ accumulation, bf16 output) and measures the error against the exact fp64
 result under the parity rule used by the GPU tests (per latent channel:
 max error beyond the bf16 output's half-ulp <= 2e-2 of the channel RMS).
 
-It records why the kernels use fp16 rather than bf16 matrix products: with bf16
-tiles and weights the rule fails on the synthetic DeepSeek-V3-shaped workload,
-with fp16 it holds; and that rounding the exact result to bf16 already costs
-more than 2e-2 of the global RMS, which is why the rule is read per channel
-beyond the output's own rounding.
+It records why the low-bit kernels use fp16 rather than bf16 matrix products:
+with bf16 tiles and weights the rule fails on the synthetic DeepSeek-V3-shaped
+workload, with fp16 it holds; why the BF16-cache kernel may use bf16 products
+(its cache values and queries are exact in bf16, so only the weights are
+rounded, and that passes); and that rounding the exact result to bf16 already
+costs more than 2e-2 of the global RMS, which is why the rule is read per
+channel beyond the output's own rounding.
 """
 import numpy as np
 import pytest
@@ -91,3 +93,27 @@ def test_bf16_output_rounding_alone_exceeds_the_global_rule(sample):
     w, rows = sample
     got, want, _ = _ratio(w, rows, _ident, _ident)
     assert np.abs(got - want).max() > 0.02 * np.sqrt((want ** 2).mean())
+
+
+@pytest.fixture(scope="module")
+def bf16_sample():
+    """Exact bf16 cache values (the BF16 cache stores the latents as they are)."""
+    w = syn.WORKLOADS["dsv3_b32_h128_4k_c4r4"]
+    lens = syn.seq_lens(w)
+    rows = []
+    for b in (0, 17):
+        L = int(lens[b])
+        c, k = syn.sequence_tokens(w, 0, b, L)
+        c_hat, kr_hat = at.bf16_bits_to_f64(c), at.bf16_bits_to_f64(k)
+        ql, qr = syn.queries(w, 0, batch=[b])
+        hs = np.arange(0, 128, 2)
+        want, _ = at.decode_sequence(ql[0][:, hs], qr[0][:, hs], c_hat, kr_hat, w.tau)
+        rows.append((at.bf16_bits_to_f64(ql[0][:, hs]).reshape(-1, 512),
+                     at.bf16_bits_to_f64(qr[0][:, hs]).reshape(-1, 64), c_hat, kr_hat, want.reshape(-1, 512)))
+    return w, rows
+
+
+def test_bf16_cache_with_bf16_weights_meets_the_rule(bf16_sample):
+    w, rows = bf16_sample
+    _, _, r = _ratio(w, rows, _ident, _rnd_bf16)
+    assert r <= 0.02, r
