@@ -42,7 +42,7 @@ def log(*a):
 def algorithmic_bytes(run) -> int:
     """HBM bytes one decode launch must move: every attended key once, queries,
     and partials (written, then read by the combine) or the output."""
-    keys = int(run.lens.astype(np.int64).sum()) * run.cache_token_bytes()
+    keys = run.key_bytes()
     q = run.B * run.s_q * run.H * (512 + 64) * 2
     rows = run.B * run.s_q * run.H
     if run.split_tokens:

@@ -201,6 +201,99 @@ int mla_splitkv_combine(const float* part_m, const float* part_s, const float* p
                         const int32_t* split_indptr, int32_t B, int32_t s_q, int32_t H,
                         int32_t d_c, uint16_t* out, float* lse, hipStream_t stream);
 
+/*
+ * BF16 protection of sink and recent tokens (Sec. 3.3; Appendix C.5, "BF16
+ * protection and cache lifecycle", "Global attention normalization",
+ * "Storage layout").  Besides the packed copy of every token, the writer keeps
+ * the pre-quantization bf16 content latent and RoPE key of the first `sink`
+ * and the last `recent` tokens of every sequence.  For a sequence of length L
+ * the protected positions are
+ *   P_L = {0 .. min(sink, L) - 1}  U  {max(0, L - recent) .. L - 1}
+ * (overlap counted once; the paper's policy is sink = 4, recent = 128).
+ * Attention reads every token once: bf16 values for positions in P_L, the
+ * packed copy otherwise, all in one softmax.  Constraints: sink, recent >= 0,
+ * 1 <= sink + recent <= 65536.
+ *
+ * Protection buffer of one sequence: sink + recent rows of d_c + d_r bf16
+ * values ([c_kv | k_rope], 1152 B at d_c = 512, d_r = 64; 152,064 B for the
+ * paper's policy).  Row p holds position p < sink; row
+ * sink + (p - sink) mod recent holds position p >= sink (a ring: the token
+ * entering the window overwrites the one leaving it, which attention then
+ * reads from its packed copy).  Rows not yet written are never read.
+ */
+typedef struct mla_protect_policy {
+    int32_t sink;       /* leading tokens kept in bf16                    */
+    int32_t recent;     /* most recent tokens kept in bf16                */
+} mla_protect_policy;
+
+/* Bytes of one sequence's protection buffer; -1 for an invalid format or
+ * policy (low-bit formats only). */
+int64_t mla_protect_buffer_bytes(const mla_cache_format* f, const mla_protect_policy* p);
+
+/*
+ * Quantize-and-append with protection: exactly mla_lowbit_quant_append for
+ * the packed cache, and in the same pass the bf16 row of every appended token
+ * that is protected once the call is done, i.e. position p < sink, or
+ * L - recent <= p < L with L = seq_lens[b] the sequence's length after the
+ * call (a prefill thus writes only the rows that stay protected, and no two
+ * tokens of one call share a row).  Rows are copied bit for bit.
+ *   token_seq  device, int32 [n]: sequence b of each token (outside [0, B):
+ *              no protection write)
+ *   positions  device, int32 [n]: the token's position in its sequence
+ *   seq_lens   device, int32 [B]: lengths after this call
+ *   prot_slot  device, int32 [B]: protection buffer index of each sequence
+ *              (outside [0, num_prot): no protection write)
+ *   prot       device, num_prot buffers of mla_protect_buffer_bytes each,
+ *              back to back, 16-byte aligned
+ * A token with a skipped slot (negative or past the cache) is skipped
+ * entirely.  Other arguments and errors as for mla_lowbit_quant_append.
+ */
+int mla_lowbit_quant_append_protected(const mla_cache_format* f, const mla_protect_policy* p,
+                                      const uint16_t* c_kv, int64_t c_kv_stride,
+                                      const uint16_t* k_rope, int64_t k_rope_stride,
+                                      const int64_t* slot_mapping, int32_t n,
+                                      void* cache, int64_t num_pages,
+                                      const int32_t* token_seq, const int32_t* positions,
+                                      const int32_t* seq_lens, const int32_t* prot_slot, int32_t B,
+                                      void* prot, int64_t num_prot, hipStream_t stream);
+
+/*
+ * Split planner for protected decode (host only).  Under protection the keys
+ * of a sequence of length L are processed as a list of 32-key tiles: the
+ * packed tiles first -- from the tile holding token `sink` through token
+ * L - recent - 1, when L - recent > sink -- then ceil(n_prot / 32) tiles of
+ * protected rows (n_prot = sink + recent, or L when every token is
+ * protected).  Split k of a sequence covers list tiles
+ * [k * split_tokens / 32, (k + 1) * split_tokens / 32); the partials of all
+ * splits merge to the single softmax (Appendix C.5).  Returns the total
+ * number of splits, or -MLA_EINVAL / -MLA_ENOTSUP as mla_plan_splits.
+ */
+int32_t mla_plan_splits_protected(const int32_t* seq_lens, int32_t B, int32_t split_tokens,
+                                  const mla_protect_policy* p, int32_t* split_indptr);
+
+/*
+ * Low-bit decode attention under protection: as mla_lowbit_decode_attn, with
+ * positions in P_L read as bf16 rows from the sequence's protection buffer
+ * (prot_slot[b], clamped into [0, num_prot)) instead of the packed cache.
+ * Split partials follow mla_plan_splits_protected; mla_splitkv_combine
+ * merges them unchanged.  Products over protected rows run in bf16 (rows and
+ * queries exact, weights rounded to bf16), over packed rows in fp16 as in
+ * mla_lowbit_decode_attn.  Precondition: the buffer holds every position of
+ * P_L (written by mla_lowbit_quant_append_protected).
+ *   prot  device, num_prot protection buffers (16-byte aligned)
+ */
+int mla_lowbit_decode_attn_protected(const mla_cache_format* f, const mla_protect_policy* p,
+                                     const uint16_t* q_lat, const uint16_t* q_rope,
+                                     const void* cache, int64_t num_pages,
+                                     const int32_t* block_table, int32_t max_pages_per_seq,
+                                     const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
+                                     float softmax_scale,
+                                     const void* prot, int64_t num_prot, const int32_t* prot_slot,
+                                     int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
+                                     uint16_t* out, float* lse,
+                                     float* part_m, float* part_s, float* part_o,
+                                     hipStream_t stream);
+
 /* Human-readable name of a status code (static string). */
 const char* mla_status_str(int status);
 

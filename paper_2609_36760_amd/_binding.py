@@ -21,7 +21,8 @@ MLA_OK, MLA_EINVAL, MLA_ENOTSUP, MLA_EHIP = 0, 1, 2, 3
 SYMBOLS = (
     "mla_lowbit_page_bytes", "mla_bf16_page_bytes", "mla_lowbit_quant_append", "mla_bf16_append",
     "mla_plan_splits", "mla_lowbit_decode_attn", "mla_bf16_decode_attn", "mla_splitkv_combine",
-    "mla_status_str", "mla_last_hip_error",
+    "mla_status_str", "mla_last_hip_error", "mla_protect_buffer_bytes", "mla_lowbit_quant_append_protected",
+    "mla_plan_splits_protected", "mla_lowbit_decode_attn_protected",
 )
 
 
@@ -37,6 +38,15 @@ class MlaError(RuntimeError):
 class mla_cache_format(ctypes.Structure):
     _fields_ = [("d_c", ctypes.c_int32), ("d_r", ctypes.c_int32), ("group", ctypes.c_int32),
                 ("c_bits", ctypes.c_int32), ("r_bits", ctypes.c_int32), ("page_size", ctypes.c_int32)]
+
+
+class mla_protect_policy(ctypes.Structure):
+    _fields_ = [("sink", ctypes.c_int32), ("recent", ctypes.c_int32)]
+
+
+def protect_policy(sink: int = 4, recent: int = 128) -> mla_protect_policy:
+    """The paper's policy by default: 4 sink tokens and a 128-token window."""
+    return mla_protect_policy(sink, recent)
 
 
 def cache_format(c_bits: int = 4, page_size: int = 64, d_c: int = 512, d_r: int = 64,
@@ -57,6 +67,7 @@ def library() -> ctypes.CDLL:
     lib = ctypes.CDLL(LIB_PATH)
     P, I32, I64, F32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
     FMT = ctypes.POINTER(mla_cache_format)
+    POL = ctypes.POINTER(mla_protect_policy)
     sig = {
         "mla_lowbit_page_bytes": (I64, [FMT]),
         "mla_bf16_page_bytes": (I64, [FMT]),
@@ -68,6 +79,12 @@ def library() -> ctypes.CDLL:
         "mla_bf16_decode_attn": (ctypes.c_int, [FMT, P, P, P, I64, P, I32, P, I32, I32, I32, F32,
                                                 I32, P, I32, P, P, P, P, P, P]),
         "mla_splitkv_combine": (ctypes.c_int, [P, P, P, P, I32, I32, I32, I32, P, P, P]),
+        "mla_protect_buffer_bytes": (I64, [FMT, POL]),
+        "mla_lowbit_quant_append_protected": (ctypes.c_int, [FMT, POL, P, I64, P, I64, P, I32, P, I64,
+                                                             P, P, P, P, I32, P, I64, P]),
+        "mla_plan_splits_protected": (I32, [P, I32, I32, POL, P]),
+        "mla_lowbit_decode_attn_protected": (ctypes.c_int, [FMT, POL, P, P, P, I64, P, I32, P, I32, I32, I32, F32,
+                                                            P, I64, P, I32, P, I32, P, P, P, P, P, P]),
         "mla_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "mla_last_hip_error": (ctypes.c_int, []),
     }
@@ -167,3 +184,39 @@ def mla_splitkv_combine(part_m, part_s, part_o, split_indptr, B, s_q, H, out, ls
     _check("mla_splitkv_combine", library().mla_splitkv_combine(
         _ptr(part_m), _ptr(part_s), _ptr(part_o), _ptr(split_indptr), B, s_q, H, 512,
         _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def mla_protect_buffer_bytes(fmt: mla_cache_format, policy: mla_protect_policy) -> int:
+    return library().mla_protect_buffer_bytes(ctypes.byref(fmt), ctypes.byref(policy))
+
+
+def mla_lowbit_quant_append_protected(fmt, policy, c_kv, k_rope, slot_mapping, cache, num_pages, token_seq,
+                                      positions, seq_lens, prot_slot, prot, num_prot, stream=None):
+    n = c_kv.shape[0]
+    _check("mla_lowbit_quant_append_protected", library().mla_lowbit_quant_append_protected(
+        ctypes.byref(fmt), ctypes.byref(policy), _ptr(c_kv), c_kv.stride(0), _ptr(k_rope), k_rope.stride(0),
+        _ptr(slot_mapping), n, _ptr(cache), num_pages, _ptr(token_seq), _ptr(positions), _ptr(seq_lens),
+        _ptr(prot_slot), seq_lens.shape[0], _ptr(prot), num_prot, _stream(stream)))
+
+
+def mla_plan_splits_protected(seq_lens, split_tokens: int, policy: mla_protect_policy):
+    """Host planner under protection; returns ``(split_indptr int32 [B+1], total_splits)``."""
+    lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    indptr = np.zeros(lens.size + 1, dtype=np.int32)
+    total = library().mla_plan_splits_protected(lens.ctypes.data, lens.size, split_tokens, ctypes.byref(policy),
+                                                indptr.ctypes.data)
+    if total < 0:
+        raise MlaError("mla_plan_splits_protected", -total)
+    return indptr, int(total)
+
+
+def mla_lowbit_decode_attn_protected(fmt, policy, q_lat, q_rope, cache, num_pages, block_table, seq_lens, s_q, H,
+                                     softmax_scale, prot, num_prot, prot_slot, split_tokens=0, split_indptr=None,
+                                     num_splits=0, out=None, lse=None, part_m=None, part_s=None, part_o=None,
+                                     stream=None):
+    B = q_lat.shape[0]
+    _check("mla_lowbit_decode_attn_protected", library().mla_lowbit_decode_attn_protected(
+        ctypes.byref(fmt), ctypes.byref(policy), _ptr(q_lat), _ptr(q_rope), _ptr(cache), num_pages,
+        _ptr(block_table), block_table.shape[1], _ptr(seq_lens), B, s_q, H, float(softmax_scale),
+        _ptr(prot), num_prot, _ptr(prot_slot), split_tokens, _ptr(split_indptr), num_splits,
+        _ptr(out), _ptr(lse), _ptr(part_m), _ptr(part_s), _ptr(part_o), _stream(stream)))

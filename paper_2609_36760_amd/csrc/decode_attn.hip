@@ -244,6 +244,13 @@ __device__ __forceinline__ int step_barrier(const int32_t* table, int index) {
     return v;
 }
 
+// The same wait and barrier without a page-table fetch.
+template <int N>
+__device__ __forceinline__ void plain_barrier() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(N) : "memory");
+}
+
 // The same entry, waited for on the spot.
 __device__ __forceinline__ int load_page_id(const int32_t* table, int index) {
     int v;
@@ -295,9 +302,12 @@ __device__ __forceinline__ void stage_lowbit(int k, const uint8_t* page, int po,
 // at or past `nvalid` re-read token nvalid - 1.  Loads 0..8 cover chunks
 // 0..2303 (chunk i by lane i % 64 of wave (i / 64) % 4); load 9 covers
 // 2304..2431 with waves 0/2 and 1/3 loading the same chunks (same data to the
-// same place), so that all waves issue the same number of loads.
-__device__ __forceinline__ void stage_bf16(int k, const uint8_t* page, int po, int nvalid, uint32_t tile_lds,
-                                           int wave, int wave_u, int lane) {
+// same place), so that all waves issue the same number of loads.  Row tok of
+// the tile starts at byte row_start(tok) of `src` (a page, or a protection
+// buffer).
+template <class RowStart>
+__device__ __forceinline__ void stage_bf16(int k, const uint8_t* src, RowStart row_start, int nvalid,
+                                           uint32_t tile_lds, int wave, int wave_u, int lane) {
     constexpr int sc = 76;
     const int base = k < 9 ? k * kThreads + wave * 64 : 2304 + 64 * (wave & 1);
     const int i = base + lane;
@@ -306,7 +316,7 @@ __device__ __forceinline__ void stage_bf16(int k, const uint8_t* page, int po, i
     const int col = min(i - row_off(sc, row) / 16, 71);
     const int tok = min(row, nvalid - 1);
     const int base_u = k < 9 ? k * kThreads + wave_u * 64 : 2304 + 64 * (wave_u & 1);
-    dma16(page, (po + tok) * 1152 + col * 16, tile_lds + base_u * 16);
+    dma16(src, row_start(tok) + col * 16, tile_lds + base_u * 16);
 }
 
 // ---------------------------------------------------------------------------
@@ -439,16 +449,26 @@ __device__ __forceinline__ void dequant_tile(const uint8_t* st, uint8_t* tile, i
 }
 
 // ---------------------------------------------------------------------------
-template <int KIND>
+// 3. The kernel.
+//
+// A work item is a sequence (unsplit launch) or one key split of it.  Under
+// BF16 protection (kProt) the keys of a sequence of length L form a list of
+// 32-token tiles: the packed tiles first (tokens sink .. L-recent-1, counted
+// from the tile that holds token `sink`; its tokens below `sink` are masked),
+// then the protected tiles, raw bf16 rows of the sequence's protection buffer
+// in position order (the sink rows, then the recent window out of the ring).
+// A work item takes a contiguous part of that list and runs it in at most two
+// phases that carry one online-softmax state -- the low-bit pipeline over its
+// packed tiles, then the BF16 pipeline over its protected tiles -- so every
+// visible token enters one softmax in exactly one representation
+// (Appendix C.5, "BF16 protection and cache lifecycle", "Global attention
+// normalization").
+template <int KIND, bool kProt>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void decode_kernel(DecodeArgs a) {
-    using C = Cfg<KIND>;
-    using OpT = std::conditional_t<C::lowbit, f16x8, bf16x8>;
-    constexpr int kDqKind = C::lowbit ? KIND : KIND_C4R4;     // unused by the BF16 kernel
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[lds_bytes<KIND>()];
-    constexpr int kTileBytes = tile_bytes<KIND>();
-    uint8_t* tiles = smem;                              // NT x kTileBytes
-    uint8_t* stages = smem + C::NT * kTileBytes;        // NS x stage_bytes (low-bit only)
+    constexpr int kLds = kProt && lds_bytes<KIND_BF16>() > lds_bytes<KIND>() ? lds_bytes<KIND_BF16>()
+                                                                              : lds_bytes<KIND>();
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[kLds];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -469,11 +489,9 @@ void decode_kernel(DecodeArgs a) {
     if (w >= a.num_work) return;
 
     const int P = a.g.page_size;
-    int b, t_begin, t_end;
+    int b, split = 0;
     if (a.split_tokens == 0) {
         b = w;
-        t_begin = 0;
-        t_end = a.seq_lens[b];
     } else {
         int lo = 0, hi = a.B;
         while (lo < hi) {
@@ -481,81 +499,16 @@ void decode_kernel(DecodeArgs a) {
             if (a.split_indptr[mid] <= w) lo = mid; else hi = mid - 1;
         }
         b = lo < a.B ? lo : a.B - 1;
-        t_begin = (w - a.split_indptr[b]) * a.split_tokens;
-        t_end = t_begin + a.split_tokens;
+        split = w - a.split_indptr[b];
     }
     const int L = min(max(a.seq_lens[b], 0), a.max_pages * P);
-    if (t_end > L) t_end = L;
-    if (t_begin < 0) t_begin = 0;
-    const int n_tiles = t_end > t_begin ? (t_end - t_begin + kTile - 1) / kTile : 0;
+    const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_pages;
 
     // this lane's query row
     const int row = rb * kRowsPerBlock + wave * 32 + (lane & 31);
     const bool row_ok = row < rows_total;
     const int qi = row_ok ? row / a.H : 0;
     const int h = row_ok ? row % a.H : 0;
-    const int lim = row_ok ? min(L - a.s_q + qi + 1, t_end) : t_begin;   // keys t < lim are visible
-    const int full_lim = min(L - a.s_q + 1, t_end);    // every valid row sees keys t < full_lim
-
-    // queries as B operands: k-step kk holds channels 16kk + 8*half .. +8
-    OpT qf[kKSteps];
-    {
-        const int64_t qrow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
-        const uint16_t* ql = a.q_lat + qrow * kDc + 8 * half;
-        const uint16_t* qr = a.q_rope + qrow * 64 + 8 * half;
-#pragma unroll
-        for (int kk = 0; kk < kKSteps; ++kk) {
-            // rows past the end read row 0 of the sequence; they are never stored
-            const uint4 v = *reinterpret_cast<const uint4*>(kk < 32 ? ql + 16 * kk : qr + 16 * (kk - 32));
-            if constexpr (C::lowbit)
-                qf[kk] = __builtin_bit_cast(f16x8, make_uint4(bf16x2_to_f16x2(v.x), bf16x2_to_f16x2(v.y),
-                                                              bf16x2_to_f16x2(v.z), bf16x2_to_f16x2(v.w)));
-            else
-                qf[kk] = __builtin_bit_cast(bf16x8, v);
-        }
-    }
-
-    // Staging.  Tile j is staged into staging slot j % NS (low-bit) or tile
-    // slot j % NT (BF16).  Step it stages tile it + D -- clamped to the last
-    // tile, whose bytes then land once more in a free slot -- so that every
-    // step issues Cfg::loads loads.  Cursor: first token and page-table index
-    // of that tile (uniform).
-    const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_pages;
-    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-    auto slot_lds = [&](int j) {
-        return C::lowbit ? lds_addr(stages + slot_offset(j, C::NS, C::stage_bytes))
-                         : lds_addr(tiles + slot_offset(j, C::NT, kTileBytes));
-    };
-    auto issue = [&](int k, int pid, int t0, int j) __attribute__((always_inline)) {
-        pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
-        const uint8_t* page = a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
-        const int nvalid = min(t_end - t0, kTile);
-        if constexpr (C::lowbit)
-            stage_lowbit<KIND>(k, page, t0 % P, nvalid, a.g, slot_lds(j), wave, wave_u, lane);
-        else
-            stage_bf16(k, page, t0 % P, nvalid, slot_lds(j), wave, wave_u, lane);
-    };
-    // prologue: the first D tiles
-#pragma unroll
-    for (int j = 0; j < C::D; ++j) {
-        if (j < n_tiles) {
-            const int t0 = t_begin + j * kTile;
-            const int pid = load_page_id(bt, t0 / P);
-#pragma unroll
-            for (int k = 0; k < C::loads; ++k) issue(k, pid, t0, j);
-        }
-    }
-    int cur_t0 = t_begin + min(C::D, n_tiles - 1) * kTile;     // tile staged by the current step
-    int cur_page = cur_t0 / P;
-
-    // per-lane addressing of the transposing V^T reads: lane (group g, index i)
-    // supplies the address of tile row k0 + i/4, channels n0 + 4(i%4) .. +3
-    // and receives rows k0 .. k0+3 of channel n0 + i
-    const int qk_row = lane & 31;
-    const int tr_i = lane & 15;
-    const int tr_g = lane >> 4;
-    const int tr_kbase = 4 * (tr_g >> 1) + (tr_i >> 2);   // + 16 * ks (+ 8 for the second read)
-    const int tr_col = 16 * (tr_g & 1) + 4 * (tr_i & 3);  // + 32 * m
 
     float m_ref = -INFINITY;    // reference of the exponentials (log2 units)
     float m_true = -INFINITY;   // true running maximum (log2 units)
@@ -563,191 +516,348 @@ void decode_kernel(DecodeArgs a) {
     f32x16 acc[16];
 #pragma unroll
     for (int m = 0; m < 16; ++m) acc[m] = f32x16{};
-    OpT pb_prev[2] = {OpT{}, OpT{}};   // weights of the previous tile (P^T operands)
-    bool move_pending = false;         // the previous tile moved the reference:
-    float alpha_pending = 1.0f;        // accumulators *= alpha before its aggregation
 
-    // One pipeline step.  QK: scores and softmax of tile `it` (low-bit: plus
-    // the dequantization of tile it+1) and the staging of tile it+D; PV:
-    // aggregation of tile it-1.
-    auto step = [&](const int it, auto QK, auto PV) __attribute__((always_inline)) {
-        constexpr bool kQK = decltype(QK)::value, kPV = decltype(PV)::value;
-        // The previous step issued Cfg::loads staging loads (none before step
-        // 0: the prologue's must all land); everything older must have landed.
-        int pid = 0;
-        if (it == 0) pid = step_barrier<0>(bt, cur_page);
-        else pid = step_barrier<C::loads>(bt, cur_page);
-        const int stage_j = it + C::D;
+    // the sequence's protection buffer (kProt): base, rows, sink rows in use
+    // and the ring index of the first window position past the sink
+    const uint8_t* ring_base = nullptr;
+    int ring_rows = 1, ring_nsink = 0, ring_q0 = 0;
 
-        f32x16 s = f32x16{};
-        if constexpr (kQK) {
-            const uint8_t* kt = tiles + slot_offset(it, C::NT, kTileBytes);
-            // every wave computes, also one whose rows all lie past the end
-            // (its results are never stored): a branch here would force the
-            // accumulators through a register-class join.
-            // Scores S^T[token][row], K = 576 in 36 steps, the operand reads
-            // kAhead steps ahead of the matrix instructions.  Low-bit: the 36
-            // pieces of the next tile's dequantization (reading staging slot
-            // (it+1) % NS, writing tile slot (it+1) % NT, which the aggregation
-            // of tile it-2 released before this step's barrier) fill the
-            // matrix pipe's shadow, one per k-step.
-            Dq<kDqKind> dq;
-            uint8_t* next_tile = tiles + slot_offset(it + 1, C::NT, kTileBytes);
-            if constexpr (C::lowbit) {
-                dq_read<kDqKind>(dq, stages + slot_offset(it + 1, C::NS, C::stage_bytes), tid);
-                dq_split<kDqKind>(dq, 0);
-            }
-            // k-step kk reads logical chunk 2kk + half: physical 2kk + half (+ kk/4 grouped)
-            const uint8_t* krow = kt + row_off(C::SC, qk_row) + 16 * half;
-            auto kread_off = [](int kk) { return 16 * (2 * kk + (C::grouped ? kk >> 2 : 0)); };
-            constexpr int kAhead = 3;
-            OpT kb[kAhead];
-#pragma unroll
-            for (int j = 0; j < kAhead; ++j) kb[j] = *reinterpret_cast<const OpT*>(krow + kread_off(j));
-            // Scheduling barriers after every k-step keep this order (left
-            // free, the scheduler trades the read-ahead for registers and every
-            // product then waits on LDS latency).
-            __builtin_amdgcn_sched_barrier(0);
+    // One phase over keys [t_begin, t_end) in one representation: PK is the
+    // cache kind whose pipeline runs; kRing reads bf16 rows of the protection
+    // buffer, t then counting protected positions in order.  This lane's row
+    // sees keys t_lo <= t < lim; every valid row sees t < full_lim.
+    auto run = [&](auto kind_c, auto ring_c, const int t_begin, const int t_end, const int t_lo, const int lim,
+                   const int full_lim) __attribute__((always_inline)) {
+        constexpr int PK = decltype(kind_c)::value;
+        constexpr bool kRing = decltype(ring_c)::value;
+        using C = Cfg<PK>;
+        using OpT = std::conditional_t<C::lowbit, f16x8, bf16x8>;
+        constexpr int kDqKind = C::lowbit ? PK : KIND_C4R4;     // unused by the BF16 pipeline
+        constexpr int kTileBytes = tile_bytes<PK>();
+        uint8_t* tiles = smem;                              // NT x kTileBytes
+        uint8_t* stages = smem + C::NT * kTileBytes;        // NS x stage_bytes (low-bit only)
+        const int n_tiles = t_end > t_begin ? (t_end - t_begin + kTile - 1) / kTile : 0;
+        (void)t_lo;
+
+        // queries as B operands: k-step kk holds channels 16kk + 8*half .. +8
+        OpT qf[kKSteps];
+        {
+            const int64_t qrow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
+            const uint16_t* ql = a.q_lat + qrow * kDc + 8 * half;
+            const uint16_t* qr = a.q_rope + qrow * 64 + 8 * half;
 #pragma unroll
             for (int kk = 0; kk < kKSteps; ++kk) {
-                s = mfma(kb[kk % kAhead], qf[kk], s);
-                if (kk + kAhead < kKSteps) kb[kk % kAhead] = *reinterpret_cast<const OpT*>(krow + kread_off(kk + kAhead));
-                if constexpr (C::lowbit) dq_step<kDqKind>(dq, kk, next_tile, tid);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            if constexpr (C::lowbit) {
-#pragma unroll
-                for (int s = kKSteps; s < kKSteps + 3; ++s) dq_step<kDqKind>(dq, s, next_tile, tid);
-            }
-            // rows see every key of the tile except in the last tile of the
-            // range or the tile holding the newest key (block-uniform test)
-            const int t0 = t_begin + it * kTile;
-            if (t0 + kTile > full_lim) {
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
-                    s[v] = t < lim ? s[v] : -INFINITY;
-                }
-            }
-        }
-        if constexpr (kPV) {
-            if (move_pending) {
-                // the previous tile moved the reference: its weights are on the
-                // new one, the accumulators follow before they are added
-#pragma unroll
-                for (int m = 0; m < 16; ++m) scale_acc(acc[m], alpha_pending);
+                // rows past the end read row 0 of the sequence; they are never stored
+                const uint4 v = *reinterpret_cast<const uint4*>(kk < 32 ? ql + 16 * kk : qr + 16 * (kk - 32));
+                if constexpr (C::lowbit)
+                    qf[kk] = __builtin_bit_cast(f16x8, make_uint4(bf16x2_to_f16x2(v.x), bf16x2_to_f16x2(v.y),
+                                                                  bf16x2_to_f16x2(v.z), bf16x2_to_f16x2(v.w)));
+                else
+                    qf[kk] = __builtin_bit_cast(bf16x8, v);
             }
         }
 
-        // Softmax of tile it in pieces (interleaved with the aggregation of
-        // tile it-1 when there is one): 0-1 the tile maximum, 2 the reference
-        // (a move reaches the accumulators in the next step), 3-10 the
-        // weights, two per piece.
-        float mr = -INFINITY, nref = 0.0f;
-        bool move = false;
-        float alpha = 1.0f;
-        uint32_t pw[8];
-        // (The empty statements pin each piece's results where it is computed:
-        // the compiler would otherwise sink the work next to its first use,
-        // after the aggregation.)
-        auto softmax_piece = [&](int q) __attribute__((always_inline)) {
-            if (q == 0) {
-                mr = s[0];
-#pragma unroll
-                for (int v = 1; v < 8; ++v) mr = fmaxf(mr, s[v]);
-                asm volatile("" : "+v"(mr));
-            } else if (q == 1) {
-#pragma unroll
-                for (int v = 8; v < 16; ++v) mr = fmaxf(mr, s[v]);
-                mr = max_halves(mr);
-                asm volatile("" : "+v"(mr));
-            } else if (q == 2) {
-                const float mt = mr * a.scale_log2;           // scale > 0: max commutes
-                m_true = fmaxf(m_true, mt);
-                if (m_ref == -INFINITY) m_ref = mt;          // first visible key: nothing accumulated yet
-                move = __builtin_amdgcn_ballot_w64(mt > m_ref + kRefSlack) != 0;
-                const float m_new = move ? fmaxf(m_ref, mt) : m_ref;   // finite for a row that moves
-                alpha = m_new == m_ref ? 1.0f : __builtin_amdgcn_exp2f(m_ref - m_new);
-                m_ref = m_new;
-                l_run *= alpha;
-                nref = m_ref == -INFINITY ? 0.0f : -m_ref;
-                asm volatile("" : "+v"(nref), "+v"(l_run), "+v"(m_ref), "+v"(m_true), "+v"(alpha));
-            } else if (q < 11) {
-                const int v2 = q - 3;
-                const float p0 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2], a.scale_log2, nref));
-                const float p1 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2 + 1], a.scale_log2, nref));
-                l_run += p0 + p1;
-                pw[v2] = C::lowbit ? pack_f16x2(p0, p1) : pack_bf16x2(p0, p1);
-                asm volatile("" : "+v"(pw[v2]), "+v"(l_run));
+        // Staging.  Tile j is staged into staging slot j % NS (low-bit) or tile
+        // slot j % NT (BF16).  Step it stages tile it + D -- clamped to the last
+        // tile, whose bytes then land once more in a free slot -- so that every
+        // step issues Cfg::loads loads.  Cursor: first token and page-table index
+        // of that tile (uniform).
+        const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+        auto slot_lds = [&](int j) {
+            return C::lowbit ? lds_addr(stages + slot_offset(j, C::NS, C::stage_bytes))
+                             : lds_addr(tiles + slot_offset(j, C::NT, kTileBytes));
+        };
+        auto issue = [&](int k, int pid, int t0, int j) __attribute__((always_inline)) {
+            const int nvalid = min(t_end - t0, kTile);
+            if constexpr (kRing) {
+                // protected position order: the sink rows, then the window from the ring
+                auto row_start = [&](int tok) {
+                    const int v = t0 + tok;
+                    const int x = ring_q0 + (v - ring_nsink);       // < 2 * recent
+                    const int r = v < ring_nsink ? v : a.sink + (x >= a.recent ? x - a.recent : x);
+                    return min(r, ring_rows - 1) * 1152;
+                };
+                stage_bf16(k, ring_base, row_start, nvalid, slot_lds(j), wave, wave_u, lane);
+            } else {
+                pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
+                const uint8_t* page = a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
+                const int po = t0 % P;
+                if constexpr (C::lowbit)
+                    stage_lowbit<PK>(k, page, po, nvalid, a.g, slot_lds(j), wave, wave_u, lane);
+                else
+                    stage_bf16(k, page, [&](int tok) { return (po + tok) * 1152; }, nvalid, slot_lds(j), wave,
+                               wave_u, lane);
             }
         };
-        constexpr int kStageSlot0 = 12, kStageGap = C::lowbit ? 4 : 2;
+        // prologue: the first D tiles
+#pragma unroll
+        for (int j = 0; j < C::D; ++j) {
+            if (j < n_tiles) {
+                const int t0 = t_begin + j * kTile;
+                const int pid = kRing ? 0 : load_page_id(bt, t0 / P);
+#pragma unroll
+                for (int k = 0; k < C::loads; ++k) issue(k, pid, t0, j);
+            }
+        }
+        int cur_t0 = t_begin + min(C::D, n_tiles - 1) * kTile;     // tile staged by the current step
+        int cur_page = cur_t0 / P;
 
-        if constexpr (kPV) {
-            // latent aggregation of tile it-1: O^T[channel][row] += V^T . P^T;
-            // the V^T operand is read transposed from the token-major tile.
-            // Rows tr_kbase + 16 ks (+ 8): the row shift term of row + 8 is
-            // that of row + 2 (tr_kbase < 8), of row + 16 that of the row;
-            // channels 32 m + tr_col ..: logical chunk 4m + (0..3), physical
-            // + m/2 in the grouped layout
-            const uint8_t* vt = tiles + slot_offset(it + C::NT - 1, C::NT, kTileBytes);
-            const uint8_t* vbase = vt + row_off(C::SC, tr_kbase) + 2 * tr_col;
-            auto vread = [&](int stp) __attribute__((always_inline)) {
-                const int ks = stp >> 4, m = stp & 15;
-                const uint8_t* p = vbase + 16 * C::SC * 16 * ks + 64 * m + (C::grouped ? 16 * (m >> 1) : 0);
-                const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
-                const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 16 * C::SC * 8 + 32));
-                return __builtin_bit_cast(OpT, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
-            };
-            constexpr int kVAhead = 2;
-            OpT vb[kVAhead];
-#pragma unroll
-            for (int j = 0; j < kVAhead; ++j) vb[j] = vread(j);
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int stp = 0; stp < 32; ++stp) {
-                const int m = stp & 15;
-                acc[m] = mfma(vb[stp % kVAhead], pb_prev[stp >> 4], acc[m]);
-                if (stp + kVAhead < 32) vb[stp % kVAhead] = vread(stp + kVAhead);
-                if constexpr (kQK) {
-                    softmax_piece(stp);
-                    // the staging of tile it+D, one load per kStageGap k-steps
-                    const int k = (stp - kStageSlot0) / kStageGap;
-                    if (stp >= kStageSlot0 && (stp - kStageSlot0) % kStageGap == 0 && k < C::loads)
-                        issue(k, pid, cur_t0, stage_j);
+        // per-lane addressing of the transposing V^T reads: lane (group g, index i)
+        // supplies the address of tile row k0 + i/4, channels n0 + 4(i%4) .. +3
+        // and receives rows k0 .. k0+3 of channel n0 + i
+        const int qk_row = lane & 31;
+        const int tr_i = lane & 15;
+        const int tr_g = lane >> 4;
+        const int tr_kbase = 4 * (tr_g >> 1) + (tr_i >> 2);   // + 16 * ks (+ 8 for the second read)
+        const int tr_col = 16 * (tr_g & 1) + 4 * (tr_i & 3);  // + 32 * m
+
+        OpT pb_prev[2] = {OpT{}, OpT{}};   // weights of the previous tile (P^T operands)
+        bool move_pending = false;         // the previous tile moved the reference:
+        float alpha_pending = 1.0f;        // accumulators *= alpha before its aggregation
+
+        // One pipeline step.  QK: scores and softmax of tile `it` (low-bit: plus
+        // the dequantization of tile it+1) and the staging of tile it+D; PV:
+        // aggregation of tile it-1.
+        auto step = [&](const int it, auto QK, auto PV) __attribute__((always_inline)) {
+            constexpr bool kQK = decltype(QK)::value, kPV = decltype(PV)::value;
+            // The previous step issued Cfg::loads staging loads (none before step
+            // 0: the prologue's must all land); everything older must have landed.
+            int pid = 0;
+            if constexpr (kRing) {
+                if (it == 0) plain_barrier<0>();
+                else plain_barrier<C::loads>();
+            } else {
+                if (it == 0) pid = step_barrier<0>(bt, cur_page);
+                else pid = step_barrier<C::loads>(bt, cur_page);
+            }
+            const int stage_j = it + C::D;
+
+            f32x16 s = f32x16{};
+            if constexpr (kQK) {
+                const uint8_t* kt = tiles + slot_offset(it, C::NT, kTileBytes);
+                // every wave computes, also one whose rows all lie past the end
+                // (its results are never stored): a branch here would force the
+                // accumulators through a register-class join.
+                // Scores S^T[token][row], K = 576 in 36 steps, the operand reads
+                // kAhead steps ahead of the matrix instructions.  Low-bit: the 36
+                // pieces of the next tile's dequantization (reading staging slot
+                // (it+1) % NS, writing tile slot (it+1) % NT, which the aggregation
+                // of tile it-2 released before this step's barrier) fill the
+                // matrix pipe's shadow, one per k-step.
+                Dq<kDqKind> dq;
+                uint8_t* next_tile = tiles + slot_offset(it + 1, C::NT, kTileBytes);
+                if constexpr (C::lowbit) {
+                    dq_read<kDqKind>(dq, stages + slot_offset(it + 1, C::NS, C::stage_bytes), tid);
+                    dq_split<kDqKind>(dq, 0);
                 }
+                // k-step kk reads logical chunk 2kk + half: physical 2kk + half (+ kk/4 grouped)
+                const uint8_t* krow = kt + row_off(C::SC, qk_row) + 16 * half;
+                auto kread_off = [](int kk) { return 16 * (2 * kk + (C::grouped ? kk >> 2 : 0)); };
+                constexpr int kAhead = 3;
+                OpT kb[kAhead];
+#pragma unroll
+                for (int j = 0; j < kAhead; ++j) kb[j] = *reinterpret_cast<const OpT*>(krow + kread_off(j));
+                // Scheduling barriers after every k-step keep this order (left
+                // free, the scheduler trades the read-ahead for registers and every
+                // product then waits on LDS latency).
                 __builtin_amdgcn_sched_barrier(0);
-            }
-        } else if constexpr (kQK) {
 #pragma unroll
-            for (int q = 0; q < 11; ++q) softmax_piece(q);
+                for (int kk = 0; kk < kKSteps; ++kk) {
+                    s = mfma(kb[kk % kAhead], qf[kk], s);
+                    if (kk + kAhead < kKSteps) kb[kk % kAhead] = *reinterpret_cast<const OpT*>(krow + kread_off(kk + kAhead));
+                    if constexpr (C::lowbit) dq_step<kDqKind>(dq, kk, next_tile, tid);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                if constexpr (C::lowbit) {
 #pragma unroll
-            for (int k = 0; k < C::loads; ++k) issue(k, pid, cur_t0, stage_j);
-        }
-        if constexpr (kQK) {
-            pb_prev[0] = __builtin_bit_cast(OpT, make_uint4(pw[0], pw[1], pw[2], pw[3]));
-            pb_prev[1] = __builtin_bit_cast(OpT, make_uint4(pw[4], pw[5], pw[6], pw[7]));
-            move_pending = move;
-            alpha_pending = alpha;
-            // advance the staging cursor (it stays on the last tile)
-            if (stage_j + 1 < n_tiles) {
-                cur_t0 += kTile;
-                if (cur_t0 % P == 0) ++cur_page;
+                    for (int s = kKSteps; s < kKSteps + 3; ++s) dq_step<kDqKind>(dq, s, next_tile, tid);
+                }
+                // rows see every key of the tile except in the last tile of the
+                // range or the tile holding the newest key (block-uniform test)
+                // (and, in a packed phase under protection, the tile holding the
+                // last sink token)
+                const int t0 = t_begin + it * kTile;
+                bool edge = t0 + kTile > full_lim;
+                if constexpr (kProt) edge = edge || t0 < t_lo;
+                if (edge) {
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int t = t0 + 8 * (v >> 2) + 4 * half + (v & 3);
+                        bool ok = t < lim;
+                        if constexpr (kProt) ok = ok && t >= t_lo;
+                        s[v] = ok ? s[v] : -INFINITY;
+                    }
+                }
             }
+            if constexpr (kPV) {
+                if (move_pending) {
+                    // the previous tile moved the reference: its weights are on the
+                    // new one, the accumulators follow before they are added
+#pragma unroll
+                    for (int m = 0; m < 16; ++m) scale_acc(acc[m], alpha_pending);
+                }
+            }
+
+            // Softmax of tile it in pieces (interleaved with the aggregation of
+            // tile it-1 when there is one): 0-1 the tile maximum, 2 the reference
+            // (a move reaches the accumulators in the next step), 3-10 the
+            // weights, two per piece.
+            float mr = -INFINITY, nref = 0.0f;
+            bool move = false;
+            float alpha = 1.0f;
+            uint32_t pw[8];
+            // (The empty statements pin each piece's results where it is computed:
+            // the compiler would otherwise sink the work next to its first use,
+            // after the aggregation.)
+            auto softmax_piece = [&](int q) __attribute__((always_inline)) {
+                if (q == 0) {
+                    mr = s[0];
+#pragma unroll
+                    for (int v = 1; v < 8; ++v) mr = fmaxf(mr, s[v]);
+                    asm volatile("" : "+v"(mr));
+                } else if (q == 1) {
+#pragma unroll
+                    for (int v = 8; v < 16; ++v) mr = fmaxf(mr, s[v]);
+                    mr = max_halves(mr);
+                    asm volatile("" : "+v"(mr));
+                } else if (q == 2) {
+                    const float mt = mr * a.scale_log2;           // scale > 0: max commutes
+                    m_true = fmaxf(m_true, mt);
+                    if (m_ref == -INFINITY) m_ref = mt;          // first visible key: nothing accumulated yet
+                    move = __builtin_amdgcn_ballot_w64(mt > m_ref + kRefSlack) != 0;
+                    const float m_new = move ? fmaxf(m_ref, mt) : m_ref;   // finite for a row that moves
+                    alpha = m_new == m_ref ? 1.0f : __builtin_amdgcn_exp2f(m_ref - m_new);
+                    m_ref = m_new;
+                    l_run *= alpha;
+                    nref = m_ref == -INFINITY ? 0.0f : -m_ref;
+                    asm volatile("" : "+v"(nref), "+v"(l_run), "+v"(m_ref), "+v"(m_true), "+v"(alpha));
+                } else if (q < 11) {
+                    const int v2 = q - 3;
+                    const float p0 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2], a.scale_log2, nref));
+                    const float p1 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2 + 1], a.scale_log2, nref));
+                    l_run += p0 + p1;
+                    pw[v2] = C::lowbit ? pack_f16x2(p0, p1) : pack_bf16x2(p0, p1);
+                    asm volatile("" : "+v"(pw[v2]), "+v"(l_run));
+                }
+            };
+            constexpr int kStageSlot0 = 12, kStageGap = C::lowbit ? 4 : 2;
+
+            if constexpr (kPV) {
+                // latent aggregation of tile it-1: O^T[channel][row] += V^T . P^T;
+                // the V^T operand is read transposed from the token-major tile.
+                // Rows tr_kbase + 16 ks (+ 8): the row shift term of row + 8 is
+                // that of row + 2 (tr_kbase < 8), of row + 16 that of the row;
+                // channels 32 m + tr_col ..: logical chunk 4m + (0..3), physical
+                // + m/2 in the grouped layout
+                const uint8_t* vt = tiles + slot_offset(it + C::NT - 1, C::NT, kTileBytes);
+                const uint8_t* vbase = vt + row_off(C::SC, tr_kbase) + 2 * tr_col;
+                auto vread = [&](int stp) __attribute__((always_inline)) {
+                    const int ks = stp >> 4, m = stp & 15;
+                    const uint8_t* p = vbase + 16 * C::SC * 16 * ks + 64 * m + (C::grouped ? 16 * (m >> 1) : 0);
+                    const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+                    const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 16 * C::SC * 8 + 32));
+                    return __builtin_bit_cast(OpT, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+                };
+                constexpr int kVAhead = 2;
+                OpT vb[kVAhead];
+#pragma unroll
+                for (int j = 0; j < kVAhead; ++j) vb[j] = vread(j);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int stp = 0; stp < 32; ++stp) {
+                    const int m = stp & 15;
+                    acc[m] = mfma(vb[stp % kVAhead], pb_prev[stp >> 4], acc[m]);
+                    if (stp + kVAhead < 32) vb[stp % kVAhead] = vread(stp + kVAhead);
+                    if constexpr (kQK) {
+                        softmax_piece(stp);
+                        // the staging of tile it+D, one load per kStageGap k-steps
+                        const int k = (stp - kStageSlot0) / kStageGap;
+                        if (stp >= kStageSlot0 && (stp - kStageSlot0) % kStageGap == 0 && k < C::loads)
+                            issue(k, pid, cur_t0, stage_j);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            } else if constexpr (kQK) {
+#pragma unroll
+                for (int q = 0; q < 11; ++q) softmax_piece(q);
+#pragma unroll
+                for (int k = 0; k < C::loads; ++k) issue(k, pid, cur_t0, stage_j);
+            }
+            if constexpr (kQK) {
+                pb_prev[0] = __builtin_bit_cast(OpT, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+                pb_prev[1] = __builtin_bit_cast(OpT, make_uint4(pw[4], pw[5], pw[6], pw[7]));
+                move_pending = move;
+                alpha_pending = alpha;
+                // advance the staging cursor (it stays on the last tile)
+                if (stage_j + 1 < n_tiles) {
+                    cur_t0 += kTile;
+                    if (cur_t0 % P == 0) ++cur_page;
+                }
+            }
+        };
+
+        if (n_tiles > 0) {
+            // prologue part 2: tile 0 decoded (low-bit) before the first step
+            if constexpr (C::lowbit) {
+                (void)step_barrier<0>(bt, cur_page);
+                dequant_tile<kDqKind>(stages, tiles, tid);
+            }
+            step(0, std::true_type{}, std::false_type{});
+            for (int it = 1; it < n_tiles; ++it) step(it, std::true_type{}, std::true_type{});
+            step(n_tiles, std::false_type{}, std::true_type{});
+            // no direct-to-LDS load may outlive the workgroup's LDS
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         }
+
     };
 
-    if (n_tiles > 0) {
-        // prologue part 2: tile 0 decoded (low-bit) before the first step
-        if constexpr (C::lowbit) {
-            (void)step_barrier<0>(bt, cur_page);
-            dequant_tile<kDqKind>(stages, tiles, tid);
+    if constexpr (!kProt) {
+        int t_begin = 0, t_end = L;
+        if (a.split_tokens != 0) {
+            t_begin = max(split * a.split_tokens, 0);
+            t_end = min(split * a.split_tokens + a.split_tokens, L);
         }
-        step(0, std::true_type{}, std::false_type{});
-        for (int it = 1; it < n_tiles; ++it) step(it, std::true_type{}, std::true_type{});
-        step(n_tiles, std::false_type{}, std::true_type{});
-        // no direct-to-LDS load may outlive the workgroup's LDS
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        const int lim = row_ok ? min(L - a.s_q + qi + 1, t_end) : t_begin;   // keys t < lim are visible
+        const int full_lim = min(L - a.s_q + 1, t_end);    // every valid row sees keys t < full_lim
+        run(std::integral_constant<int, KIND>{}, std::false_type{}, t_begin, t_end, t_begin, lim, full_lim);
+    } else {
+        const int sink = a.sink, recent = a.recent;
+        const bool has_packed = L - recent > sink;          // else every token is protected
+        const int pk0 = has_packed ? sink / kTile : 0;
+        const int n_pk = has_packed ? (L - recent + kTile - 1) / kTile - pk0 : 0;
+        const int n_prot = has_packed ? sink + recent : L;
+        const int n_list = n_pk + (n_prot + kTile - 1) / kTile;
+        int u0 = 0, u1 = n_list;
+        if (a.split_tokens != 0) {
+            u0 = split * (a.split_tokens / kTile);
+            u1 = min(u0 + a.split_tokens / kTile, n_list);
+        }
+        if (u0 < n_pk) {
+            const int tb = kTile * (pk0 + u0);
+            const int te = min(kTile * (pk0 + min(u1, n_pk)), L - recent);
+            const int lim = row_ok ? min(L - a.s_q + qi + 1, te) : tb;
+            const int full_lim = min(L - a.s_q + 1, te);
+            run(std::integral_constant<int, KIND>{}, std::false_type{}, tb, te, sink, lim, full_lim);
+        }
+        if (u1 > n_pk) {
+            // every wave is done with the packed phase's LDS before the
+            // protected phase stages into the same memory
+            if (u0 < n_pk) __syncthreads();
+            ring_rows = sink + recent;
+            ring_nsink = min(sink, L);
+            const int r0 = max(sink, L - recent);       // first window position past the sink
+            ring_q0 = recent > 0 ? (r0 - sink) % recent : 0;
+            int64_t pslot = a.prot_slot[b];
+            pslot = pslot < 0 ? 0 : (pslot >= a.num_prot ? a.num_prot - 1 : pslot);
+            ring_base = a.prot + pslot * ring_rows * 1152;
+            // protected positions below x
+            auto below = [&](int x) { return min(max(x, 0), ring_nsink) + max(0, x - r0); };
+            const int vb = kTile * (max(u0, n_pk) - n_pk);
+            const int ve = min(kTile * (u1 - n_pk), n_prot);
+            const int lim = row_ok ? min(below(L - a.s_q + qi + 1), ve) : vb;
+            const int full_lim = min(below(L - a.s_q + 1), ve);
+            run(std::integral_constant<int, KIND_BF16>{}, std::true_type{}, vb, ve, 0, lim, full_lim);
+        }
     }
 
     if (!row_ok) return;
@@ -797,9 +907,23 @@ hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream
     const int blocks = ((a.num_work + 7) / 8) * 8 * RB;
     const dim3 grid(static_cast<unsigned>(blocks)), block(kThreads);
     switch (kind) {
-        case KIND_C4R4: hipLaunchKernelGGL(decode_kernel<KIND_C4R4>, grid, block, 0, stream, a); break;
-        case KIND_C2R4: hipLaunchKernelGGL(decode_kernel<KIND_C2R4>, grid, block, 0, stream, a); break;
-        case KIND_BF16: hipLaunchKernelGGL(decode_kernel<KIND_BF16>, grid, block, 0, stream, a); break;
+        case KIND_C4R4: hipLaunchKernelGGL((decode_kernel<KIND_C4R4, false>), grid, block, 0, stream, a); break;
+        case KIND_C2R4: hipLaunchKernelGGL((decode_kernel<KIND_C2R4, false>), grid, block, 0, stream, a); break;
+        case KIND_BF16: hipLaunchKernelGGL((decode_kernel<KIND_BF16, false>), grid, block, 0, stream, a); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_decode_protected(CacheKind kind, const DecodeArgs& a, hipStream_t stream) {
+    if (a.num_work == 0) return hipSuccess;
+    const int rows = a.s_q * a.H;
+    const int RB = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
+    const int blocks = ((a.num_work + 7) / 8) * 8 * RB;
+    const dim3 grid(static_cast<unsigned>(blocks)), block(kThreads);
+    switch (kind) {
+        case KIND_C4R4: hipLaunchKernelGGL((decode_kernel<KIND_C4R4, true>), grid, block, 0, stream, a); break;
+        case KIND_C2R4: hipLaunchKernelGGL((decode_kernel<KIND_C2R4, true>), grid, block, 0, stream, a); break;
+        default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }

@@ -30,6 +30,15 @@ struct AppendArgs {
     uint8_t* cache;
     int64_t num_slots;      // num_pages * page_size
     PageGeom g;
+    // BF16 protection writes (lowbit_append_kernel<CBITS, true> only)
+    uint8_t* prot;
+    int64_t num_prot;
+    const int32_t* token_seq;   // [n] sequence of each token
+    const int32_t* positions;   // [n] position of each token in its sequence
+    const int32_t* seq_lens;    // [B] lengths after the append
+    const int32_t* prot_slot;   // [B] buffer of each sequence
+    int32_t B;
+    int32_t sink, recent;
 };
 
 enum CacheKind { KIND_C4R4 = 0, KIND_C2R4 = 1, KIND_BF16 = 2 };
@@ -53,6 +62,11 @@ struct DecodeArgs {
     float* part_s;
     float* part_o;
     PageGeom g;             // for BF16: page_size and page_bytes only
+    // BF16 protection (decode_kernel<KIND, true> only)
+    const uint8_t* prot;    // protection buffers, num_prot x (sink + recent) rows of 1152 bytes
+    int64_t num_prot;
+    const int32_t* prot_slot;   // [B] buffer of each sequence
+    int32_t sink, recent;
 };
 
 struct CombineArgs {
@@ -68,6 +82,8 @@ struct CombineArgs {
 hipError_t launch_lowbit_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_bf16_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
+hipError_t launch_decode_protected(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
+hipError_t launch_lowbit_append_protected(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 
 }  // namespace mla

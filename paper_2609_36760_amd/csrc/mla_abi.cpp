@@ -19,7 +19,37 @@ constexpr int32_t kDr = 64;
 constexpr int32_t kGroup = 64;
 constexpr int32_t kTile = 32;
 
+constexpr int32_t kMaxProtRows = 65536;
+constexpr int64_t kProtRowBytes = (kDc + kDr) * 2;
+
 bool aligned(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+int check_policy(const mla_protect_policy* p) {
+    if (p == nullptr) return MLA_EINVAL;
+    if (p->sink < 0 || p->recent < 0) return MLA_EINVAL;
+    const int64_t rows = static_cast<int64_t>(p->sink) + p->recent;
+    if (rows < 1 || rows > kMaxProtRows) return MLA_EINVAL;
+    return MLA_OK;
+}
+
+// Tiles of 32 keys a sequence of length L is processed in under protection:
+// packed tiles from the one holding token `sink` up to token L - recent - 1,
+// then the protected rows (sink + recent of them, or all L when the packed
+// range is empty).
+int64_t protected_tile_count(int64_t L, int64_t sink, int64_t recent) {
+    const bool has_packed = L - recent > sink;
+    const int64_t n_pk = has_packed ? (L - recent + kTile - 1) / kTile - sink / kTile : 0;
+    const int64_t n_prot = has_packed ? sink + recent : L;
+    return n_pk + (n_prot + kTile - 1) / kTile;
+}
+
+// The protection arguments of a decode call (null: no protection).
+struct ProtDecode {
+    const mla_protect_policy* policy;
+    const void* prot;
+    int64_t num_prot;
+    const int32_t* prot_slot;
+};
 
 // Structural checks shared by both cache kinds.
 int check_shape(const mla_cache_format* f) {
@@ -85,12 +115,11 @@ int check_append(const uint16_t* c_kv, int64_t c_kv_stride, const uint16_t* k_ro
 
 int append_common(const mla_cache_format* f, bool lowbit, const uint16_t* c_kv, int64_t c_kv_stride,
                   const uint16_t* k_rope, int64_t k_rope_stride, const int64_t* slot_mapping, int32_t n,
-                  void* cache, int64_t num_pages, hipStream_t stream) {
+                  void* cache, int64_t num_pages, hipStream_t stream, mla::AppendArgs a = {}) {
     int st = lowbit ? check_lowbit_format(f) : check_shape(f);
     if (st != MLA_OK) return st;
     st = check_append(c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, n, cache, num_pages);
     if (st != MLA_OK || n == 0) return st;
-    mla::AppendArgs a{};
     a.c_kv = c_kv;
     a.c_kv_stride = c_kv_stride;
     a.k_rope = k_rope;
@@ -100,6 +129,7 @@ int append_common(const mla_cache_format* f, bool lowbit, const uint16_t* c_kv, 
     a.cache = static_cast<uint8_t*>(cache);
     a.num_slots = num_pages * f->page_size;
     a.g = lowbit ? lowbit_geom(f) : bf16_geom(f);
+    if (a.prot != nullptr) return hip_status(mla::launch_lowbit_append_protected(a, stream));
     return hip_status(lowbit ? mla::launch_lowbit_append(a, stream) : mla::launch_bf16_append(a, stream));
 }
 
@@ -107,9 +137,15 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
                   const void* cache, int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
                   const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H, float softmax_scale,
                   int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits, uint16_t* out,
-                  float* lse, float* part_m, float* part_s, float* part_o, hipStream_t stream) {
+                  float* lse, float* part_m, float* part_s, float* part_o, const ProtDecode* pd,
+                  hipStream_t stream) {
     int st = lowbit ? check_lowbit_format(f) : check_shape(f);
     if (st != MLA_OK) return st;
+    if (pd != nullptr) {
+        st = check_policy(pd->policy);
+        if (st != MLA_OK) return st;
+        if (pd->num_prot < 0) return MLA_EINVAL;
+    }
     if (B < 0 || num_pages < 0 || max_pages_per_seq <= 0 || split_tokens < 0) return MLA_EINVAL;
     if (s_q != 1 && s_q != 2) return MLA_EINVAL;
     if (H <= 0 || H % 16 != 0) return MLA_EINVAL;
@@ -121,6 +157,10 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
     if (num_pages == 0) return MLA_EINVAL;
     if (!aligned(cache, 256)) return MLA_EINVAL;
     if (!aligned(q_lat, 16) || !aligned(q_rope, 16)) return MLA_ENOTSUP;
+    if (pd != nullptr) {
+        if (pd->prot == nullptr || pd->prot_slot == nullptr || pd->num_prot == 0) return MLA_EINVAL;
+        if (!aligned(pd->prot, 16)) return MLA_ENOTSUP;
+    }
     if (split_tokens == 0) {
         if (out == nullptr) return MLA_EINVAL;
         if (!aligned(out, 8)) return MLA_ENOTSUP;
@@ -151,7 +191,13 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
     a.part_o = part_o;
     a.g = lowbit ? lowbit_geom(f) : bf16_geom(f);
     const mla::CacheKind kind = !lowbit ? mla::KIND_BF16 : (f->c_bits == 4 ? mla::KIND_C4R4 : mla::KIND_C2R4);
-    return hip_status(mla::launch_decode(kind, a, stream));
+    if (pd == nullptr) return hip_status(mla::launch_decode(kind, a, stream));
+    a.prot = static_cast<const uint8_t*>(pd->prot);
+    a.num_prot = pd->num_prot;
+    a.prot_slot = pd->prot_slot;
+    a.sink = pd->policy->sink;
+    a.recent = pd->policy->recent;
+    return hip_status(mla::launch_decode_protected(kind, a, stream));
 }
 
 }  // namespace
@@ -182,6 +228,71 @@ int mla_bf16_append(const mla_cache_format* f, const uint16_t* c_kv, int64_t c_k
                          stream);
 }
 
+int64_t mla_protect_buffer_bytes(const mla_cache_format* f, const mla_protect_policy* p) {
+    if (check_lowbit_format(f) != MLA_OK || check_policy(p) != MLA_OK) return -1;
+    return (static_cast<int64_t>(p->sink) + p->recent) * kProtRowBytes;
+}
+
+int mla_lowbit_quant_append_protected(const mla_cache_format* f, const mla_protect_policy* p,
+                                      const uint16_t* c_kv, int64_t c_kv_stride, const uint16_t* k_rope,
+                                      int64_t k_rope_stride, const int64_t* slot_mapping, int32_t n, void* cache,
+                                      int64_t num_pages, const int32_t* token_seq, const int32_t* positions,
+                                      const int32_t* seq_lens, const int32_t* prot_slot, int32_t B, void* prot,
+                                      int64_t num_prot, hipStream_t stream) {
+    int st = check_policy(p);
+    if (st != MLA_OK) return st;
+    if (B < 0 || num_prot < 0) return MLA_EINVAL;
+    if (n > 0) {
+        if (token_seq == nullptr || positions == nullptr || seq_lens == nullptr || prot_slot == nullptr ||
+            prot == nullptr || B == 0 || num_prot == 0)
+            return MLA_EINVAL;
+        if (!aligned(prot, 16)) return MLA_ENOTSUP;
+    }
+    mla::AppendArgs a{};
+    a.prot = static_cast<uint8_t*>(prot);
+    a.num_prot = num_prot;
+    a.token_seq = token_seq;
+    a.positions = positions;
+    a.seq_lens = seq_lens;
+    a.prot_slot = prot_slot;
+    a.B = B;
+    a.sink = p->sink;
+    a.recent = p->recent;
+    return append_common(f, true, c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, n, cache, num_pages,
+                         stream, a);
+}
+
+int32_t mla_plan_splits_protected(const int32_t* seq_lens, int32_t B, int32_t split_tokens,
+                                  const mla_protect_policy* p, int32_t* split_indptr) {
+    if (seq_lens == nullptr || split_indptr == nullptr || B < 0 || split_tokens <= 0) return -MLA_EINVAL;
+    if (check_policy(p) != MLA_OK) return -MLA_EINVAL;
+    if (split_tokens % kTile != 0) return -MLA_ENOTSUP;
+    const int64_t per_split = split_tokens / kTile;
+    int64_t total = 0;
+    split_indptr[0] = 0;
+    for (int32_t b = 0; b < B; ++b) {
+        if (seq_lens[b] < 1) return -MLA_EINVAL;
+        total += (protected_tile_count(seq_lens[b], p->sink, p->recent) + per_split - 1) / per_split;
+        if (total > INT32_MAX) return -MLA_EINVAL;
+        split_indptr[b + 1] = static_cast<int32_t>(total);
+    }
+    return static_cast<int32_t>(total);
+}
+
+int mla_lowbit_decode_attn_protected(const mla_cache_format* f, const mla_protect_policy* p,
+                                     const uint16_t* q_lat, const uint16_t* q_rope, const void* cache,
+                                     int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
+                                     const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
+                                     float softmax_scale, const void* prot, int64_t num_prot,
+                                     const int32_t* prot_slot, int32_t split_tokens, const int32_t* split_indptr,
+                                     int32_t num_splits, uint16_t* out, float* lse, float* part_m, float* part_s,
+                                     float* part_o, hipStream_t stream) {
+    const ProtDecode pd{p, prot, num_prot, prot_slot};
+    return decode_common(f, true, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
+                         s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
+                         part_o, &pd, stream);
+}
+
 int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens, int32_t* split_indptr) {
     if (seq_lens == nullptr || split_indptr == nullptr || B < 0 || split_tokens <= 0) return -MLA_EINVAL;
     if (split_tokens % kTile != 0) return -MLA_ENOTSUP;
@@ -204,7 +315,7 @@ int mla_lowbit_decode_attn(const mla_cache_format* f, const uint16_t* q_lat, con
                            float* part_o, hipStream_t stream) {
     return decode_common(f, true, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
                          s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
-                         part_o, stream);
+                         part_o, nullptr, stream);
 }
 
 int mla_bf16_decode_attn(const mla_cache_format* f, const uint16_t* q_lat, const uint16_t* q_rope,
@@ -214,7 +325,7 @@ int mla_bf16_decode_attn(const mla_cache_format* f, const uint16_t* q_lat, const
                          float* lse, float* part_m, float* part_s, float* part_o, hipStream_t stream) {
     return decode_common(f, false, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
                          s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
-                         part_o, stream);
+                         part_o, nullptr, stream);
 }
 
 int mla_splitkv_combine(const float* part_m, const float* part_s, const float* part_o, const int32_t* split_indptr,

@@ -14,6 +14,13 @@
 // Work split: 8 lanes per group of 64 channels, each lane owning 8 channels
 // (one 16-byte load); min/max are reduced across the 8 lanes.  A token has 9
 // groups: 8 content groups (d_c = 512) and one RoPE-key group (d_r = 64).
+//
+// With BF16 protection (Sec. 3.3; Appendix C.5, "BF16 protection and cache
+// lifecycle") the same lanes also store the bf16 values they loaded into the
+// token's row of its sequence's protection buffer when the token is protected
+// once the append is done: position p < sink (row p) or p >= L - recent
+// (row sink + (p - sink) mod recent, a ring), L the sequence's new length.
+// Tokens leaving the window keep the packed copy written here at insertion.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -40,7 +47,7 @@ __device__ inline uint16_t f16_bits(float v) {
     return __builtin_bit_cast(uint16_t, h);
 }
 
-template <int CBITS>
+template <int CBITS, bool kProt>
 __global__ __launch_bounds__(kThreads) void lowbit_append_kernel(AppendArgs a) {
     const int64_t tid = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
     const int64_t gid = tid / kLanesPerGroup;           // the 8 lanes of a group share gid
@@ -54,8 +61,25 @@ __global__ __launch_bounds__(kThreads) void lowbit_append_kernel(AppendArgs a) {
     const bool rope = (g == kGroupsPerToken - 1);
     const uint16_t* src = rope ? a.k_rope + token * a.k_rope_stride + lig * 8
                                : a.c_kv + token * a.c_kv_stride + g * kGroup + lig * 8;
+    const uint4 raw = *reinterpret_cast<const uint4*>(src);
     float x[8];
-    widen_bf16x8(*reinterpret_cast<const uint4*>(src), x);
+    widen_bf16x8(raw, x);
+
+    if constexpr (kProt) {
+        const int bseq = a.token_seq[token];
+        if (bseq >= 0 && bseq < a.B) {
+            const int p = a.positions[token];
+            const int L = a.seq_lens[bseq];
+            const int64_t ps = a.prot_slot[bseq];
+            // p >= L - recent with p < L implies recent >= 1
+            if (p >= 0 && p < L && (p < a.sink || p >= L - a.recent) && ps >= 0 && ps < a.num_prot) {
+                const int prow = p < a.sink ? p : a.sink + (p - a.sink) % a.recent;
+                uint8_t* dst = a.prot + (ps * (a.sink + a.recent) + prow) * 1152 +
+                               (rope ? 1024 + lig * 16 : (g * kGroup + lig * 8) * 2);
+                *reinterpret_cast<uint4*>(dst) = raw;
+            }
+        }
+    }
 
     float lo = x[0], hi = x[0];
 #pragma unroll
@@ -126,9 +150,20 @@ hipError_t launch_lowbit_append(const AppendArgs& a, hipStream_t stream) {
     const int64_t threads = static_cast<int64_t>(a.n) * kGroupsPerToken * kLanesPerGroup;
     const dim3 grid(static_cast<unsigned>((threads + kThreads - 1) / kThreads));
     if (a.g.c_bits == 4)
-        hipLaunchKernelGGL(lowbit_append_kernel<4>, grid, dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL((lowbit_append_kernel<4, false>), grid, dim3(kThreads), 0, stream, a);
     else
-        hipLaunchKernelGGL(lowbit_append_kernel<2>, grid, dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL((lowbit_append_kernel<2, false>), grid, dim3(kThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_lowbit_append_protected(const AppendArgs& a, hipStream_t stream) {
+    if (a.n == 0) return hipSuccess;
+    const int64_t threads = static_cast<int64_t>(a.n) * kGroupsPerToken * kLanesPerGroup;
+    const dim3 grid(static_cast<unsigned>((threads + kThreads - 1) / kThreads));
+    if (a.g.c_bits == 4)
+        hipLaunchKernelGGL((lowbit_append_kernel<4, true>), grid, dim3(kThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL((lowbit_append_kernel<2, true>), grid, dim3(kThreads), 0, stream, a);
     return hipGetLastError();
 }
 

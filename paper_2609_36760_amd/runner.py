@@ -26,9 +26,15 @@ def _dev(a, device):
 class DecodeRun:
     def __init__(self, w: syn.Workload, layer: int = 0, kind: str = "lowbit", device: str = "cuda",
                  split_tokens: int | None = None, seq_lens=None, threads: int = 16, prefill: bool = True,
-                 token_cache: dict | None = None):
+                 token_cache: dict | None = None, protect=None, prot_slots=None):
+        """``protect``: an ``mla_protect_policy`` to keep sink/recent tokens in
+        bf16 (low-bit caches only); ``prot_slots``: the protection buffer of
+        each sequence (default: buffer b for sequence b)."""
         if kind not in ("lowbit", "bf16"):
             raise ValueError(kind)
+        if protect is not None and kind != "lowbit":
+            raise ValueError("protection applies to low-bit caches")
+        self.protect = protect
         self.w, self.layer, self.kind, self.device = w, layer, kind, device
         self.c_bits, self.r_bits = w.layers[layer]
         self.fmt = mb.cache_format(c_bits=self.c_bits)
@@ -47,9 +53,19 @@ class DecodeRun:
         ql, qr = syn.queries(w, layer)
         self.q_lat = _dev(ql.view(np.int16), device)
         self.q_rope = _dev(qr.view(np.int16), device)
+        if protect is not None:
+            slots = np.arange(self.B, dtype=np.int32) if prot_slots is None else np.asarray(prot_slots, np.int32)
+            self.num_prot = int(slots.max()) + 1
+            self.prot_bytes = mb.mla_protect_buffer_bytes(self.fmt, protect)
+            self.prot = torch.zeros(self.num_prot * self.prot_bytes, dtype=torch.uint8, device=device)
+            self.prot_slot_host = slots
+            self.prot_slot = _dev(slots, device)
         self.split_tokens = w.split_tokens if split_tokens is None else split_tokens
         if self.split_tokens:
-            indptr, total = mb.mla_plan_splits(lens, self.split_tokens)
+            if protect is not None:
+                indptr, total = mb.mla_plan_splits_protected(lens, self.split_tokens, protect)
+            else:
+                indptr, total = mb.mla_plan_splits(lens, self.split_tokens)
             self.split_indptr_host = indptr
             self.split_indptr = _dev(indptr, device)
             self.num_splits = total
@@ -73,26 +89,38 @@ class DecodeRun:
         self.new_c = _dev(np.concatenate(new_c).view(np.int16), device)
         self.new_k = _dev(np.concatenate(new_k).view(np.int16), device)
         self.new_slots = _dev(np.concatenate(new_slots), device)
+        if protect is not None:
+            self.new_seq = _dev(np.repeat(np.arange(self.B, dtype=np.int32), self.s_q), device)
+            self.new_pos = _dev(np.concatenate([np.arange(int(l) - self.s_q, int(l), dtype=np.int32)
+                                                for l in lens]), device)
+            hist = np.maximum(lens.astype(np.int64) - self.s_q, 0).astype(np.int32)
+            self.hist_lens = _dev(hist, device)
         self.token_cache = token_cache
         if prefill:
             self._prefill(threads)
 
-    def _append(self, c, k, slots):
+    def _append(self, c, k, slots, seq=None, pos=None):
+        if self.protect is not None:
+            mb.mla_lowbit_quant_append_protected(self.fmt, self.protect, c, k, slots, self.cache, self.num_pages,
+                                                 seq, pos, self.hist_lens, self.prot_slot, self.prot,
+                                                 self.num_prot)
+            return
         fn = mb.mla_lowbit_quant_append if self.kind == "lowbit" else mb.mla_bf16_append
         fn(self.fmt, c, k, slots, self.cache, self.num_pages)
 
     def _prefill(self, threads: int, chunk_tokens: int = 1 << 20):
         """Write every sequence's history (all but the step's s_q new tokens)."""
-        pend_c, pend_k, pend_s, pend_n = [], [], [], 0
+        pend_c, pend_k, pend_s, pend_b, pend_p, pend_n = [], [], [], [], [], 0
 
         def flush():
-            nonlocal pend_c, pend_k, pend_s, pend_n
+            nonlocal pend_c, pend_k, pend_s, pend_b, pend_p, pend_n
             if pend_n:
                 self._append(_dev(np.concatenate(pend_c).view(np.int16), self.device),
                              _dev(np.concatenate(pend_k).view(np.int16), self.device),
-                             _dev(np.concatenate(pend_s), self.device))
+                             _dev(np.concatenate(pend_s), self.device),
+                             _dev(np.concatenate(pend_b), self.device), _dev(np.concatenate(pend_p), self.device))
                 torch.cuda.synchronize()
-            pend_c, pend_k, pend_s, pend_n = [], [], [], 0
+            pend_c, pend_k, pend_s, pend_b, pend_p, pend_n = [], [], [], [], [], 0
 
         hist = np.maximum(self.lens.astype(np.int64) - self.s_q, 0)
         tc = self.token_cache
@@ -112,22 +140,38 @@ class DecodeRun:
             pend_c.append(c)
             pend_k.append(k)
             pend_s.append(syn.slots_of(self.block_table_host[b], np.arange(n)))
+            pend_b.append(np.full(n, b, np.int32))
+            pend_p.append(np.arange(n, dtype=np.int32))
             pend_n += n
             if pend_n >= chunk_tokens:
                 flush()
         flush()
 
     def append_new_tokens(self, stream=None):
+        if self.protect is not None:
+            mb.mla_lowbit_quant_append_protected(self.fmt, self.protect, self.new_c, self.new_k, self.new_slots,
+                                                 self.cache, self.num_pages, self.new_seq, self.new_pos,
+                                                 self.seq_lens, self.prot_slot, self.prot, self.num_prot,
+                                                 stream=stream)
+            return
         fn = mb.mla_lowbit_quant_append if self.kind == "lowbit" else mb.mla_bf16_append
         fn(self.fmt, self.new_c, self.new_k, self.new_slots, self.cache, self.num_pages, stream=stream)
 
     def attend(self, stream=None):
         """Decode attention (+ combine when split); results in ``out``/``lse``."""
-        fn = mb.mla_lowbit_decode_attn if self.kind == "lowbit" else mb.mla_bf16_decode_attn
-        fn(self.fmt, self.q_lat, self.q_rope, self.cache, self.num_pages, self.block_table, self.seq_lens,
-           self.s_q, self.H, self.tau, split_tokens=self.split_tokens, split_indptr=self.split_indptr,
-           num_splits=self.num_splits, out=self.out, lse=self.lse, part_m=self.part_m,
-           part_s=self.part_s, part_o=self.part_o, stream=stream)
+        if self.protect is not None:
+            mb.mla_lowbit_decode_attn_protected(
+                self.fmt, self.protect, self.q_lat, self.q_rope, self.cache, self.num_pages, self.block_table,
+                self.seq_lens, self.s_q, self.H, self.tau, self.prot, self.num_prot, self.prot_slot,
+                split_tokens=self.split_tokens, split_indptr=self.split_indptr, num_splits=self.num_splits,
+                out=self.out, lse=self.lse, part_m=self.part_m, part_s=self.part_s, part_o=self.part_o,
+                stream=stream)
+        else:
+            fn = mb.mla_lowbit_decode_attn if self.kind == "lowbit" else mb.mla_bf16_decode_attn
+            fn(self.fmt, self.q_lat, self.q_rope, self.cache, self.num_pages, self.block_table, self.seq_lens,
+               self.s_q, self.H, self.tau, split_tokens=self.split_tokens, split_indptr=self.split_indptr,
+               num_splits=self.num_splits, out=self.out, lse=self.lse, part_m=self.part_m,
+               part_s=self.part_s, part_o=self.part_o, stream=stream)
         if self.split_tokens:
             mb.mla_splitkv_combine(self.part_m, self.part_s, self.part_o, self.split_indptr, self.B, self.s_q,
                                    self.H, self.out, self.lse, stream=stream)
@@ -151,7 +195,15 @@ class DecodeRun:
             return 1152
         return (512 * self.c_bits + 64 * self.r_bits) // 8 + 9 * 4
 
+    def key_bytes(self) -> int:
+        """Bytes of every cached key once (under protection, the
+        min(L, sink + recent) protected tokens as 1152-byte bf16 rows)."""
+        L = self.lens.astype(np.int64)
+        if self.protect is None:
+            return int(L.sum()) * self.cache_token_bytes()
+        n_prot = np.minimum(L, self.protect.sink + self.protect.recent)
+        return int(((L - n_prot) * self.cache_token_bytes() + n_prot * 1152).sum())
+
     def cache_bytes_read(self) -> int:
         """Cache bytes attention reads per step (every key once per 128-row block)."""
-        row_blocks = math.ceil(self.s_q * self.H / 128)
-        return int(self.lens.astype(np.int64).sum()) * self.cache_token_bytes() * row_blocks
+        return self.key_bytes() * math.ceil(self.s_q * self.H / 128)

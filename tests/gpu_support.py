@@ -33,6 +33,7 @@ import numpy as np
 
 from oracle import attention as at
 from oracle import paged_cache as pc
+from oracle import protection as pr
 from oracle import quantizer as qz
 from paper_2609_36760_amd import synthetic as syn
 
@@ -137,6 +138,24 @@ def check_sequence(stats, run, b, heads=None):
     got_lse = run.lse[b].cpu().numpy()[:, hs]
     bound = lse_bound(ql[0][:, hs], qr[0][:, hs], c_hat, kr_hat, w.tau, L, w.s_q)
     tol = elem_bound(ql[0][:, hs], qr[0][:, hs], c_hat, kr_hat, w.tau, L, w.s_q, want_out, bound)
+    stats.add(got, want_out, got_lse, want_lse, bound, tol)
+
+
+def check_sequence_protected(stats, run, b, heads=None):
+    """As :func:`check_sequence` for a run under BF16 protection: the oracle
+    attends every token in its single representation (bf16 inside P_L)."""
+    w, L = run.w, int(run.lens[b])
+    c_bits, r_bits = w.layers[run.layer]
+    c, k = syn.sequence_tokens(w, run.layer, b, L)
+    c_rep, k_rep = pr.representation(pc.CacheFormat(c_bits=c_bits, r_bits=r_bits), c, k,
+                                     run.protect.sink, run.protect.recent)
+    ql, qr = syn.queries(w, run.layer, batch=[b])
+    hs = np.arange(w.H) if heads is None else np.asarray(heads)
+    want_out, want_lse = at.decode_sequence(ql[0], qr[0], c_rep, k_rep, w.tau, heads=hs)
+    got = bf16_bits_to_f64(run.out[b].cpu().numpy())[:, hs]
+    got_lse = run.lse[b].cpu().numpy()[:, hs]
+    bound = lse_bound(ql[0][:, hs], qr[0][:, hs], c_rep, k_rep, w.tau, L, w.s_q)
+    tol = elem_bound(ql[0][:, hs], qr[0][:, hs], c_rep, k_rep, w.tau, L, w.s_q, want_out, bound)
     stats.add(got, want_out, got_lse, want_lse, bound, tol)
 
 

@@ -32,7 +32,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(mb):
     names = declared_functions()
-    assert len(names) == 10
+    assert len(names) == 14
     lib = ctypes.CDLL(mb.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -108,4 +108,77 @@ def test_append_and_combine_validation(mb):
     assert lib.mla_splitkv_combine(16, 16, 16, 16, 1, 3, 128, 512, 16, None, None) == 1
     assert lib.mla_splitkv_combine(16, 16, 16, 16, 1, 1, 128, 256, 16, None, None) == 2
     assert lib.mla_splitkv_combine(16, 16, 16, 16, 0, 1, 128, 512, 16, None, None) == 0
+    assert lib.mla_last_hip_error() == 0
+
+
+def test_protection_buffer_bytes(mb):
+    fmt = mb.cache_format()
+    assert mb.mla_protect_buffer_bytes(fmt, mb.protect_policy()) == 152064      # 132 rows x 1152 B
+    assert mb.mla_protect_buffer_bytes(fmt, mb.protect_policy(0, 1)) == 1152
+    assert mb.mla_protect_buffer_bytes(mb.cache_format(c_bits=2), mb.protect_policy(3, 0)) == 3456
+    assert mb.mla_protect_buffer_bytes(fmt, mb.protect_policy(-1, 4)) == -1
+    assert mb.mla_protect_buffer_bytes(fmt, mb.protect_policy(0, 0)) == -1
+    assert mb.mla_protect_buffer_bytes(fmt, mb.protect_policy(0, 65537)) == -1
+    assert mb.mla_protect_buffer_bytes(mb.cache_format(c_bits=3), mb.protect_policy()) == -1
+
+
+def test_planner_protected(mb):
+    """Tile lists (sink 4, recent 128): L=1 -> 1 protected tile; 132 -> 5 (every
+    token protected); 133 -> 1 packed tile (tokens 4) + 5; 4096 -> 124 packed
+    tiles (tokens 4..3967) + 5.  Policy (40, 8), L=100: packed tiles 1..2
+    (tokens 40..91) + 2 tiles of 48 protected rows."""
+    lens = np.array([1, 132, 133, 4096], np.int32)
+    pol = mb.protect_policy()
+    indptr, total = mb.mla_plan_splits_protected(lens, 32, pol)
+    assert indptr.tolist() == [0, 1, 6, 12, 141] and total == 141
+    indptr, total = mb.mla_plan_splits_protected(lens, 512, pol)
+    assert indptr.tolist() == [0, 1, 2, 3, 12] and total == 12
+    indptr, total = mb.mla_plan_splits_protected(np.array([100], np.int32), 32, mb.protect_policy(40, 8))
+    assert total == 4
+    with pytest.raises(mb.MlaError):
+        mb.mla_plan_splits_protected(lens, 48, pol)
+    with pytest.raises(mb.MlaError):
+        mb.mla_plan_splits_protected(lens, 64, mb.protect_policy(-1, 2))
+    with pytest.raises(mb.MlaError):
+        mb.mla_plan_splits_protected(np.array([0], np.int32), 64, pol)
+
+
+def _prot_decode_status(mb, pol, prot=256, prot_slot=16, num_prot=1):
+    lib = mb.library()
+    fmt = mb.cache_format()
+    return lib.mla_lowbit_decode_attn_protected(ctypes.byref(fmt), ctypes.byref(pol), 16, 16, 256, 4, 16, 2, 16,
+                                                1, 1, 128, 0.07, prot, num_prot, prot_slot, 0, None, 0, 16, None,
+                                                None, None, None, None)
+
+
+def test_protected_entry_points_reject_before_any_hip_call(mb):
+    pol = mb.protect_policy()
+    assert _prot_decode_status(mb, mb.protect_policy(-1, 4)) == 1
+    assert _prot_decode_status(mb, mb.protect_policy(0, 0)) == 1
+    assert _prot_decode_status(mb, pol, prot=None) == 1
+    assert _prot_decode_status(mb, pol, prot_slot=None) == 1
+    assert _prot_decode_status(mb, pol, num_prot=0) == 1
+    assert _prot_decode_status(mb, pol, num_prot=-1) == 1
+    assert _prot_decode_status(mb, pol, prot=264) == 2                   # not 16-byte aligned
+    lib = mb.library()
+    fmt = mb.cache_format()
+    f, p = ctypes.byref(fmt), ctypes.byref(pol)
+    good = dict(token_seq=16, positions=16, seq_lens=16, prot_slot=16, B=1, prot=256, num_prot=1)
+
+    def app(**over):
+        a = dict(good, **over)
+        return lib.mla_lowbit_quant_append_protected(f, p, 16, 512, 16, 64, 16, 4, 256, 1, a["token_seq"],
+                                                     a["positions"], a["seq_lens"], a["prot_slot"], a["B"],
+                                                     a["prot"], a["num_prot"], None)
+    assert app(token_seq=None) == 1
+    assert app(prot=None) == 1
+    assert app(B=0) == 1
+    assert app(num_prot=0) == 1
+    assert app(prot=260) == 2
+    bad = mb.protect_policy(5, -1)
+    assert lib.mla_lowbit_quant_append_protected(f, ctypes.byref(bad), 16, 512, 16, 64, 16, 4, 256, 1, 16, 16, 16,
+                                                 16, 1, 256, 1, None) == 1
+    # n = 0 is a no-op once the policy is valid
+    assert lib.mla_lowbit_quant_append_protected(f, p, None, 512, None, 64, None, 0, None, 0, None, None, None,
+                                                 None, 0, None, 0, None) == 0
     assert lib.mla_last_hip_error() == 0
