@@ -51,7 +51,7 @@ def algorithmic_bytes(run) -> int:
     return keys + q + rows * 512 * 2
 
 
-def time_workload(name, kind, steps, warmup, layers, token_cache=None):
+def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=None, split_tokens=None):
     import torch
 
     from paper_2609_36760_amd import _binding as mb
@@ -59,8 +59,9 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None):
     from paper_2609_36760_amd.runner import DecodeRun
     w = syn.WORKLOADS[name]
     t0 = time.perf_counter()
-    run = DecodeRun(w, kind=kind, token_cache=token_cache)
+    run = DecodeRun(w, kind=kind, token_cache=token_cache, protect=protect, split_tokens=split_tokens)
     caches = [run.cache] + [run.cache.clone() for _ in range(layers - 1)]
+    prots = [None] * layers if protect is None else [run.prot] + [run.prot.clone() for _ in range(layers - 1)]
     torch.cuda.synchronize()
     log(f"[{name} {kind}] setup {time.perf_counter() - t0:.1f}s, cache {run.cache.numel() / 1e6:.1f} MB x {layers}")
     stream = torch.cuda.current_stream()
@@ -69,13 +70,26 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None):
     app = mb.mla_lowbit_quant_append if kind == "lowbit" else mb.mla_bf16_append
 
     def one_step(i, ev=None):
-        cache = caches[i % layers]
-        app(run.fmt, run.new_c, run.new_k, run.new_slots, cache, run.num_pages, stream=sh)
+        cache, prot = caches[i % layers], prots[i % layers]
+        if protect is None:
+            app(run.fmt, run.new_c, run.new_k, run.new_slots, cache, run.num_pages, stream=sh)
+        else:
+            mb.mla_lowbit_quant_append_protected(run.fmt, protect, run.new_c, run.new_k, run.new_slots, cache,
+                                                 run.num_pages, run.new_seq, run.new_pos, run.seq_lens,
+                                                 run.prot_slot, prot, run.num_prot, stream=sh)
         if ev is not None:
             ev[0].record(stream)
-        dec(run.fmt, run.q_lat, run.q_rope, cache, run.num_pages, run.block_table, run.seq_lens, run.s_q, run.H,
-            run.tau, split_tokens=run.split_tokens, split_indptr=run.split_indptr, num_splits=run.num_splits,
-            out=run.out, lse=run.lse, part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
+        if protect is None:
+            dec(run.fmt, run.q_lat, run.q_rope, cache, run.num_pages, run.block_table, run.seq_lens, run.s_q,
+                run.H, run.tau, split_tokens=run.split_tokens, split_indptr=run.split_indptr,
+                num_splits=run.num_splits, out=run.out, lse=run.lse, part_m=run.part_m, part_s=run.part_s,
+                part_o=run.part_o, stream=sh)
+        else:
+            mb.mla_lowbit_decode_attn_protected(
+                run.fmt, protect, run.q_lat, run.q_rope, cache, run.num_pages, run.block_table, run.seq_lens,
+                run.s_q, run.H, run.tau, prot, run.num_prot, run.prot_slot, split_tokens=run.split_tokens,
+                split_indptr=run.split_indptr, num_splits=run.num_splits, out=run.out, lse=run.lse,
+                part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
         if ev is not None:
             ev[1].record(stream)
         if run.split_tokens:
@@ -107,10 +121,12 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None):
     }
     res["mfma_frac"] = res["decode_kernel_tflops"] / PEAK_BF16_TFLOPS
     res["hbm_frac"] = res["decode_kernel_gbs"] / PEAK_HBM_GBS
-    log(f"[{name} {kind}] {ms_step * 1e3:.1f} us/step, decode kernel {kern_ms * 1e3:.1f} us = "
+    if protect is not None:
+        res["protect"] = {"sink": protect.sink, "recent": protect.recent}
+    log(f"[{name} {kind}{'' if protect is None else ' protected'}] {ms_step * 1e3:.1f} us/step, decode kernel {kern_ms * 1e3:.1f} us = "
         f"{res['decode_kernel_tflops']:.1f} TFLOP/s ({100 * res['mfma_frac']:.1f}% MFMA), "
         f"{res['decode_kernel_gbs']:.0f} GB/s ({100 * res['hbm_frac']:.1f}% HBM)")
-    del run, caches
+    del run, caches, prots
     torch.cuda.empty_cache()
     return res
 
@@ -176,7 +192,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-target", action="store_true", help="skip the batch-64 x 32K target shape")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--kinds", default="lowbit,bf16", help="cache kinds to time on the main workload")
+    ap.add_argument("--kinds", default="lowbit,bf16,protected",
+                    help="steps to time on the main workload: lowbit, bf16, protected (the low-bit cache with "
+                         "the 4 sink / 128 recent bf16 protection)")
+    ap.add_argument("--protect-split", type=int, default=0,
+                    help="key split of the protected step (0: as many splits per sequence as the unprotected plan)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="first copy a 256 MiB buffer once (reference for HBM traffic counters)")
     args = ap.parse_args()
@@ -204,6 +224,24 @@ def main():
         return
     main_bf = time_workload(MAIN, "bf16", args.steps, args.warmup, LAYERS)
     extra = {}
+    if "protected" in kinds:
+        from paper_2609_36760_amd import _binding as mb
+        from paper_2609_36760_amd import synthetic as syn
+        # as many key splits per sequence as the unprotected plan: the tile list
+        # (packed tiles + protected rows) is one tile longer than the sequence
+        w = syn.WORKLOADS[MAIN]
+        L, pol = w.context, mb.protect_policy(4, 128)
+        n_list = -(-(L - pol.recent) // 32) - pol.sink // 32 + -(-(pol.sink + pol.recent) // 32)
+        split = args.protect_split or 32 * -(-n_list // -(-L // w.split_tokens))
+        pr = time_workload(MAIN, "lowbit", args.steps, args.warmup, LAYERS, protect=pol, split_tokens=split)
+        extra["protected_sink4_recent128"] = {
+            "value": pr["decode_tokens_per_s"], "ms_per_step": pr["ms_per_step"],
+            "decode_kernel_ms": pr["decode_kernel_ms"], "decode_kernel_tflops": pr["decode_kernel_tflops"],
+            "mfma_frac": pr["mfma_frac"], "hbm_gbs": pr["decode_kernel_gbs"], "splits": pr["splits"],
+            "split_tokens": split,
+            "bytes_per_launch": pr["bytes_per_launch"],
+            "step_vs_unprotected": main_lb["ms_per_step"] / pr["ms_per_step"],
+            "speedup_vs_bf16": main_bf["ms_per_step"] / pr["ms_per_step"]}
     if not args.no_target:
         tc = {}
         t_lb = time_workload(TARGET, "lowbit", max(args.steps // 5, 5), 3, 1, token_cache=tc)
