@@ -20,6 +20,18 @@ and the page size in bytes is rounded up to a multiple of 256.  A slot is
 For ``d_c=512, d_r=64, P=64`` this is 20 736 B per page with 4-bit content
 (324 B per token) and 12 544 B with 2-bit content (196 B per token).
 
+The paper's own storage (``meta="paper"``; Appendix C.4 last sentence,
+Appendix C.5 "Storage layout"; reading 22 in DESIGN.md) keeps three regions::
+
+    codes_c[P][d_c * c_bits / 8]
+    codes_r[P][d_r * r_bits / 8]
+    meta   [P][32]   per token: bf16 content scales [d_c/64], byte content
+                     zero-points [d_c/64], fp32 RoPE scales [d_r/64], byte
+                     RoPE zero-points [d_r/64], zero padding to 32 bytes
+
+which is 320 B per token and 20 480 B per 64-token page with 4-bit content,
+the paper's figures (192 B and 12 288 B with 2-bit content).
+
 Pure numpy; shares no code with the GPU library.
 """
 from __future__ import annotations
@@ -38,6 +50,7 @@ class CacheFormat:
     c_bits: int = 4
     r_bits: int = 4
     page_size: int = 64
+    meta: str = "fp16"                      # or "paper"
 
     @property
     def codes_c_bytes(self) -> int:          # per token
@@ -56,18 +69,26 @@ class CacheFormat:
         return (self.d_r // qz.GROUP) * 4
 
     @property
+    def paper_meta_bytes(self) -> int:       # per token, paper storage
+        gc, gr = self.d_c // qz.GROUP, self.d_r // qz.GROUP
+        return (3 * gc + 5 * gr + 15) // 16 * 16
+
+    def region_sizes(self):
+        """Bytes per token of each page region, in page order."""
+        if self.meta == "paper":
+            return [self.codes_c_bytes, self.codes_r_bytes, self.paper_meta_bytes]
+        return [self.codes_c_bytes, self.codes_r_bytes, self.meta_c_bytes, self.meta_r_bytes]
+
+    @property
     def token_bytes(self) -> int:
-        return self.codes_c_bytes + self.codes_r_bytes + self.meta_c_bytes + self.meta_r_bytes
+        return sum(self.region_sizes())
 
     def region_offsets(self):
-        """Byte offset of each region inside a page."""
-        P = self.page_size
-        off_cc = 0
-        off_cr = off_cc + P * self.codes_c_bytes
-        off_mc = off_cr + P * self.codes_r_bytes
-        off_mr = off_mc + P * self.meta_c_bytes
-        end = off_mr + P * self.meta_r_bytes
-        return off_cc, off_cr, off_mc, off_mr, end
+        """Byte offset of each region inside a page, then the end of the last."""
+        offs = [0]
+        for n in self.region_sizes():
+            offs.append(offs[-1] + self.page_size * n)
+        return tuple(offs)
 
     @property
     def page_bytes(self) -> int:
@@ -86,13 +107,7 @@ def bf16_page_bytes(fmt: CacheFormat) -> int:
 def _token_byte_ranges(fmt: CacheFormat, slot: int):
     page, off = divmod(int(slot), fmt.page_size)
     base = page * fmt.page_bytes
-    cc, cr, mc, mr, _ = fmt.region_offsets()
-    return (
-        (base + cc + off * fmt.codes_c_bytes, fmt.codes_c_bytes),
-        (base + cr + off * fmt.codes_r_bytes, fmt.codes_r_bytes),
-        (base + mc + off * fmt.meta_c_bytes, fmt.meta_c_bytes),
-        (base + mr + off * fmt.meta_r_bytes, fmt.meta_r_bytes),
-    )
+    return tuple((base + o + off * n, n) for o, n in zip(fmt.region_offsets()[:-1], fmt.region_sizes()))
 
 
 def _meta_bytes(scale16: np.ndarray, zero16: np.ndarray) -> np.ndarray:
@@ -101,12 +116,33 @@ def _meta_bytes(scale16: np.ndarray, zero16: np.ndarray) -> np.ndarray:
     return pairs.reshape(pairs.shape[0], -1).astype('<f2').view(np.uint8)
 
 
-def encode_tokens(fmt: CacheFormat, c_kv_bits: np.ndarray, k_rope_bits: np.ndarray):
-    """Quantize and pack ``n`` tokens; returns the four per-token byte blocks."""
+def _paper_meta_bytes(fmt: CacheFormat, sc, zc, sr, zr) -> np.ndarray:
+    """The paper-storage metadata record of every token (layout above)."""
+    n = sc.shape[0]
+    rec = np.zeros((n, fmt.paper_meta_bytes), np.uint8)
+    gc, gr = sc.shape[1], sr.shape[1]
+    bf16_bits = (np.asarray(sc, np.float32).view(np.uint32) >> np.uint32(16)).astype('<u2')
+    rec[:, 0:2 * gc] = bf16_bits.view(np.uint8).reshape(n, 2 * gc)
+    rec[:, 2 * gc:3 * gc] = np.asarray(zc, np.uint8)
+    rec[:, 3 * gc:3 * gc + 4 * gr] = np.asarray(sr, '<f4').view(np.uint8).reshape(n, 4 * gr)
+    rec[:, 3 * gc + 4 * gr:3 * gc + 5 * gr] = np.asarray(zr, np.uint8)
+    return rec
+
+
+def _stored_meta(fmt: CacheFormat, c_kv_bits, k_rope_bits):
     c_kv_bits = np.asarray(c_kv_bits, np.uint16).reshape(-1, fmt.d_c)
     k_rope_bits = np.asarray(k_rope_bits, np.uint16).reshape(-1, fmt.d_r)
-    pc, sc, zc = qz.quantize_token_path(c_kv_bits, fmt.c_bits)
-    pr, sr, zr = qz.quantize_token_path(k_rope_bits, fmt.r_bits)
+    pc, sc, zc = qz.quantize_token_path(c_kv_bits, fmt.c_bits, fmt.meta, rope=False)
+    pr, sr, zr = qz.quantize_token_path(k_rope_bits, fmt.r_bits, fmt.meta, rope=True)
+    return pc, sc, zc, pr, sr, zr
+
+
+def encode_tokens(fmt: CacheFormat, c_kv_bits: np.ndarray, k_rope_bits: np.ndarray):
+    """Quantize and pack ``n`` tokens; returns the per-token byte block of
+    every page region."""
+    pc, sc, zc, pr, sr, zr = _stored_meta(fmt, c_kv_bits, k_rope_bits)
+    if fmt.meta == "paper":
+        return pc, pr, _paper_meta_bytes(fmt, sc, zc, sr, zr)
     return pc, pr, _meta_bytes(sc, zc), _meta_bytes(sr, zr)
 
 
@@ -129,17 +165,24 @@ def read_tokens(cache: np.ndarray, fmt: CacheFormat, slots):
     """Reconstruct fp32 content latents ``[n, d_c]`` and RoPE keys ``[n, d_r]``."""
     slots = np.asarray(slots, np.int64).reshape(-1)
     n = slots.size
-    pc = np.empty((n, fmt.codes_c_bytes), np.uint8)
-    pr = np.empty((n, fmt.codes_r_bytes), np.uint8)
-    mc = np.empty((n, fmt.meta_c_bytes), np.uint8)
-    mr = np.empty((n, fmt.meta_r_bytes), np.uint8)
+    blocks = [np.empty((n, size), np.uint8) for size in fmt.region_sizes()]
     for i, slot in enumerate(slots):
-        for (start, size), dst in zip(_token_byte_ranges(fmt, slot), (pc, pr, mc, mr)):
+        for (start, size), dst in zip(_token_byte_ranges(fmt, slot), blocks):
             dst[i] = cache[start:start + size]
-    mc16 = mc.view('<f2').reshape(n, -1, 2)
-    mr16 = mr.view('<f2').reshape(n, -1, 2)
-    c_hat = qz.dequantize_token_path(pc, mc16[..., 0], mc16[..., 1], fmt.c_bits)
-    kr_hat = qz.dequantize_token_path(pr, mr16[..., 0], mr16[..., 1], fmt.r_bits)
+    pc, pr = blocks[0], blocks[1]
+    if fmt.meta == "paper":
+        rec = blocks[2]
+        gc, gr = fmt.d_c // qz.GROUP, fmt.d_r // qz.GROUP
+        sc = qz.bf16_bits_to_f32(np.ascontiguousarray(rec[:, 0:2 * gc]).view('<u2'))
+        zc = rec[:, 2 * gc:3 * gc]
+        sr = np.ascontiguousarray(rec[:, 3 * gc:3 * gc + 4 * gr]).view('<f4')
+        zr = rec[:, 3 * gc + 4 * gr:3 * gc + 5 * gr]
+    else:
+        mc16 = blocks[2].view('<f2').reshape(n, -1, 2)
+        mr16 = blocks[3].view('<f2').reshape(n, -1, 2)
+        sc, zc, sr, zr = mc16[..., 0], mc16[..., 1], mr16[..., 0], mr16[..., 1]
+    c_hat = qz.dequantize_token_path(pc, sc, zc, fmt.c_bits)
+    kr_hat = qz.dequantize_token_path(pr, sr, zr, fmt.r_bits)
     return c_hat, kr_hat
 
 
@@ -149,10 +192,7 @@ def encode_sequence_dense(fmt: CacheFormat, c_kv_bits, k_rope_bits):
     Used where the oracle needs the reconstructed cache of many tokens at once:
     the values equal :func:`read_tokens` after :func:`write_tokens`.
     """
-    c_kv_bits = np.asarray(c_kv_bits, np.uint16).reshape(-1, fmt.d_c)
-    k_rope_bits = np.asarray(k_rope_bits, np.uint16).reshape(-1, fmt.d_r)
-    pc, sc, zc = qz.quantize_token_path(c_kv_bits, fmt.c_bits)
-    pr, sr, zr = qz.quantize_token_path(k_rope_bits, fmt.r_bits)
+    pc, sc, zc, pr, sr, zr = _stored_meta(fmt, c_kv_bits, k_rope_bits)
     c_hat = qz.dequantize_token_path(pc, sc, zc, fmt.c_bits)
     kr_hat = qz.dequantize_token_path(pr, sr, zr, fmt.r_bits)
     return c_hat, kr_hat

@@ -24,7 +24,12 @@ Readings taken where the paper leaves a choice (all listed in the design doc):
     ``fp16(s)`` (round-half-to-even, subnormals kept) and the stored zero is
     ``fp16(z)``, which is exact;
   * dequantization is ``fp16scale * (q - fp16zero)`` evaluated in fp32
-    (``q - z`` is exact, so this is a single rounding).
+    (``q - z`` is exact, so this is a single rounding);
+  * the paper's own storage (same paragraph, last sentence): content scales
+    in BF16 (``bf16(s)``, round-half-to-even), RoPE scales in FP32 (``s``
+    itself); the zero-point, whose dtype the paper leaves open, as an unsigned
+    byte (exact: an integer in ``[0, m]``).  Dequantization multiplies by the
+    stored scale the same way.
 
 Codes are packed little-endian inside a byte: for 4 bits channel ``2j`` sits in
 bits 0-3 of byte ``j`` and channel ``2j+1`` in bits 4-7; for 2 bits channel
@@ -75,6 +80,22 @@ def quantize_groups(x: np.ndarray, bits: int):
     return q, s, z
 
 
+def f32_to_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bf16 (ties to even), returned as
+    float32 values; finite inputs only."""
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    lsb = (b >> np.uint32(16)) & np.uint32(1)
+    r = ((b + np.uint32(0x7FFF) + lsb) >> np.uint32(16)) << np.uint32(16)
+    return r.astype(np.uint32).view(np.float32)
+
+
+def stored_meta_paper(s: np.ndarray, z: np.ndarray, rope: bool):
+    """The paper's stored scale (BF16 for the content path, FP32 for the RoPE
+    path) and the zero-point as an unsigned byte."""
+    s = np.asarray(s, dtype=np.float32)
+    return (s.copy() if rope else f32_to_bf16(s)), np.asarray(z, dtype=np.float32).astype(np.uint8)
+
+
 def stored_meta(s: np.ndarray, z: np.ndarray):
     """Stored fp16 scale and zero-point (round-half-to-even, subnormals kept)."""
     return (np.asarray(s, dtype=np.float32).astype(np.float16),
@@ -82,12 +103,14 @@ def stored_meta(s: np.ndarray, z: np.ndarray):
 
 
 def dequantize(q: np.ndarray, scale16: np.ndarray, zero16: np.ndarray) -> np.ndarray:
-    """``x_hat = scale * (q - zero)`` in fp32 with the stored fp16 metadata.
+    """``x_hat = scale * (q - zero)`` in fp32 with the stored metadata.
 
-    ``q`` has a trailing group axis of 64; ``scale16``/``zero16`` one value per group.
+    ``q`` has a trailing group axis of 64; ``scale16``/``zero16`` one value per
+    group, as stored (fp16, or the paper's bf16-valued / fp32 scales and byte
+    zero-points); every stored value widens exactly to fp32.
     """
-    sc = np.asarray(scale16, dtype=np.float16).astype(np.float32)[..., None]
-    ze = np.asarray(zero16, dtype=np.float16).astype(np.float32)[..., None]
+    sc = np.asarray(scale16).astype(np.float32)[..., None]
+    ze = np.asarray(zero16).astype(np.float32)[..., None]
     d = (np.asarray(q).astype(np.float32) - ze).astype(np.float32)   # exact: small integers
     return (sc * d).astype(np.float32)
 
@@ -118,19 +141,27 @@ def unpack_codes(packed: np.ndarray, bits: int) -> np.ndarray:
     return out.reshape(packed.shape[:-1] + (packed.shape[-1] * per,))
 
 
-def quantize_token_path(x_bits: np.ndarray, bits: int):
+def quantize_token_path(x_bits: np.ndarray, bits: int, meta: str = "fp16", rope: bool = False):
     """Quantize one cache path for a batch of tokens.
 
     ``x_bits``: bf16 bit patterns, shape ``[n, d]`` with ``d % 64 == 0``.
-    Returns ``(packed [n, d*bits/8] uint8, scale16 [n, d/64], zero16 [n, d/64])``.
+    Returns ``(packed [n, d*bits/8] uint8, scale [n, d/64], zero [n, d/64])``
+    with the metadata as stored: fp16 scale and zero (``meta="fp16"``), or the
+    paper's bf16 (content) / fp32 (RoPE, ``rope=True``) scale and byte zero
+    (``meta="paper"``).
     """
     x = bf16_bits_to_f32(x_bits)
     n, d = x.shape
     if d % GROUP:
         raise ValueError("path width must be a multiple of the group size")
     q, s, z = quantize_groups(x.reshape(n, d // GROUP, GROUP), bits)
-    s16, z16 = stored_meta(s, z)
-    return pack_codes(q.reshape(n, d), bits), s16, z16
+    if meta == "paper":
+        sm, zm = stored_meta_paper(s, z, rope)
+    elif meta == "fp16":
+        sm, zm = stored_meta(s, z)
+    else:
+        raise ValueError(meta)
+    return pack_codes(q.reshape(n, d), bits), sm, zm
 
 
 def dequantize_token_path(packed: np.ndarray, scale16: np.ndarray, zero16: np.ndarray,

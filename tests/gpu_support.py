@@ -13,16 +13,19 @@ Tolerances (attention, floating point):
     more than 2e-2 of the global RMS (and of their own channel RMS), for any
     kernel;
   * lse: |gpu - oracle| <= d_r + 1e-5 * |lse| per row, with
-    d_r = tau * 2^-8 * max_t sum_c |q_rc| |k_hat_tc|.  The kernel rounds the
-    reconstructed keys to bf16 once (relative error <= 2^-9 per element) and
-    accumulates in fp32, so every logit moves by at most
-    tau * 2^-9 * sum_c |q_c k_hat_c| (d_r takes twice that), and the
+    d_r = tau * 2^-8 * max_t sum_c |q_rc| |k_hat_tc|.  The kernels round a
+    reconstructed key at most once, to fp16 (low-bit kernels, relative error
+    <= 2^-11) or not at all (BF16 rows), and accumulate in fp32, so every
+    logit moves by at most tau * 2^-11 * sum_c |q_c k_hat_c| plus fp32
+    accumulation error -- d_r allows the bf16 unit roundoff 2^-8 -- and the
     log-sum-exp moves by at most the largest logit move;
   * every output element: |gpu - oracle|_rc <= 1.25 * (2^-8 |out_rc| +
     (2^-8 + 2.1 d_r) A_rc), A_rc = sum_t w_rt |c_hat_tc| with w the exact
-    attention weights.  Weights move by a factor within e^{+-2 d_r}; the bf16
-    roundings of the probabilities and of the reconstructed values each add
-    a relative 2^-9 per term, and the bf16 output adds 2^-9 |out|.
+    attention weights.  Weights move by a factor within e^{+-2 d_r}; the
+    rounding of the probabilities (bf16 at most, unit roundoff 2^-8) and of
+    the reconstructed values (fp16, 2^-11, or none) add at most a relative
+    2^-8 + 2^-11 per term (the factor 1.25 covers the 2^-11), and the bf16
+    output adds 2^-8 |out|.
     This bound holds for any row, including rows whose output is a single
     key with 10x outlier channels, where bf16 output rounding alone exceeds
     2e-2 of the output RMS.
