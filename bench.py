@@ -51,7 +51,8 @@ def algorithmic_bytes(run) -> int:
     return keys + q + rows * 512 * 2
 
 
-def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=None, split_tokens=None):
+def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=None, split_tokens=None,
+                  meta="fp16"):
     import torch
 
     from paper_2609_36760_amd import _binding as mb
@@ -59,7 +60,7 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
     from paper_2609_36760_amd.runner import DecodeRun
     w = syn.WORKLOADS[name]
     t0 = time.perf_counter()
-    run = DecodeRun(w, kind=kind, token_cache=token_cache, protect=protect, split_tokens=split_tokens)
+    run = DecodeRun(w, kind=kind, token_cache=token_cache, protect=protect, split_tokens=split_tokens, meta=meta)
     caches = [run.cache] + [run.cache.clone() for _ in range(layers - 1)]
     prots = [None] * layers if protect is None else [run.prot] + [run.prot.clone() for _ in range(layers - 1)]
     torch.cuda.synchronize()
@@ -123,7 +124,8 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
     res["hbm_frac"] = res["decode_kernel_gbs"] / PEAK_HBM_GBS
     if protect is not None:
         res["protect"] = {"sink": protect.sink, "recent": protect.recent}
-    log(f"[{name} {kind}{'' if protect is None else ' protected'}] {ms_step * 1e3:.1f} us/step, decode kernel {kern_ms * 1e3:.1f} us = "
+    tag = ("" if protect is None else " protected") + ("" if meta == "fp16" else f" {meta} metadata")
+    log(f"[{name} {kind}{tag}] {ms_step * 1e3:.1f} us/step, decode kernel {kern_ms * 1e3:.1f} us = "
         f"{res['decode_kernel_tflops']:.1f} TFLOP/s ({100 * res['mfma_frac']:.1f}% MFMA), "
         f"{res['decode_kernel_gbs']:.0f} GB/s ({100 * res['hbm_frac']:.1f}% HBM)")
     del run, caches, prots
@@ -192,9 +194,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-target", action="store_true", help="skip the batch-64 x 32K target shape")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--kinds", default="lowbit,bf16,protected",
+    ap.add_argument("--kinds", default="lowbit,bf16,protected,paper",
                     help="steps to time on the main workload: lowbit, bf16, protected (the low-bit cache with "
-                         "the 4 sink / 128 recent bf16 protection)")
+                         "the 4 sink / 128 recent bf16 protection), paper (the paper's metadata storage: bf16 "
+                         "content scales, fp32 RoPE scales, 320 B/token)")
     ap.add_argument("--protect-split", type=int, default=0,
                     help="key split of the protected step (0: as many splits per sequence as the unprotected plan)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -249,6 +252,15 @@ def main():
         del tc
         extra[TARGET] = {"c4r4": t_lb, "bf16": t_bf,
                          "speedup_vs_bf16": t_bf["ms_per_step"] / t_lb["ms_per_step"]}
+    if "paper" in kinds:
+        pp = time_workload(MAIN, "lowbit", args.steps, args.warmup, LAYERS, meta="paper")
+        extra["paper_storage_c4r4"] = {
+            "value": pp["decode_tokens_per_s"], "ms_per_step": pp["ms_per_step"],
+            "decode_kernel_ms": pp["decode_kernel_ms"], "decode_kernel_tflops": pp["decode_kernel_tflops"],
+            "mfma_frac": pp["mfma_frac"], "hbm_gbs": pp["decode_kernel_gbs"],
+            "bytes_per_launch": pp["bytes_per_launch"], "cache_bytes_per_token": 320,
+            "step_vs_fp16_metadata": main_lb["ms_per_step"] / pp["ms_per_step"],
+            "speedup_vs_bf16": main_bf["ms_per_step"] / pp["ms_per_step"]}
     cpu = None if args.no_cpu else cpu_baseline()
 
     line = {

@@ -48,9 +48,12 @@ enum { MLA_OK = 0, MLA_EINVAL = 1, MLA_ENOTSUP = 2, MLA_EHIP = 3 };
 /*
  * Cache format (Appendix C.4 "Affine group quantization", Appendix C.5
  * "Storage layout").  Supported: d_c = 512, d_r = 64, group = 64,
- * c_bits in {4, 2}, r_bits = 4, page_size a positive multiple of 32.
- * The BF16 cache calls read only d_c, d_r and page_size.
+ * c_bits in {4, 2}, r_bits = 4, page_size a positive multiple of 32,
+ * meta in {MLA_META_FP16, MLA_META_PAPER}.  The BF16 cache calls read only
+ * d_c, d_r and page_size.
  */
+enum { MLA_META_FP16 = 0, MLA_META_PAPER = 1 };
+
 typedef struct mla_cache_format {
     int32_t d_c;        /* content latent channels                         */
     int32_t d_r;        /* decoupled RoPE key channels                     */
@@ -58,20 +61,29 @@ typedef struct mla_cache_format {
     int32_t c_bits;     /* content code width                              */
     int32_t r_bits;     /* RoPE key code width                             */
     int32_t page_size;  /* tokens per page                                 */
+    int32_t meta;       /* metadata storage, MLA_META_*                    */
 } mla_cache_format;
 
 /*
- * Packed page layout.  A page of P tokens holds four token-major regions:
+ * Packed page layout, MLA_META_FP16.  A page of P tokens holds four
+ * token-major regions:
  *   codes_c[P][d_c*c_bits/8]   content codes
  *   codes_r[P][d_r*r_bits/8]   RoPE key codes
  *   meta_c [P][d_c/group]{fp16 scale, fp16 zero}
  *   meta_r [P][d_r/group]{fp16 scale, fp16 zero}
- * and the page size is rounded up to 256 bytes; the cache is num_pages such
+ * MLA_META_PAPER, the paper's storage (content scales in BF16, RoPE scales in
+ * FP32; Appendix C.4 last sentence), holds three:
+ *   codes_c[P][d_c*c_bits/8], codes_r[P][d_r*r_bits/8],
+ *   meta   [P][32]: bf16 content scales [8] (bytes 0-15), byte content
+ *          zero-points [8] (16-23), fp32 RoPE scale (24-27), byte RoPE
+ *          zero-point (28), zero (29-31)
+ * The page size is rounded up to 256 bytes; the cache is num_pages such
  * pages back to back from a 256-byte aligned base.  Inside a byte, codes are
  * little-endian fields: 4-bit channel 2j in bits 0-3 of byte j and 2j+1 in
  * bits 4-7; 2-bit channel 4j+k in bits 2k..2k+1.  Token t of page p is slot
  * p*P + t.  For d_c=512, d_r=64, P=64: 20736 bytes per page with 4-bit
- * content (324 B/token), 12544 with 2-bit content (196 B/token).
+ * content (324 B/token), 12544 with 2-bit content (196 B/token); with the
+ * paper's metadata 20480 (320 B/token, the paper's figure) and 12288.
  * A BF16 cache page holds P rows of d_c + d_r bf16 values (73728 B at P=64).
  * Both return -1 for an invalid format.
  */
@@ -86,7 +98,9 @@ int64_t mla_bf16_page_bytes(const mla_cache_format* f);
  *   s = max(xmax - xmin, 1e-8) / m     (m = 2^bits - 1, a true division)
  *   z = clip(rint(-xmin / s), 0, m)
  *   q = clip(rint(x / s + z), 0, m)    (divide, then add: two roundings)
- * stores q packed, fp16(s) and fp16(z) (fp16 subnormals kept).
+ * stores q packed and the metadata: fp16(s), fp16(z) (fp16 subnormals kept)
+ * under MLA_META_FP16; bf16(s) (round-half-to-even) for content groups, s
+ * itself (fp32) for the RoPE group and z as a byte under MLA_META_PAPER.
  *   c_kv     device, bf16 [n][c_kv_stride], first d_c used
  *   k_rope   device, bf16 [n][k_rope_stride], first d_r used (post-RoPE key)
  *   slot_mapping device, int64 [n]: destination slot; a negative slot skips
@@ -134,7 +148,7 @@ int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens
  *   z_t = softmax_scale * (q_lat[b,i,h,:] . C_hat[t,:] + q_rope[b,i,h,:] . K_hat[t,:])
  *   out[b,i,h,:] = sum_t softmax(z)_t C_hat[t,:],   lse[b,i,h] = ln sum_t e^{z_t}
  * where C_hat, K_hat are dequantized from the packed cache with the stored
- * fp16 scale and zero: x_hat = scale * (q - zero).
+ * scale and zero: x_hat = scale * (q - zero).
  *   q_lat   device, bf16 [B][s_q][H][d_c]  absorbed content query
  *   q_rope  device, bf16 [B][s_q][H][d_r]  RoPE-encoded query
  *   cache   device, packed pages; num_pages of them
@@ -158,7 +172,9 @@ int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens
  * Scores and latent aggregation run as fp16 matrix products with fp32
  * accumulation: the dequantized cache (x_hat, one fp16 rounding) and the
  * softmax weights are fp16 operands, so queries and x_hat must lie within the
- * fp16 range.  The output is rounded to bf16 once.
+ * fp16 range.  Under MLA_META_PAPER the RoPE scale enters as fp16(scale) (a
+ * second rounding of the RoPE key, relative 2^-11).  The output is rounded to
+ * bf16 once.
  */
 int mla_lowbit_decode_attn(const mla_cache_format* f,
                            const uint16_t* q_lat, const uint16_t* q_rope,

@@ -35,9 +35,13 @@ class MlaError(RuntimeError):
         super().__init__(msg)
 
 
+MLA_META_FP16, MLA_META_PAPER = 0, 1
+
+
 class mla_cache_format(ctypes.Structure):
     _fields_ = [("d_c", ctypes.c_int32), ("d_r", ctypes.c_int32), ("group", ctypes.c_int32),
-                ("c_bits", ctypes.c_int32), ("r_bits", ctypes.c_int32), ("page_size", ctypes.c_int32)]
+                ("c_bits", ctypes.c_int32), ("r_bits", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("meta", ctypes.c_int32)]
 
 
 class mla_protect_policy(ctypes.Structure):
@@ -50,8 +54,8 @@ def protect_policy(sink: int = 4, recent: int = 128) -> mla_protect_policy:
 
 
 def cache_format(c_bits: int = 4, page_size: int = 64, d_c: int = 512, d_r: int = 64,
-                 group: int = 64, r_bits: int = 4) -> mla_cache_format:
-    return mla_cache_format(d_c, d_r, group, c_bits, r_bits, page_size)
+                 group: int = 64, r_bits: int = 4, meta: int = MLA_META_FP16) -> mla_cache_format:
+    return mla_cache_format(d_c, d_r, group, c_bits, r_bits, page_size, meta)
 
 
 _lib = None

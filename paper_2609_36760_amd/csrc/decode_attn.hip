@@ -100,6 +100,7 @@ constexpr float kLn2 = 0.693147180559945309f;
 template <int KIND> struct Cfg;
 template <> struct Cfg<KIND_C4R4> {
     static constexpr bool lowbit = true;
+    static constexpr bool pmeta = false;                // fp16 {scale, zero} metadata regions
     static constexpr int cc = 256;                      // content code bytes per token
     static constexpr int code_rounds = 2;               // content codes: 2 x 256 chunks
     static constexpr int rcodes = kTile * cc, meta = rcodes + 1024, rmeta = meta + 1024,
@@ -110,6 +111,7 @@ template <> struct Cfg<KIND_C4R4> {
 };
 template <> struct Cfg<KIND_C2R4> {
     static constexpr bool lowbit = true;
+    static constexpr bool pmeta = false;
     static constexpr int cc = 128;
     static constexpr int code_rounds = 1;
     static constexpr int rcodes = kTile * cc, meta = rcodes + 1024, rmeta = meta + 1024,
@@ -118,8 +120,18 @@ template <> struct Cfg<KIND_C2R4> {
     static constexpr int SC = 84;
     static constexpr bool grouped = true;
 };
+// The paper's storage: one 32-byte metadata record per token (staged where
+// the content metadata goes; the RoPE metadata slot only receives a dummy
+// load that keeps the load count uniform).
+template <> struct Cfg<KIND_C4R4P> : Cfg<KIND_C4R4> {
+    static constexpr bool pmeta = true;
+};
+template <> struct Cfg<KIND_C2R4P> : Cfg<KIND_C2R4> {
+    static constexpr bool pmeta = true;
+};
 template <> struct Cfg<KIND_BF16> {
     static constexpr bool lowbit = false;
+    static constexpr bool pmeta = false;
     static constexpr int stage_bytes = 0;
     static constexpr int NT = 4, NS = 0, D = 2, loads = 10;   // 2432 chunks: 9 rounds of 256 + 128
     static constexpr int SC = 76;
@@ -146,6 +158,7 @@ static_assert(row_off(76, 16) - row_off(76, 15) >= 16 * 72, "plain rows do not o
 template <int KIND>
 constexpr int lds_bytes() { return Cfg<KIND>::NT * tile_bytes<KIND>() + Cfg<KIND>::NS * Cfg<KIND>::stage_bytes; }
 static_assert(lds_bytes<KIND_C4R4>() <= 160 * 1024, "LDS budget of a gfx950 CU");
+static_assert(lds_bytes<KIND_C4R4P>() == lds_bytes<KIND_C4R4>(), "same staging for both metadata layouts");
 static_assert(lds_bytes<KIND_BF16>() <= 160 * 1024, "LDS budget of a gfx950 CU");
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -263,9 +276,10 @@ __device__ __forceinline__ int load_page_id(const int32_t* table, int index) {
 
 // Packed tile: the content codes in whole rounds (chunk i of the region by
 // lane i % 64 of wave (i / 64) % 4), then one load per wave for the small
-// regions: wave 0 the RoPE codes, wave 1 the content metadata, wave 2 the RoPE
-// metadata, wave 3 the RoPE metadata again into a spare area (every wave
-// issues Cfg::loads loads).  Tokens at or past `nvalid` re-read token
+// regions: wave 0 the RoPE codes, wave 1 the content metadata (or the paper's
+// 32-byte records), wave 2 the RoPE metadata, wave 3 the RoPE metadata again
+// into a spare area (every wave issues Cfg::loads loads; under the paper's
+// storage wave 2 too loads into the spare area).  Tokens at or past `nvalid` re-read token
 // nvalid - 1 (per-token regions; a RoPE metadata chunk holds four tokens and
 // is read as it is -- such a token's score is masked and its RoPE channels
 // never enter the aggregation).  Load `k` of the Cfg::loads.
@@ -291,7 +305,7 @@ __device__ __forceinline__ void stage_lowbit(int k, const uint8_t* page, int po,
         dst_off = C::meta;
     } else {
         src_off = g.off_mr + po * 4 + (lane & 7) * 16;
-        dst_off = wave_u == 2 ? C::rmeta : C::spare;
+        dst_off = wave_u == 2 && !C::pmeta ? C::rmeta : C::spare;
     }
     if (wave_u < 2 || lane < 8) dma16(page, src_off, st_lds + dst_off);
 }
@@ -325,6 +339,16 @@ __device__ __forceinline__ void stage_bf16(int k, const uint8_t* src, RowStart r
 // Codes become fp16 values 1024 + q (the fp16 with bits 0x6400 | q, exact);
 // (1024 + q) - (1024 + zero) = q - zero exactly, and one fp16 multiply by the
 // stored scale rounds s * (q - zero) once.  Both in packed fp16 (2 per op).
+// The paper's storage: scale (bf16 bits, or fp32 for the RoPE group) and a
+// byte zero-point.  The bf16 scale converts to fp16 exactly inside the fp16
+// range; the fp32 RoPE scale is rounded to fp16 once.
+__device__ __forceinline__ void pmeta_to_f16(float scale, uint32_t zero, f16x2& zz, f16x2& ss) {
+    const _Float16 s = static_cast<_Float16>(scale);
+    const _Float16 zb = static_cast<_Float16>(static_cast<float>(zero) + 1024.0f);   // exact
+    zz = f16x2{zb, zb};
+    ss = f16x2{s, s};
+}
+
 __device__ __forceinline__ void meta_to_f16(uint32_t meta, f16x2& zz, f16x2& ss) {
     const _Float16 s = __builtin_bit_cast(_Float16, static_cast<uint16_t>(meta & 0xFFFFu));
     const _Float16 z = __builtin_bit_cast(_Float16, static_cast<uint16_t>(meta >> 16));
@@ -353,6 +377,9 @@ __device__ __forceinline__ int dq_row(int tid) {
 template <int KIND> struct Dq {
     uint4 c0, c1;                   // content codes of the group (c1: 4-bit only)
     uint32_t meta, rcode, rmeta;    // content {scale, zero}, RoPE codes, RoPE {scale, zero}
+                                    // (paper storage: meta = bf16 scale | zero << 16,
+                                    // rmeta = fp32 scale bits, rzero)
+    uint32_t rzero;
     f16x2 zz, ss, rz, rs;           // metadata as fp16 (zero + 1024, scale)
     uint32_t lo[2], hi[2];          // nibbles of the 4-bit code words of chunks j (index j & 1)
     uint32_t pr[4];                 // pairs in flight (index task & 3)
@@ -363,25 +390,35 @@ template <int KIND>
 __device__ __forceinline__ void dq_read(Dq<KIND>& d, const uint8_t* st, int tid) {
     using C = Cfg<KIND>;
     const int row = dq_row(tid), part = tid & 7;
-    if constexpr (KIND == KIND_C4R4) {
+    if constexpr (C::cc == 256) {
         d.c0 = *reinterpret_cast<const uint4*>(st + row * 256 + part * 32);
         d.c1 = *reinterpret_cast<const uint4*>(st + row * 256 + part * 32 + 16);
     } else {
         d.c0 = *reinterpret_cast<const uint4*>(st + row * 128 + part * 16);
         d.c1 = make_uint4(0u, 0u, 0u, 0u);
     }
-    d.meta = *reinterpret_cast<const uint32_t*>(st + C::meta + row * 32 + part * 4);
     d.rcode = *reinterpret_cast<const uint32_t*>(st + C::rcodes + row * 32 + part * 4);
-    d.rmeta = *reinterpret_cast<const uint32_t*>(st + C::rmeta + row * 4);
+    if constexpr (C::pmeta) {
+        const uint8_t* rec = st + C::meta + row * 32;
+        d.meta = static_cast<uint32_t>(*reinterpret_cast<const uint16_t*>(rec + 2 * part)) |
+                 (static_cast<uint32_t>(rec[16 + part]) << 16);
+        const uint2 r = *reinterpret_cast<const uint2*>(rec + 24);
+        d.rmeta = r.x;
+        d.rzero = r.y & 0xFFu;
+    } else {
+        d.meta = *reinterpret_cast<const uint32_t*>(st + C::meta + row * 32 + part * 4);
+        d.rmeta = *reinterpret_cast<const uint32_t*>(st + C::rmeta + row * 4);
+        d.rzero = 0;
+    }
 }
 
 // chunk j holds 4-bit codes (channel 2i in the low nibble of byte i)?
 template <int KIND>
-__device__ __forceinline__ constexpr bool dq_is4(int j) { return KIND == KIND_C4R4 || j == 8; }
+__device__ __forceinline__ constexpr bool dq_is4(int j) { return Cfg<KIND>::cc == 256 || j == 8; }
 
 template <int KIND>
 __device__ __forceinline__ uint32_t dq_word(const Dq<KIND>& d, int j) {
-    if constexpr (KIND == KIND_C4R4) {
+    if constexpr (Cfg<KIND>::cc == 256) {
         const uint32_t cw[9] = {d.c0.x, d.c0.y, d.c0.z, d.c0.w, d.c1.x, d.c1.y, d.c1.z, d.c1.w, d.rcode};
         return cw[j];
     } else {
@@ -403,8 +440,13 @@ __device__ __forceinline__ void dq_split(Dq<KIND>& d, int j) {
 template <int KIND>
 __device__ __forceinline__ void dq_step(Dq<KIND>& d, int s, uint8_t* tile, int tid) {
     if (s == 0) {
-        meta_to_f16(d.meta, d.zz, d.ss);
-        meta_to_f16(d.rmeta, d.rz, d.rs);
+        if constexpr (Cfg<KIND>::pmeta) {
+            pmeta_to_f16(__uint_as_float(d.meta << 16), d.meta >> 16, d.zz, d.ss);
+            pmeta_to_f16(__uint_as_float(d.rmeta), d.rzero, d.rz, d.rs);
+        } else {
+            meta_to_f16(d.meta, d.zz, d.ss);
+            meta_to_f16(d.rmeta, d.rz, d.rs);
+        }
     }
     if (s >= 3 && s - 3 < 36) {                 // D: scale; store a finished chunk
         const int t = s - 3, j = t >> 2, p = t & 3;
@@ -909,6 +951,8 @@ hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream
     switch (kind) {
         case KIND_C4R4: hipLaunchKernelGGL((decode_kernel<KIND_C4R4, false>), grid, block, 0, stream, a); break;
         case KIND_C2R4: hipLaunchKernelGGL((decode_kernel<KIND_C2R4, false>), grid, block, 0, stream, a); break;
+        case KIND_C4R4P: hipLaunchKernelGGL((decode_kernel<KIND_C4R4P, false>), grid, block, 0, stream, a); break;
+        case KIND_C2R4P: hipLaunchKernelGGL((decode_kernel<KIND_C2R4P, false>), grid, block, 0, stream, a); break;
         case KIND_BF16: hipLaunchKernelGGL((decode_kernel<KIND_BF16, false>), grid, block, 0, stream, a); break;
     }
     return hipGetLastError();
@@ -923,6 +967,8 @@ hipError_t launch_decode_protected(CacheKind kind, const DecodeArgs& a, hipStrea
     switch (kind) {
         case KIND_C4R4: hipLaunchKernelGGL((decode_kernel<KIND_C4R4, true>), grid, block, 0, stream, a); break;
         case KIND_C2R4: hipLaunchKernelGGL((decode_kernel<KIND_C2R4, true>), grid, block, 0, stream, a); break;
+        case KIND_C4R4P: hipLaunchKernelGGL((decode_kernel<KIND_C4R4P, true>), grid, block, 0, stream, a); break;
+        case KIND_C2R4P: hipLaunchKernelGGL((decode_kernel<KIND_C2R4P, true>), grid, block, 0, stream, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -16,8 +16,9 @@ struct PageGeom {
     int32_t cr_bytes;       // RoPE code bytes per token
     int32_t off_cr;         // region offsets inside a page
     int32_t off_mc;
-    int32_t off_mr;
+    int32_t off_mr;         // (fp16 metadata only)
     int64_t page_bytes;
+    int32_t paper_meta;     // 1: the paper's metadata record at off_mc
 };
 
 struct AppendArgs {
@@ -41,7 +42,8 @@ struct AppendArgs {
     int32_t sink, recent;
 };
 
-enum CacheKind { KIND_C4R4 = 0, KIND_C2R4 = 1, KIND_BF16 = 2 };
+// Low-bit kinds: content bits and metadata storage (P: the paper's record).
+enum CacheKind { KIND_C4R4 = 0, KIND_C2R4 = 1, KIND_BF16 = 2, KIND_C4R4P = 3, KIND_C2R4P = 4 };
 
 struct DecodeArgs {
     const uint16_t* q_lat;

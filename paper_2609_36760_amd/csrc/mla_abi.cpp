@@ -20,6 +20,7 @@ constexpr int32_t kGroup = 64;
 constexpr int32_t kTile = 32;
 
 constexpr int32_t kMaxProtRows = 65536;
+constexpr int32_t kPaperMetaBytes = 32;
 constexpr int64_t kProtRowBytes = (kDc + kDr) * 2;
 
 bool aligned(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
@@ -67,6 +68,7 @@ int check_lowbit_format(const mla_cache_format* f) {
     if (f->group <= 0 || f->d_c % f->group != 0 || f->d_r % f->group != 0) return MLA_EINVAL;
     if (f->c_bits != 4 && f->c_bits != 2) return MLA_EINVAL;
     if (f->r_bits != 4) return MLA_EINVAL;
+    if (f->meta != MLA_META_FP16 && f->meta != MLA_META_PAPER) return MLA_EINVAL;
     if (f->group != kGroup) return MLA_ENOTSUP;
     return MLA_OK;
 }
@@ -80,8 +82,16 @@ mla::PageGeom lowbit_geom(const mla_cache_format* f) {
     g.cr_bytes = f->d_r * f->r_bits / 8;
     g.off_cr = P * g.cc_bytes;
     g.off_mc = g.off_cr + P * g.cr_bytes;
-    g.off_mr = g.off_mc + P * (f->d_c / f->group) * 4;
-    const int64_t end = g.off_mr + static_cast<int64_t>(P) * (f->d_r / f->group) * 4;
+    int64_t end;
+    if (f->meta == MLA_META_PAPER) {
+        // one 32-byte record per token: bf16 scales, byte zeros, fp32 RoPE scale, byte RoPE zero
+        g.paper_meta = 1;
+        g.off_mr = g.off_mc;
+        end = g.off_mc + static_cast<int64_t>(P) * kPaperMetaBytes;
+    } else {
+        g.off_mr = g.off_mc + P * (f->d_c / f->group) * 4;
+        end = g.off_mr + static_cast<int64_t>(P) * (f->d_r / f->group) * 4;
+    }
     g.page_bytes = (end + 255) / 256 * 256;
     return g;
 }
@@ -190,7 +200,10 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
     a.part_s = part_s;
     a.part_o = part_o;
     a.g = lowbit ? lowbit_geom(f) : bf16_geom(f);
-    const mla::CacheKind kind = !lowbit ? mla::KIND_BF16 : (f->c_bits == 4 ? mla::KIND_C4R4 : mla::KIND_C2R4);
+    const bool paper = f->meta == MLA_META_PAPER;
+    const mla::CacheKind kind = !lowbit ? mla::KIND_BF16
+                                : f->c_bits == 4 ? (paper ? mla::KIND_C4R4P : mla::KIND_C4R4)
+                                                 : (paper ? mla::KIND_C2R4P : mla::KIND_C2R4);
     if (pd == nullptr) return hip_status(mla::launch_decode(kind, a, stream));
     a.prot = static_cast<const uint8_t*>(pd->prot);
     a.num_prot = pd->num_prot;

@@ -11,6 +11,12 @@
 // -ffp-contract=off and correctly rounded fp32 division, so the codes and
 // fp16 metadata are bit-identical to any IEEE implementation of the formula.
 //
+// Metadata: fp16(s) and fp16(z) per group (MLA_META_FP16); or the paper's
+// storage (Appendix C.4, last sentence): bf16(s) (round-half-to-even) for the
+// content groups and s itself (fp32) for the RoPE group, z as a byte, in one
+// 32-byte record per token (layout in mla_lowbit.h).  The codes come from
+// the unrounded fp32 s in both.
+//
 // Work split: 8 lanes per group of 64 channels, each lane owning 8 channels
 // (one 16-byte load); min/max are reduced across the 8 lanes.  A token has 9
 // groups: 8 content groups (d_c = 512) and one RoPE-key group (d_r = 64).
@@ -47,7 +53,7 @@ __device__ inline uint16_t f16_bits(float v) {
     return __builtin_bit_cast(uint16_t, h);
 }
 
-template <int CBITS, bool kProt>
+template <int CBITS, bool kProt, bool kPaper>
 __global__ __launch_bounds__(kThreads) void lowbit_append_kernel(AppendArgs a) {
     const int64_t tid = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
     const int64_t gid = tid / kLanesPerGroup;           // the 8 lanes of a group share gid
@@ -119,9 +125,22 @@ __global__ __launch_bounds__(kThreads) void lowbit_append_kernel(AppendArgs a) {
             static_cast<uint16_t>(packed);
     }
     if (lig == 0) {
-        const uint32_t meta = static_cast<uint32_t>(f16_bits(s)) | (static_cast<uint32_t>(f16_bits(z)) << 16);
-        uint8_t* mp = rope ? base + a.g.off_mr + off * 4 : base + a.g.off_mc + off * 32 + g * 4;
-        *reinterpret_cast<uint32_t*>(mp) = meta;
+        if constexpr (kPaper) {
+            uint8_t* rec = base + a.g.off_mc + off * 32;
+            const uint32_t zb = static_cast<uint32_t>(z);
+            if (rope) {
+                // fp32 scale, byte zero-point, three zero bytes
+                *reinterpret_cast<uint2*>(rec + 24) = make_uint2(__float_as_uint(s), zb);
+            } else {
+                const __bf16 sb = static_cast<__bf16>(s);     // round-half-to-even
+                *reinterpret_cast<uint16_t*>(rec + 2 * g) = __builtin_bit_cast(uint16_t, sb);
+                rec[16 + g] = static_cast<uint8_t>(zb);
+            }
+        } else {
+            const uint32_t meta = static_cast<uint32_t>(f16_bits(s)) | (static_cast<uint32_t>(f16_bits(z)) << 16);
+            uint8_t* mp = rope ? base + a.g.off_mr + off * 4 : base + a.g.off_mc + off * 32 + g * 4;
+            *reinterpret_cast<uint32_t*>(mp) = meta;
+        }
     }
 }
 
@@ -145,26 +164,30 @@ __global__ __launch_bounds__(kThreads) void bf16_append_kernel(AppendArgs a) {
 
 }  // namespace
 
-hipError_t launch_lowbit_append(const AppendArgs& a, hipStream_t stream) {
+namespace {
+
+template <bool kProt>
+hipError_t launch_append(const AppendArgs& a, hipStream_t stream) {
     if (a.n == 0) return hipSuccess;
     const int64_t threads = static_cast<int64_t>(a.n) * kGroupsPerToken * kLanesPerGroup;
     const dim3 grid(static_cast<unsigned>((threads + kThreads - 1) / kThreads));
-    if (a.g.c_bits == 4)
-        hipLaunchKernelGGL((lowbit_append_kernel<4, false>), grid, dim3(kThreads), 0, stream, a);
-    else
-        hipLaunchKernelGGL((lowbit_append_kernel<2, false>), grid, dim3(kThreads), 0, stream, a);
+    const bool paper = a.g.paper_meta != 0;
+    if (a.g.c_bits == 4) {
+        if (paper) hipLaunchKernelGGL((lowbit_append_kernel<4, kProt, true>), grid, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL((lowbit_append_kernel<4, kProt, false>), grid, dim3(kThreads), 0, stream, a);
+    } else {
+        if (paper) hipLaunchKernelGGL((lowbit_append_kernel<2, kProt, true>), grid, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL((lowbit_append_kernel<2, kProt, false>), grid, dim3(kThreads), 0, stream, a);
+    }
     return hipGetLastError();
 }
 
+}  // namespace
+
+hipError_t launch_lowbit_append(const AppendArgs& a, hipStream_t stream) { return launch_append<false>(a, stream); }
+
 hipError_t launch_lowbit_append_protected(const AppendArgs& a, hipStream_t stream) {
-    if (a.n == 0) return hipSuccess;
-    const int64_t threads = static_cast<int64_t>(a.n) * kGroupsPerToken * kLanesPerGroup;
-    const dim3 grid(static_cast<unsigned>((threads + kThreads - 1) / kThreads));
-    if (a.g.c_bits == 4)
-        hipLaunchKernelGGL((lowbit_append_kernel<4, true>), grid, dim3(kThreads), 0, stream, a);
-    else
-        hipLaunchKernelGGL((lowbit_append_kernel<2, true>), grid, dim3(kThreads), 0, stream, a);
-    return hipGetLastError();
+    return launch_append<true>(a, stream);
 }
 
 hipError_t launch_bf16_append(const AppendArgs& a, hipStream_t stream) {

@@ -26,10 +26,11 @@ def _dev(a, device):
 class DecodeRun:
     def __init__(self, w: syn.Workload, layer: int = 0, kind: str = "lowbit", device: str = "cuda",
                  split_tokens: int | None = None, seq_lens=None, threads: int = 16, prefill: bool = True,
-                 token_cache: dict | None = None, protect=None, prot_slots=None):
+                 token_cache: dict | None = None, protect=None, prot_slots=None, meta: str = "fp16"):
         """``protect``: an ``mla_protect_policy`` to keep sink/recent tokens in
         bf16 (low-bit caches only); ``prot_slots``: the protection buffer of
-        each sequence (default: buffer b for sequence b)."""
+        each sequence (default: buffer b for sequence b); ``meta``: "fp16"
+        (fp16 scale and zero) or "paper" (the paper's bf16 / fp32 scales)."""
         if kind not in ("lowbit", "bf16"):
             raise ValueError(kind)
         if protect is not None and kind != "lowbit":
@@ -37,7 +38,11 @@ class DecodeRun:
         self.protect = protect
         self.w, self.layer, self.kind, self.device = w, layer, kind, device
         self.c_bits, self.r_bits = w.layers[layer]
-        self.fmt = mb.cache_format(c_bits=self.c_bits)
+        if meta not in ("fp16", "paper"):
+            raise ValueError(meta)
+        self.meta = meta
+        self.fmt = mb.cache_format(c_bits=self.c_bits,
+                                   meta=mb.MLA_META_PAPER if meta == "paper" else mb.MLA_META_FP16)
         self.B, self.H, self.s_q = w.B, w.H, w.s_q
         self.tau = w.tau
         lens = syn.seq_lens(w) if seq_lens is None else np.asarray(seq_lens, np.int32)
@@ -193,7 +198,7 @@ class DecodeRun:
     def cache_token_bytes(self) -> int:
         if self.kind == "bf16":
             return 1152
-        return (512 * self.c_bits + 64 * self.r_bits) // 8 + 9 * 4
+        return (512 * self.c_bits + 64 * self.r_bits) // 8 + (32 if self.meta == "paper" else 9 * 4)
 
     def key_bytes(self) -> int:
         """Bytes of every cached key once (under protection, the

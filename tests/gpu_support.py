@@ -50,13 +50,13 @@ def bf16_bits_to_f64(t) -> np.ndarray:
     return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
 
 
-def reconstructed_sequence(w, layer, b, L, kind):
+def reconstructed_sequence(w, layer, b, L, kind, meta="fp16"):
     """Oracle reconstruction of sequence b's cache (fp32 [L, 512], [L, 64])."""
     c_bits, r_bits = w.layers[layer]
     c, k = syn.sequence_tokens(w, layer, b, L)
     if kind == "bf16":
         return qz.bf16_bits_to_f32(c), qz.bf16_bits_to_f32(k)
-    return pc.encode_sequence_dense(pc.CacheFormat(c_bits=c_bits, r_bits=r_bits), c, k)
+    return pc.encode_sequence_dense(pc.CacheFormat(c_bits=c_bits, r_bits=r_bits, meta=meta), c, k)
 
 
 def lse_bound(q_lat_bits, q_rope_bits, c_hat, kr_hat, tau, L, s_q):
@@ -133,7 +133,7 @@ class AttnStats:
 def check_sequence(stats, run, b, heads=None):
     """Compare rows of sequence b of a finished DecodeRun with the oracle."""
     w, L = run.w, int(run.lens[b])
-    c_hat, kr_hat = reconstructed_sequence(w, run.layer, b, L, run.kind)
+    c_hat, kr_hat = reconstructed_sequence(w, run.layer, b, L, run.kind, run.meta)
     ql, qr = syn.queries(w, run.layer, batch=[b])
     hs = np.arange(w.H) if heads is None else np.asarray(heads)
     want_out, want_lse = at.decode_sequence(ql[0], qr[0], c_hat, kr_hat, w.tau, heads=hs)
@@ -150,7 +150,7 @@ def check_sequence_protected(stats, run, b, heads=None):
     w, L = run.w, int(run.lens[b])
     c_bits, r_bits = w.layers[run.layer]
     c, k = syn.sequence_tokens(w, run.layer, b, L)
-    c_rep, k_rep = pr.representation(pc.CacheFormat(c_bits=c_bits, r_bits=r_bits), c, k,
+    c_rep, k_rep = pr.representation(pc.CacheFormat(c_bits=c_bits, r_bits=r_bits, meta=run.meta), c, k,
                                      run.protect.sink, run.protect.recent)
     ql, qr = syn.queries(w, run.layer, batch=[b])
     hs = np.arange(w.H) if heads is None else np.asarray(heads)

@@ -47,6 +47,12 @@ def test_page_geometry(mb):
     assert mb.mla_lowbit_page_bytes(mb.cache_format(c_bits=3)) == -1
     assert mb.mla_lowbit_page_bytes(mb.cache_format(page_size=48)) == -1
     assert mb.mla_bf16_page_bytes(mb.cache_format(d_c=256)) == -1
+    # the paper's metadata: 320 B per token, 20480 B per 64-token page
+    assert mb.mla_lowbit_page_bytes(mb.cache_format(c_bits=4, meta=mb.MLA_META_PAPER)) == 20480
+    assert mb.mla_lowbit_page_bytes(mb.cache_format(c_bits=2, meta=mb.MLA_META_PAPER)) == 12288
+    assert mb.mla_lowbit_page_bytes(mb.cache_format(c_bits=4, page_size=32, meta=mb.MLA_META_PAPER)) == 10240
+    assert mb.mla_lowbit_page_bytes(mb.cache_format(meta=2)) == -1
+    assert mb.mla_bf16_page_bytes(mb.cache_format(meta=2)) == 73728      # the BF16 cache ignores it
 
 
 def test_planner(mb):
@@ -80,14 +86,14 @@ def _decode_status(mb, **over):
     (dict(cache=272), 1), (dict(q_lat=8), 2), (dict(scale=float("inf")), 1), (dict(scale=0.0), 1), (dict(scale=-0.1), 1),
     (dict(split_tokens=64, split_indptr=16, part_m=16, part_s=16, part_o=None), 1),
     (dict(split_tokens=48, split_indptr=16, part_m=16, part_s=16, part_o=16), 2),
-    (dict(fmt="c3"), 1), (dict(fmt="r2"), 1), (dict(fmt="g32"), 2), (dict(fmt="p48"), 2), (dict(fmt="p40"), 1), (dict(fmt="dc256"), 2),
+    (dict(fmt="c3"), 1), (dict(fmt="r2"), 1), (dict(fmt="m2"), 1), (dict(fmt="g32"), 2), (dict(fmt="p48"), 2), (dict(fmt="p40"), 1), (dict(fmt="dc256"), 2),
     (dict(B=0), 0), (dict(B=0, q_lat=None, cache=None, out=None), 0), (dict(B=0, s_q=3), 1),
 ])
 def test_decode_rejects_before_any_hip_call(mb, over, status):
     fmts = {"c3": mb.cache_format(c_bits=3), "r2": mb.cache_format(r_bits=2),
             "g32": mb.cache_format(group=32), "p48": mb.cache_format(page_size=48),
             "p40": mb.cache_format(page_size=40),
-            "dc256": mb.cache_format(d_c=256)}
+            "dc256": mb.cache_format(d_c=256), "m2": mb.cache_format(meta=2)}
     if "fmt" in over:
         over = dict(over, fmt=fmts[over["fmt"]])
     assert _decode_status(mb, **over) == status

@@ -1,7 +1,8 @@
 """GPU parity of the writers: packed codes and fp16 metadata bit-exact.
 
 The GPU quantize-append must produce the same cache bytes as the oracle's
-quantizer and page layout (Appendix C.4; Appendix C.5) for every token: the
+quantizer and page layout (Appendix C.4; Appendix C.5), with fp16 metadata
+and with the paper's bf16 / fp32 scales, for every token: the
 hand-derived cases, random tokens with outlier channels over 12 decades of
 scale, constant groups, fp16-subnormal scales, signed zeros, skipped slots.
 Bytes the writer must not touch are checked too (both caches start from the
@@ -70,21 +71,23 @@ def _tokens(c_bits, rng):
     return _bits(C), _bits(R)
 
 
+@pytest.mark.parametrize("meta", ["fp16", "paper"])
 @pytest.mark.parametrize("c_bits", [4, 2])
-def test_quant_append_bit_exact(c_bits):
+def test_quant_append_bit_exact(c_bits, meta):
     import torch
 
     from paper_2609_36760_amd import _binding as mb
     rng = np.random.default_rng(100 + c_bits)
     cb, rb = _tokens(c_bits, rng)
     n = cb.shape[0]
-    fmt = pc.CacheFormat(c_bits=c_bits)
+    fmt = pc.CacheFormat(c_bits=c_bits, meta=meta)
+    mfmt = mb.cache_format(c_bits=c_bits, meta=mb.MLA_META_PAPER if meta == "paper" else mb.MLA_META_FP16)
     num_pages = (n + 40) // 64 + 3
     num_slots = num_pages * 64
     slots = rng.permutation(num_slots)[:n].astype(np.int64)
     slots[5] = -1                       # skipped
     slots[17] = num_slots + 7           # beyond the cache: skipped
-    assert fmt.page_bytes == mb.mla_lowbit_page_bytes(mb.cache_format(c_bits=c_bits))
+    assert fmt.page_bytes == mb.mla_lowbit_page_bytes(mfmt)
     want = np.full(num_pages * fmt.page_bytes, 0x5A, np.uint8)
     keep = slots.copy()
     keep[keep >= num_slots] = -1
@@ -92,7 +95,7 @@ def test_quant_append_bit_exact(c_bits):
 
     dev = "cuda"
     cache = torch.full((num_pages * fmt.page_bytes,), 0x5A, dtype=torch.uint8, device=dev)
-    mb.mla_lowbit_quant_append(mb.cache_format(c_bits=c_bits), torch.from_numpy(cb.view(np.int16)).to(dev),
+    mb.mla_lowbit_quant_append(mfmt, torch.from_numpy(cb.view(np.int16)).to(dev),
                                torch.from_numpy(rb.view(np.int16)).to(dev), torch.from_numpy(slots).to(dev),
                                cache, num_pages)
     got = cache.cpu().numpy()
