@@ -310,6 +310,20 @@ int mla_lowbit_decode_attn_protected(const mla_cache_format* f, const mla_protec
                                      float* part_m, float* part_s, float* part_o,
                                      hipStream_t stream);
 
+/*
+ * Per-layer persistent cache bytes of one request of L tokens
+ * (Appendix C.5, eq. physical_cache_storage):
+ *   ceil(L / page_size) * (page bytes + 8) + protection buffer bytes
+ * with this library's page geometry for `f`, the 8-byte reverse page mapping
+ * a paging allocator keeps per physical page (counted by the equation, not
+ * allocated by this library), and the protection buffer of `p` (NULL: no
+ * protection).  With MLA_META_PAPER, c_bits = 4 and the paper's policy this is
+ * the paper's M_C4R4(L); for a BF16 format (c_bits = 16) it returns the
+ * equation's M_BF16(L) = ceil(L / page_size) * mla_bf16_page_bytes.
+ * Returns -1 for an invalid format, policy or L < 0.
+ */
+int64_t mla_persistent_cache_bytes(const mla_cache_format* f, const mla_protect_policy* p, int64_t L);
+
 /* Human-readable name of a status code (static string). */
 const char* mla_status_str(int status);
 

@@ -22,7 +22,7 @@ SYMBOLS = (
     "mla_lowbit_page_bytes", "mla_bf16_page_bytes", "mla_lowbit_quant_append", "mla_bf16_append",
     "mla_plan_splits", "mla_lowbit_decode_attn", "mla_bf16_decode_attn", "mla_splitkv_combine",
     "mla_status_str", "mla_last_hip_error", "mla_protect_buffer_bytes", "mla_lowbit_quant_append_protected",
-    "mla_plan_splits_protected", "mla_lowbit_decode_attn_protected",
+    "mla_plan_splits_protected", "mla_lowbit_decode_attn_protected", "mla_persistent_cache_bytes",
 )
 
 
@@ -84,6 +84,7 @@ def library() -> ctypes.CDLL:
                                                 I32, P, I32, P, P, P, P, P, P]),
         "mla_splitkv_combine": (ctypes.c_int, [P, P, P, P, I32, I32, I32, I32, P, P, P]),
         "mla_protect_buffer_bytes": (I64, [FMT, POL]),
+        "mla_persistent_cache_bytes": (I64, [FMT, POL, I64]),
         "mla_lowbit_quant_append_protected": (ctypes.c_int, [FMT, POL, P, I64, P, I64, P, I32, P, I64,
                                                              P, P, P, P, I32, P, I64, P]),
         "mla_plan_splits_protected": (I32, [P, I32, I32, POL, P]),
@@ -224,3 +225,10 @@ def mla_lowbit_decode_attn_protected(fmt, policy, q_lat, q_rope, cache, num_page
         _ptr(block_table), block_table.shape[1], _ptr(seq_lens), B, s_q, H, float(softmax_scale),
         _ptr(prot), num_prot, _ptr(prot_slot), split_tokens, _ptr(split_indptr), num_splits,
         _ptr(out), _ptr(lse), _ptr(part_m), _ptr(part_s), _ptr(part_o), _stream(stream)))
+
+
+def mla_persistent_cache_bytes(fmt: mla_cache_format, policy, L: int) -> int:
+    """eq. physical_cache_storage for one request of ``L`` tokens (``policy``
+    None: no protection)."""
+    return library().mla_persistent_cache_bytes(ctypes.byref(fmt), None if policy is None else ctypes.byref(policy),
+                                                int(L))

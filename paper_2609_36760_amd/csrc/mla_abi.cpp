@@ -21,6 +21,7 @@ constexpr int32_t kTile = 32;
 
 constexpr int32_t kMaxProtRows = 65536;
 constexpr int32_t kPaperMetaBytes = 32;
+constexpr int64_t kReverseMapBytes = 8;     // per physical page, eq. physical_cache_storage
 constexpr int64_t kProtRowBytes = (kDc + kDr) * 2;
 
 bool aligned(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
@@ -239,6 +240,19 @@ int mla_bf16_append(const mla_cache_format* f, const uint16_t* c_kv, int64_t c_k
                     void* cache, int64_t num_pages, hipStream_t stream) {
     return append_common(f, false, c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, n, cache, num_pages,
                          stream);
+}
+
+int64_t mla_persistent_cache_bytes(const mla_cache_format* f, const mla_protect_policy* p, int64_t L) {
+    if (f == nullptr || L < 0) return -1;
+    if (f->c_bits == 16) {
+        if (check_shape(f) != MLA_OK || p != nullptr) return -1;
+        return (L + f->page_size - 1) / f->page_size * bf16_geom(f).page_bytes;
+    }
+    if (check_lowbit_format(f) != MLA_OK) return -1;
+    if (p != nullptr && check_policy(p) != MLA_OK) return -1;
+    const int64_t pages = (L + f->page_size - 1) / f->page_size;
+    const int64_t prot = p == nullptr ? 0 : (static_cast<int64_t>(p->sink) + p->recent) * kProtRowBytes;
+    return pages * (lowbit_geom(f).page_bytes + kReverseMapBytes) + prot;
 }
 
 int64_t mla_protect_buffer_bytes(const mla_cache_format* f, const mla_protect_policy* p) {

@@ -32,7 +32,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(mb):
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 15
     lib = ctypes.CDLL(mb.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -188,3 +188,22 @@ def test_protected_entry_points_reject_before_any_hip_call(mb):
     assert lib.mla_lowbit_quant_append_protected(f, p, None, 512, None, 64, None, 0, None, 0, None, None, None,
                                                  None, 0, None, 0, None) == 0
     assert lib.mla_last_hip_error() == 0
+
+
+def test_persistent_cache_bytes_reproduce_the_printed_ratios(mb):
+    """eq. physical_cache_storage: 3.22x at 4K and 3.59x at 128K for the paper's
+    storage (20480 + 8 B per page, 152064 B of protection) against BF16."""
+    paper = mb.cache_format(c_bits=4, meta=mb.MLA_META_PAPER)
+    bf16 = mb.cache_format(c_bits=16)
+    pol = mb.protect_policy()
+    assert mb.mla_persistent_cache_bytes(paper, pol, 64) == 20488 + 152064
+    assert mb.mla_persistent_cache_bytes(paper, pol, 65) == 2 * 20488 + 152064
+    assert mb.mla_persistent_cache_bytes(paper, None, 0) == 0
+    for L, ratio in ((4096, 3.22), (131072, 3.59)):
+        r = mb.mla_persistent_cache_bytes(bf16, None, L) / mb.mla_persistent_cache_bytes(paper, pol, L)
+        assert round(r, 2) == ratio
+    # the fp16-metadata layout: 20736 B pages
+    assert mb.mla_persistent_cache_bytes(mb.cache_format(), None, 4096) == 64 * (20736 + 8)
+    assert mb.mla_persistent_cache_bytes(paper, pol, -1) == -1
+    assert mb.mla_persistent_cache_bytes(bf16, pol, 10) == -1
+    assert mb.mla_persistent_cache_bytes(mb.cache_format(c_bits=3), None, 10) == -1
