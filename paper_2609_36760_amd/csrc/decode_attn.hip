@@ -72,18 +72,13 @@
 #include <type_traits>
 
 #include "internal.h"
+#include "kernel_common.h"
 
 namespace mla {
 namespace {
 
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) void lds_void;
-typedef const __attribute__((address_space(1))) void gbl_void;
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+using namespace kc;
+
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
@@ -131,7 +126,6 @@ template <> struct Cfg<KIND_C2R4P> : Cfg<KIND_C2R4> {
 };
 template <> struct Cfg<KIND_BF16> {
     static constexpr bool lowbit = false;
-    static constexpr bool pmeta = false;
     static constexpr int stage_bytes = 0;
     static constexpr int NT = 4, NS = 0, D = 2, loads = 10;   // 2432 chunks: 9 rounds of 256 + 128
     static constexpr int SC = 76;
@@ -161,21 +155,6 @@ static_assert(lds_bytes<KIND_C4R4>() <= 160 * 1024, "LDS budget of a gfx950 CU")
 static_assert(lds_bytes<KIND_C4R4P>() == lds_bytes<KIND_C4R4>(), "same staging for both metadata layouts");
 static_assert(lds_bytes<KIND_BF16>() <= 160 * 1024, "LDS budget of a gfx950 CU");
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    const bf16x2 v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};   // RNE
-    return __builtin_bit_cast(uint32_t, v);
-}
-
-__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
-    const f16x2 v = {static_cast<_Float16>(lo), static_cast<_Float16>(hi)}; // v_cvt_pk_f16_f32, RNE
-    return __builtin_bit_cast(uint32_t, v);
-}
-
-__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
-    return pack_f16x2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
-}
-
 // max / sum of a value and its copy in lane ^ 32 (v_permlane32_swap hands each
 // lane the pair {own value, partner's value} in its two results)
 __device__ __forceinline__ float max_halves(float v) {
@@ -185,15 +164,6 @@ __device__ __forceinline__ float max_halves(float v) {
 __device__ __forceinline__ float sum_halves(float v) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-// Byte offset of buffer (j mod n) of `bytes` bytes, as an opaque scalar: the
-// compiler then forms every LDS address as one per-lane base plus this offset
-// plus an immediate, instead of keeping a per-lane address for every buffer.
-__device__ __forceinline__ int slot_offset(int j, int n, int bytes) {
-    int off = (j % n) * bytes;
-    asm volatile("" : "+s"(off));
-    return off;
 }
 
 __device__ __forceinline__ f32x16 mfma(f16x8 a, f16x8 b, f32x16 c) {
@@ -217,30 +187,8 @@ __device__ __forceinline__ void scale_acc(f32x16& acc, float alpha) {
 }
 
 // ---------------------------------------------------------------------------
-// 1. HBM -> LDS staging.
+// 1. HBM -> LDS staging (direct-to-LDS loads: dma16 in kernel_common.h).
 //
-// Direct-to-LDS load of 16 bytes per lane: lane l copies base + voff into LDS
-// bytes [lds + 16 l, lds + 16 l + 16) (base and lds wave-uniform).  Written as
-// inline assembly so that the compiler does not track it: it would otherwise
-// wait for every such load in flight before any LDS read of the same array.
-// Every read of staged data instead follows an explicit counted wait and a
-// barrier (step_barrier).  M0 is saved and restored around the load.
-__device__ __forceinline__ void dma16(const uint8_t* base, uint32_t voff, uint32_t lds) {
-    uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\t"
-        "global_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
-        : "=&s"(saved)
-        : "v"(voff), "s"(base), "s"(lds)
-        : "memory");
-}
-
-// 32-bit LDS address of a pointer into shared memory (uniform).
-__device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
-    return __builtin_amdgcn_readfirstlane(
-        static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint8_t*)p)));
-}
-
 // Wait until at most N direct-to-LDS loads of this wave are in flight and all
 // of its LDS accesses are done, then synchronize the workgroup.  Also fetches
 // a page-table entry through the scalar cache (one cache line holds the ids
@@ -262,16 +210,6 @@ template <int N>
 __device__ __forceinline__ void plain_barrier() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(N) : "memory");
-}
-
-// The same entry, waited for on the spot.
-__device__ __forceinline__ int load_page_id(const int32_t* table, int index) {
-    int v;
-    asm volatile("s_load_dword %0, %1, %2\n\ts_waitcnt lgkmcnt(0)"
-                 : "=&s"(v)
-                 : "s"(table), "s"(__builtin_amdgcn_readfirstlane(index * 4))
-                 : "memory");
-    return v;
 }
 
 // Packed tile: the content codes in whole rounds (chunk i of the region by
@@ -334,29 +272,9 @@ __device__ __forceinline__ void stage_bf16(int k, const uint8_t* src, RowStart r
 }
 
 // ---------------------------------------------------------------------------
-// 2. Dequantization of a staged tile into the fp16 tile.
+// 2. Dequantization of a staged tile into the fp16 tile (metadata as fp16
+// pairs: meta_to_f16 / pmeta_to_f16 in kernel_common.h).
 //
-// Codes become fp16 values 1024 + q (the fp16 with bits 0x6400 | q, exact);
-// (1024 + q) - (1024 + zero) = q - zero exactly, and one fp16 multiply by the
-// stored scale rounds s * (q - zero) once.  Both in packed fp16 (2 per op).
-// The paper's storage: scale (bf16 bits, or fp32 for the RoPE group) and a
-// byte zero-point.  The bf16 scale converts to fp16 exactly inside the fp16
-// range; the fp32 RoPE scale is rounded to fp16 once.
-__device__ __forceinline__ void pmeta_to_f16(float scale, uint32_t zero, f16x2& zz, f16x2& ss) {
-    const _Float16 s = static_cast<_Float16>(scale);
-    const _Float16 zb = static_cast<_Float16>(static_cast<float>(zero) + 1024.0f);   // exact
-    zz = f16x2{zb, zb};
-    ss = f16x2{s, s};
-}
-
-__device__ __forceinline__ void meta_to_f16(uint32_t meta, f16x2& zz, f16x2& ss) {
-    const _Float16 s = __builtin_bit_cast(_Float16, static_cast<uint16_t>(meta & 0xFFFFu));
-    const _Float16 z = __builtin_bit_cast(_Float16, static_cast<uint16_t>(meta >> 16));
-    const _Float16 zb = z + static_cast<_Float16>(1024.0f);    // exact: z is an integer in [0, 15]
-    zz = f16x2{zb, zb};
-    ss = f16x2{s, s};
-}
-
 // Thread t dequantizes part (t & 7) -- one content group of 64 channels (8
 // chunks) plus one RoPE chunk of 8 channels -- of tile row dq_row(t); the
 // eight threads of a row and the row two further on share a 16-lane store

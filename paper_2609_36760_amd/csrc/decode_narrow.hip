@@ -1,0 +1,524 @@
+// Decode attention for few query rows per sequence (16 per workgroup), the
+// regime of 16 heads and one query token (Appendix F.1, "Native Attention"),
+// where the 128-row kernel of decode_attn.hip would leave 7/8 of every matrix
+// instruction idle.  Same computation and results contract: absorbed MLA
+// scores z_t = tau (q_lat . C_hat_t + q_rope . K_hat_t), softmax, latent
+// aggregation O = A C_hat (Sec. 2.1, eq. mla_compact), split partials as in
+// Appendix C.5 "Global attention normalization", BF16 protection of sink and
+// recent tokens as in Appendix C.5 "BF16 protection and cache lifecycle".
+//
+// Workgroup = one wave (64 lanes), several per CU; no workgroup barriers.
+// It owns one (sequence or key split, block of 16 query rows).  Lane l works
+// on query row l % 16 and lane group g = l / 16.
+//
+// Per 16-token tile (low-bit cache):
+//   1. the packed bytes are copied HBM -> LDS by direct-to-LDS loads two tiles
+//      ahead, gathered chunk-major (16-byte chunk j of token m at chunk slot
+//      16 j + m) so that the per-lane code reads below are bank-conflict-free;
+//   2. scores S^T[token][row] = K_tile . Q^T with v_mfma_f32_16x16x32_f16: the
+//      A operand of k-step kk is token l % 16, channels 32 kk + 8 g .. +8 --
+//      one 32-bit word of 4-bit codes, dequantized in registers (x_hat =
+//      scale * (q - zero), one fp16 rounding); the dequantized content
+//      channels are also stored to an fp16 tile in LDS;
+//   3. softmax: a lane holds tokens 4 g .. 4 g + 3 of its row; maxima and sums
+//      combine the four lane groups with v_permlane16/32_swap;
+//   4. aggregation O^T[channel][row] += V^T . P^T with v_mfma_f32_16x16x16_f16
+//      (32 channel blocks, K = the 16 tokens): V^T read transposed from the
+//      fp16 tile with ds_read_b64_tr_b16, P^T straight from the score
+//      registers (the lane's four tokens are the B operand's K slice).
+// BF16 rows (the BF16 cache, and protected rows from a protection buffer)
+// are staged raw into a padded tile and feed both products directly.
+//
+// Online softmax as in decode_attn.hip: a per-row reference (log2 units) that
+// moves only when a tile exceeds it by more than 2^10, the accumulators
+// rescaled on the move; the true maximum is tracked for the split partials.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <type_traits>
+
+#include "internal.h"
+#include "kernel_common.h"
+
+namespace mla {
+namespace {
+
+using namespace kc;
+
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kRows = 16;           // query rows per workgroup
+constexpr int kTok = 16;            // tokens per tile
+constexpr int kQSteps = 18;         // 576 channels / 32 per k-step
+constexpr int kDc = 512;
+constexpr float kRefSlack = 10.0f;
+constexpr float kLn2 = 0.693147180559945309f;
+
+// LDS tiles, in 16-byte units.  Row r of the fp16 content tile starts at unit
+// 66 r + r / 8, row r of a raw bf16 tile at 74 r + r / 8: the dequantization
+// stores and score reads (16 rows, one chunk each) and the transposing reads
+// (8 rows, two chunks each, per half wave) then fall on distinct banks.
+__host__ __device__ constexpr int f16_row(int r) { return 66 * r + (r >> 3); }
+__host__ __device__ constexpr int bf_row(int r) { return 74 * r + (r >> 3); }
+constexpr int kF16TileBytes = 16 * (f16_row(15) + 64);
+constexpr int kBfUnits = (bf_row(15) + 72 + 63) / 64 * 64;
+constexpr int kBfTileBytes = 16 * kBfUnits;
+constexpr int kBfLoads = kBfUnits / 64;
+static_assert(kBfLoads == 19, "bf16 tile staging loads");
+
+// Narrow configuration per cache kind.  Low-bit staging slot (units): content
+// codes chunk-major [cc/16 chunks][16 tokens], RoPE codes [2][16], metadata
+// [2][16] (fp16 content pairs, or the paper's 32-byte record), and for fp16
+// metadata the RoPE pairs token-major (4 units).
+template <int KIND> struct NCfg {
+    static constexpr bool lowbit = true;
+    static constexpr bool pmeta = KIND == KIND_C4R4P || KIND == KIND_C2R4P;
+    static constexpr int cbits = (KIND == KIND_C4R4 || KIND == KIND_C4R4P) ? 4 : 2;
+    static constexpr int cc = 512 * cbits / 8;            // content code bytes per token
+    static constexpr int u_rc = cc, u_mc = cc + 32, u_mr = cc + 64;
+    static constexpr int units = u_mr + (pmeta ? 0 : 4);
+    static constexpr int loads = (units + 63) / 64;
+    static constexpr int stage_bytes = 16 * units;
+    static constexpr int NS = 3, D = 2;                   // staging slots, tiles ahead
+    static constexpr int lds = NS * stage_bytes + kF16TileBytes;
+};
+template <> struct NCfg<KIND_BF16> {
+    static constexpr bool lowbit = false;
+    static constexpr int loads = kBfLoads;
+    static constexpr int NS = 2, D = 1;                   // tile slots, tiles ahead
+    static constexpr int lds = NS * kBfTileBytes;
+};
+
+template <int KIND>
+constexpr int narrow_lds(bool prot) {
+    return prot && NCfg<KIND_BF16>::lds > NCfg<KIND>::lds ? NCfg<KIND_BF16>::lds : NCfg<KIND>::lds;
+}
+
+template <int N>
+__device__ __forceinline__ void wait_loads() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" : : "n"(N) : "memory");
+}
+
+// value and its copies in lanes ^16, ^32, ^48 combined
+__device__ __forceinline__ float max4(float v) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum4(float v) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ void scale_acc4(f32x4& acc, float alpha) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        float t;
+        asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
+                     : "+a"(acc[v]), "=&v"(t)
+                     : "v"(alpha));
+    }
+}
+
+// Staging of one low-bit tile: load k (of NCfg::loads) covers slot units
+// 64 k .. 64 k + 63 (lane = unit - 64 k).  Tokens at or past nvalid re-read
+// token nvalid - 1 (the RoPE pairs: four tokens per chunk, read as they are).
+template <int KIND>
+__device__ __forceinline__ void stage_narrow_lowbit(int k, const uint8_t* page, int po, int nvalid,
+                                                    const PageGeom& g, uint32_t lds, int lane) {
+    using C = NCfg<KIND>;
+    const int u = 64 * k + lane;
+    if (u >= C::units) return;     // only in the last load; lane 0 of every load is active
+    int off;
+    if (u < C::u_rc) {
+        off = (po + min(u & 15, nvalid - 1)) * C::cc + 16 * (u >> 4);
+    } else if (u < C::u_mc) {
+        const int v = u - C::u_rc;
+        off = g.off_cr + (po + min(v & 15, nvalid - 1)) * 32 + 16 * (v >> 4);
+    } else if (u < C::u_mr) {
+        const int v = u - C::u_mc;
+        off = g.off_mc + (po + min(v & 15, nvalid - 1)) * 32 + 16 * (v >> 4);
+    } else {
+        off = g.off_mr + po * 4 + 16 * (u - C::u_mr);
+    }
+    dma16(page, off, lds + 64 * 16 * k);
+}
+
+// Staging of one raw bf16 tile (576 channels per row) into the padded layout:
+// unit u belongs to the last row starting at or before it; padding units
+// re-read column 71.  Row tok of the tile starts at byte row_start(tok).
+template <class RowStart>
+__device__ __forceinline__ void stage_narrow_bf16(int k, const uint8_t* src, RowStart row_start, int nvalid,
+                                                  uint32_t lds, int lane) {
+    const int u = 64 * k + lane;
+    int r = min(u / 74, 15);
+    if (u < bf_row(r)) --r;
+    const int col = min(u - bf_row(r), 71);
+    dma16(src, row_start(min(r, nvalid - 1)) + 16 * col, lds + 64 * 16 * k);
+}
+
+// Dequantize 8 channels (one code word) into fp16: pairs (2p, 2p+1).
+template <int CBITS>
+__device__ __forceinline__ f16x8 dequant8(uint32_t w, f16x2 zz, f16x2 ss) {
+    uint32_t o[4];
+    if constexpr (CBITS == 4) {
+        const uint32_t lo = w & 0x0F0F0F0Fu, hi = (w >> 4) & 0x0F0F0F0Fu;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            const uint32_t sel = static_cast<uint32_t>(p) | 0x0C000C00u | (static_cast<uint32_t>(4 + p) << 16);
+            const uint32_t b = __builtin_amdgcn_perm(hi, lo, sel) | 0x64006400u;   // 1024 + q
+            o[p] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, b) - zz) * ss);
+        }
+    } else {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            const uint32_t b = ((w >> (4 * p)) & 3u) | (((w >> (4 * p + 2)) & 3u) << 16) | 0x64006400u;
+            o[p] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, b) - zz) * ss);
+        }
+    }
+    return __builtin_bit_cast(f16x8, make_uint4(o[0], o[1], o[2], o[3]));
+}
+
+// ---------------------------------------------------------------------------
+template <int KIND, bool kProt>
+__global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[narrow_lds<KIND>(kProt)];
+
+    const int lane = threadIdx.x;
+    const int g = lane >> 4;            // lane group: tokens 4g..4g+3 of a tile, k slice 8g..8g+7
+    const int li = lane & 15;           // query row within the block; token of the score A operand
+    const int rows_total = a.s_q * a.H;
+    const int RB = (rows_total + kRows - 1) / kRows;
+
+    // Block -> (work item, row block): contiguous work items per XCD (block
+    // id mod 8), as in decode_attn.hip.
+    const int per_xcd = (a.num_work + 7) / 8;
+    const int slot = blockIdx.x >> 3;
+    const int w = (blockIdx.x & 7) * per_xcd + slot / RB;
+    const int rb = slot % RB;
+    if (w >= a.num_work) return;
+
+    const int P = a.g.page_size;
+    int b, split = 0;
+    if (a.split_tokens == 0) {
+        b = w;
+    } else {
+        int lo = 0, hi = a.B;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (a.split_indptr[mid] <= w) lo = mid; else hi = mid - 1;
+        }
+        b = lo < a.B ? lo : a.B - 1;
+        split = w - a.split_indptr[b];
+    }
+    const int L = min(max(a.seq_lens[b], 0), a.max_pages * P);
+    const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_pages;
+
+    const int row = rb * kRows + li;
+    const bool row_ok = row < rows_total;
+    const int qi = row_ok ? row / a.H : 0;
+    const int h = row_ok ? row % a.H : 0;
+    const int64_t qrow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
+
+    float m_ref = -INFINITY, m_true = -INFINITY, l_run = 0.0f;
+    f32x4 acc[32];
+#pragma unroll
+    for (int m = 0; m < 32; ++m) acc[m] = f32x4{};
+
+    const uint8_t* ring_base = nullptr;
+    int ring_rows = 1, ring_nsink = 0, ring_q0 = 0;
+
+    // One phase over keys [t_begin, t_end) in one representation (see
+    // decode_attn.hip): PK is the cache kind whose pipeline runs; kRing reads
+    // bf16 rows of the protection buffer.  This lane's row sees keys
+    // t_lo <= t < lim.
+    auto run = [&](auto kind_c, auto ring_c, const int t_begin, const int t_end, const int t_lo,
+                   const int lim) __attribute__((always_inline)) {
+        constexpr int PK = decltype(kind_c)::value;
+        constexpr bool kRing = decltype(ring_c)::value;
+        using C = NCfg<PK>;
+        using OpT = std::conditional_t<C::lowbit, f16x8, bf16x8>;
+        const int n_tiles = t_end > t_begin ? (t_end - t_begin + kTok - 1) / kTok : 0;
+        (void)t_lo;
+
+        // queries (B operand of the scores): k-step kk holds channels 32 kk + 8 g .. +8 of row li
+        OpT qf[kQSteps];
+        {
+            const uint16_t* ql = a.q_lat + qrow * kDc + 8 * g;
+            const uint16_t* qr = a.q_rope + qrow * 64 + 8 * g;
+#pragma unroll
+            for (int kk = 0; kk < kQSteps; ++kk) {
+                // rows past the end read a valid row; their results are never stored
+                const uint4 v = *reinterpret_cast<const uint4*>(kk < 16 ? ql + 32 * kk : qr + 32 * (kk - 16));
+                if constexpr (C::lowbit)
+                    qf[kk] = __builtin_bit_cast(f16x8, make_uint4(bf16x2_to_f16x2(v.x), bf16x2_to_f16x2(v.y),
+                                                                  bf16x2_to_f16x2(v.z), bf16x2_to_f16x2(v.w)));
+                else
+                    qf[kk] = __builtin_bit_cast(bf16x8, v);
+            }
+        }
+
+        auto slot_base = [&](int j) {
+            if constexpr (C::lowbit) return smem + slot_offset(j, C::NS, C::stage_bytes);
+            else return smem + slot_offset(j, C::NS, kBfTileBytes);
+        };
+        auto issue_tile = [&](int j) __attribute__((always_inline)) {
+            const int t0 = t_begin + min(j, n_tiles - 1) * kTok;   // past the end: the last tile again
+            const int nvalid = min(t_end - t0, kTok);
+            const uint32_t lds = lds_addr(slot_base(j));
+            if constexpr (kRing) {
+                auto row_start = [&](int tok) {
+                    const int v = t0 + tok;
+                    const int x = ring_q0 + (v - ring_nsink);       // < 2 * recent
+                    const int r = v < ring_nsink ? v : a.sink + (x >= a.recent ? x - a.recent : x);
+                    return min(r, ring_rows - 1) * 1152;
+                };
+#pragma unroll
+                for (int k = 0; k < C::loads; ++k) stage_narrow_bf16(k, ring_base, row_start, nvalid, lds, lane);
+            } else {
+                int pid = load_page_id(bt, t0 / P);
+                pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
+                const uint8_t* page = a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
+                const int po = t0 % P;
+                if constexpr (C::lowbit) {
+#pragma unroll
+                    for (int k = 0; k < C::loads; ++k) stage_narrow_lowbit<PK>(k, page, po, nvalid, a.g, lds, lane);
+                } else {
+                    auto row_start = [&](int tok) { return (po + tok) * 1152; };
+#pragma unroll
+                    for (int k = 0; k < C::loads; ++k) stage_narrow_bf16(k, page, row_start, nvalid, lds, lane);
+                }
+            }
+        };
+
+        if (n_tiles == 0) return;
+#pragma unroll
+        for (int j = 0; j < C::D; ++j) issue_tile(j);
+
+        for (int it = 0; it < n_tiles; ++it) {
+            // tile it has landed (tiles it+1 .. it+D-1 may still be in flight) and
+            // every LDS access of the previous step is done; then stage tile it+D
+            // into the slot tile it-1 used
+            wait_loads<(C::D - 1) * C::loads>();
+            issue_tile(it + C::D);
+            const uint8_t* st = slot_base(it);
+
+            // ---- scores
+            f32x4 s = f32x4{};
+            if constexpr (C::lowbit) {
+                uint8_t* tile = smem + C::NS * C::stage_bytes;
+                const uint4 mc0 = *reinterpret_cast<const uint4*>(st + 16 * (C::u_mc + li));
+                const uint4 mc1 = *reinterpret_cast<const uint4*>(st + 16 * (C::u_mc + 16 + li));
+                f16x2 rz, rs;
+                if constexpr (C::pmeta) {
+                    pmeta_to_f16(__uint_as_float(mc1.z), mc1.w & 0xFFu, rz, rs);
+                } else {
+                    meta_to_f16(*reinterpret_cast<const uint32_t*>(st + 16 * C::u_mr + 4 * li), rz, rs);
+                }
+#pragma unroll
+                for (int kk = 0; kk < kQSteps; ++kk) {
+                    uint32_t word;
+                    f16x2 zz = rz, ss = rs;
+                    if (kk < 16) {
+                        if constexpr (C::cbits == 4) {
+                            word = *reinterpret_cast<const uint32_t*>(st + 16 * (16 * kk + li) + 4 * g);
+                        } else {
+                            word = *reinterpret_cast<const uint16_t*>(st + 16 * (16 * (kk >> 1) + li) + 8 * (kk & 1) +
+                                                                      2 * g);
+                        }
+                        const int grp = kk >> 1;
+                        if constexpr (C::pmeta) {
+                            const uint32_t sw = grp < 4 ? (grp < 2 ? mc0.x : mc0.y) : (grp < 6 ? mc0.z : mc0.w);
+                            const uint32_t sbits = (sw >> (16 * (grp & 1))) & 0xFFFFu;
+                            const uint32_t zw = grp < 4 ? mc1.x : mc1.y;
+                            pmeta_to_f16(__uint_as_float(sbits << 16), (zw >> (8 * (grp & 3))) & 0xFFu, zz, ss);
+                        } else {
+                            const uint32_t mw = grp < 4 ? (grp < 2 ? (grp == 0 ? mc0.x : mc0.y) : (grp == 2 ? mc0.z : mc0.w))
+                                                        : (grp < 6 ? (grp == 4 ? mc1.x : mc1.y) : (grp == 6 ? mc1.z : mc1.w));
+                            meta_to_f16(mw, zz, ss);
+                        }
+                    } else {
+                        word = *reinterpret_cast<const uint32_t*>(st + 16 * (C::u_rc + 16 * (kk - 16) + li) + 4 * g);
+                    }
+                    const f16x8 kv = kk < 16 ? dequant8<C::cbits>(word, zz, ss) : dequant8<4>(word, zz, ss);
+                    if (kk < 16)
+                        *reinterpret_cast<f16x8*>(tile + 16 * (f16_row(li) + 4 * kk + g)) = kv;
+                    s = __builtin_amdgcn_mfma_f32_16x16x32_f16(kv, qf[kk], s, 0, 0, 0);
+                }
+            } else {
+#pragma unroll
+                for (int kk = 0; kk < kQSteps; ++kk) {
+                    const bf16x8 kv = *reinterpret_cast<const bf16x8*>(st + 16 * (bf_row(li) + 4 * kk + g));
+                    s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qf[kk], s, 0, 0, 0);
+                }
+            }
+
+            // ---- mask and online softmax (lane: tokens 4g+v of its row)
+            const int t0 = t_begin + it * kTok;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int t = t0 + 4 * g + v;
+                bool ok = t < lim;
+                if constexpr (kProt) ok = ok && t >= t_lo;
+                s[v] = ok ? s[v] : -INFINITY;
+            }
+            const float mr = max4(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
+            const float mt = mr * a.scale_log2;
+            m_true = fmaxf(m_true, mt);
+            if (m_ref == -INFINITY) m_ref = mt;
+            const bool move = __builtin_amdgcn_ballot_w64(mt > m_ref + kRefSlack) != 0;
+            if (move) {
+                const float m_new = fmaxf(m_ref, mt);
+                const float alpha = m_new == m_ref ? 1.0f : __builtin_amdgcn_exp2f(m_ref - m_new);
+                m_ref = m_new;
+                l_run *= alpha;
+#pragma unroll
+                for (int m = 0; m < 32; ++m) scale_acc4(acc[m], alpha);
+            }
+            const float nref = m_ref == -INFINITY ? 0.0f : -m_ref;
+            float p[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                p[v] = __builtin_amdgcn_exp2f(fmaf(s[v], a.scale_log2, nref));
+                l_run += p[v];
+            }
+
+            // ---- aggregation: O^T[16 channels][16 rows] += V^T . P^T per block
+            const uint8_t* vt;
+            int vrow;
+            if constexpr (C::lowbit) {
+                vt = smem + C::NS * C::stage_bytes;
+                vrow = f16_row(4 * g + (li >> 2));
+            } else {
+                vt = st;
+                vrow = bf_row(4 * g + (li >> 2));
+            }
+            const uint8_t* vbase = vt + 16 * vrow + 8 * (li & 3);
+            if constexpr (C::lowbit) {
+                const f16x4 pb = {static_cast<_Float16>(p[0]), static_cast<_Float16>(p[1]),
+                                  static_cast<_Float16>(p[2]), static_cast<_Float16>(p[3])};
+#pragma unroll
+                for (int m = 0; m < 32; ++m) {
+                    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + 32 * m));
+                    acc[m] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, v), pb, acc[m], 0, 0, 0);
+                }
+            } else {
+                const uint32_t p01 = pack_bf16x2(p[0], p[1]), p23 = pack_bf16x2(p[2], p[3]);
+                const s16x4 pb = __builtin_bit_cast(s16x4, make_uint2(p01, p23));
+#pragma unroll
+                for (int m = 0; m < 32; ++m) {
+                    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + 32 * m));
+                    acc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(v, pb, acc[m], 0, 0, 0);
+                }
+            }
+        }
+        // no direct-to-LDS load may outlive the workgroup's LDS
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    };
+
+    if constexpr (!kProt) {
+        int t_begin = 0, t_end = L;
+        if (a.split_tokens != 0) {
+            t_begin = max(split * a.split_tokens, 0);
+            t_end = min(split * a.split_tokens + a.split_tokens, L);
+        }
+        const int lim = row_ok ? min(L - a.s_q + qi + 1, t_end) : t_begin;
+        run(std::integral_constant<int, KIND>{}, std::false_type{}, t_begin, t_end, t_begin, lim);
+    } else {
+        // the tile list of mla_plan_splits_protected (32-key list tiles)
+        const int sink = a.sink, recent = a.recent;
+        const bool has_packed = L - recent > sink;
+        const int pk0 = has_packed ? sink / 32 : 0;
+        const int n_pk = has_packed ? (L - recent + 31) / 32 - pk0 : 0;
+        const int n_prot = has_packed ? sink + recent : L;
+        const int n_list = n_pk + (n_prot + 31) / 32;
+        int u0 = 0, u1 = n_list;
+        if (a.split_tokens != 0) {
+            u0 = split * (a.split_tokens / 32);
+            u1 = min(u0 + a.split_tokens / 32, n_list);
+        }
+        if (u0 < n_pk) {
+            const int tb = 32 * (pk0 + u0);
+            const int te = min(32 * (pk0 + min(u1, n_pk)), L - recent);
+            const int lim = row_ok ? min(L - a.s_q + qi + 1, te) : tb;
+            run(std::integral_constant<int, KIND>{}, std::false_type{}, tb, te, sink, lim);
+        }
+        if (u1 > n_pk) {
+            ring_rows = sink + recent;
+            ring_nsink = min(sink, L);
+            const int r0 = max(sink, L - recent);
+            ring_q0 = recent > 0 ? (r0 - sink) % recent : 0;
+            int64_t pslot = a.prot_slot[b];
+            pslot = pslot < 0 ? 0 : (pslot >= a.num_prot ? a.num_prot - 1 : pslot);
+            ring_base = a.prot + pslot * ring_rows * 1152;
+            auto below = [&](int x) { return min(max(x, 0), ring_nsink) + max(0, x - r0); };
+            const int vb = 32 * (max(u0, n_pk) - n_pk);
+            const int ve = min(32 * (u1 - n_pk), n_prot);
+            const int lim = row_ok ? min(below(L - a.s_q + qi + 1), ve) : vb;
+            run(std::integral_constant<int, KIND_BF16>{}, std::true_type{}, vb, ve, 0, lim);
+        }
+    }
+
+    // ---- epilogue: this lane holds channels 16 m + 4 g .. +3 of row li
+    const float l_tot = sum4(l_run);
+    if (!row_ok) return;
+    const int64_t orow = qrow;
+    if (a.split_tokens == 0) {
+        const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+        uint16_t* op = a.out + orow * kDc + 4 * g;
+#pragma unroll
+        for (int m = 0; m < 32; ++m)
+            *reinterpret_cast<uint2*>(op + 16 * m) =
+                make_uint2(pack_bf16x2(acc[m][0] * inv, acc[m][1] * inv), pack_bf16x2(acc[m][2] * inv, acc[m][3] * inv));
+        if (a.lse != nullptr && g == 0)
+            a.lse[orow] = l_tot > 0.0f ? (m_ref + log2f(l_tot)) * kLn2 : -INFINITY;
+    } else {
+        const int64_t prow = (static_cast<int64_t>(w) * a.s_q + qi) * a.H + h;
+        const float f = m_true == -INFINITY ? 0.0f : exp2f(m_ref - m_true);
+        float* op = a.part_o + prow * kDc + 4 * g;
+#pragma unroll
+        for (int m = 0; m < 32; ++m)
+            *reinterpret_cast<float4*>(op + 16 * m) =
+                make_float4(acc[m][0] * f, acc[m][1] * f, acc[m][2] * f, acc[m][3] * f);
+        if (g == 0) {
+            a.part_m[prow] = m_true * kLn2;
+            a.part_s[prow] = l_tot * f;
+        }
+    }
+}
+
+template <bool kProt>
+hipError_t launch(CacheKind kind, const DecodeArgs& a, hipStream_t stream) {
+    if (a.num_work == 0) return hipSuccess;
+    const int RB = (a.s_q * a.H + kRows - 1) / kRows;
+    const dim3 grid(static_cast<unsigned>(((a.num_work + 7) / 8) * 8 * RB)), block(64);
+    switch (kind) {
+        case KIND_C4R4: hipLaunchKernelGGL((narrow_kernel<KIND_C4R4, kProt>), grid, block, 0, stream, a); break;
+        case KIND_C2R4: hipLaunchKernelGGL((narrow_kernel<KIND_C2R4, kProt>), grid, block, 0, stream, a); break;
+        case KIND_C4R4P: hipLaunchKernelGGL((narrow_kernel<KIND_C4R4P, kProt>), grid, block, 0, stream, a); break;
+        case KIND_C2R4P: hipLaunchKernelGGL((narrow_kernel<KIND_C2R4P, kProt>), grid, block, 0, stream, a); break;
+        case KIND_BF16:
+            if constexpr (kProt) return hipErrorInvalidValue;
+            else hipLaunchKernelGGL((narrow_kernel<KIND_BF16, false>), grid, block, 0, stream, a);
+            break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_decode_narrow(CacheKind kind, const DecodeArgs& a, hipStream_t stream) {
+    return launch<false>(kind, a, stream);
+}
+
+hipError_t launch_decode_narrow_protected(CacheKind kind, const DecodeArgs& a, hipStream_t stream) {
+    return launch<true>(kind, a, stream);
+}
+
+}  // namespace mla

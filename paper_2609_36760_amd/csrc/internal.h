@@ -85,6 +85,10 @@ hipError_t launch_lowbit_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_bf16_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_decode_protected(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
+// The same computation for few query rows (s_q * H <= kNarrowRows): 16 rows per one-wave workgroup.
+constexpr int kNarrowRows = 32;
+hipError_t launch_decode_narrow(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
+hipError_t launch_decode_narrow_protected(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_lowbit_append_protected(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 

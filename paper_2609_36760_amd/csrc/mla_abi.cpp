@@ -205,13 +205,16 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
     const mla::CacheKind kind = !lowbit ? mla::KIND_BF16
                                 : f->c_bits == 4 ? (paper ? mla::KIND_C4R4P : mla::KIND_C4R4)
                                                  : (paper ? mla::KIND_C2R4P : mla::KIND_C2R4);
-    if (pd == nullptr) return hip_status(mla::launch_decode(kind, a, stream));
+    const bool narrow = s_q * H <= mla::kNarrowRows;
+    if (pd == nullptr)
+        return hip_status(narrow ? mla::launch_decode_narrow(kind, a, stream) : mla::launch_decode(kind, a, stream));
     a.prot = static_cast<const uint8_t*>(pd->prot);
     a.num_prot = pd->num_prot;
     a.prot_slot = pd->prot_slot;
     a.sink = pd->policy->sink;
     a.recent = pd->policy->recent;
-    return hip_status(mla::launch_decode_protected(kind, a, stream));
+    return hip_status(narrow ? mla::launch_decode_narrow_protected(kind, a, stream)
+                             : mla::launch_decode_protected(kind, a, stream));
 }
 
 }  // namespace

@@ -269,3 +269,29 @@ def test_repeated_launches_are_deterministic():
         torch.cuda.synchronize()
         assert torch.equal(run.part_o, ref_o) and torch.equal(run.part_m, ref_m)
         assert torch.equal(run.out, ref_out)
+
+
+# ---- few query rows (s_q * H <= 32: the narrow kernel) ----------------------
+
+NARROW = [
+    # (name, H, s_q, lens, c_bits or 'bf16', split)
+    ("n_c2_h16_sq1_split32", 16, 1, [1, 15, 16, 17, 200, 331], 2, 32),
+    ("n_c4_h32_sq1_nosplit", 32, 1, [3, 48, 95, 260], 4, 0),
+    ("n_bf16_h16_sq2_split64", 16, 2, [2, 31, 130, 257], "bf16", 64),
+    ("n_c4_h16_sq1_split96", 16, 1, [1, 96, 97, 1000, 2049], 4, 96),
+]
+
+
+@pytest.mark.parametrize("case", NARROW, ids=[c[0] for c in NARROW])
+def test_decode_narrow_all_rows(case):
+    name, H, s_q, lens, cb, split = case
+    kind = "bf16" if cb == "bf16" else "lowbit"
+    bits = 4 if cb == "bf16" else cb
+    w = syn.Workload(name, 160 + NARROW.index(case), B=len(lens), H=H, s_q=s_q, context=None,
+                     layers=((bits, 4),), split_tokens=split, ctx_range=(1, 2))
+    run = _run(w, kind=kind, seq_lens=np.asarray(lens, np.int32))
+    stats = AttnStats()
+    for b in range(len(lens)):
+        check_sequence(stats, run, b)
+        print(f"  seq {b} L={lens[b]}: cumulative max_abs={stats.abs_max:.4g}", flush=True)
+    stats.check(name, rms_max=False)

@@ -114,3 +114,15 @@ def test_protected_decode_bench_shape_sampled():
     stats.check("dsv3_b32_h128_4k_c4r4 protected")
     del run
     torch.cuda.empty_cache()
+
+
+def test_protected_decode_paper_attention_shape():
+    """The paper's kernel configuration: 16 heads, one query token, C4R4 with
+    sink 4 / recent 128, split key ranges; 8 sequences of 4096 tokens, every row."""
+    from paper_2609_36760_amd import _binding as mb
+    w = syn.Workload("paper_h16_b8_4k", 330, B=8, H=16, s_q=1, context=4096, split_tokens=256)
+    run = _run(w, mb.protect_policy())
+    stats = AttnStats()
+    for b in range(w.B):
+        check_sequence_protected(stats, run, b)
+    stats.check("paper_h16_b8_4k protected")
