@@ -187,6 +187,82 @@ def measured_traffic(workload: str):
     return fetch + write
 
 
+# The paper's attention latency table (Appendix F.1): 16 heads, one query token,
+# C4R4 with sink 4 / recent 128 against a BF16 cache, on its own (unnamed
+# NVIDIA) GPU, microseconds.  Context only.
+PAPER_GRID_US = {
+    (8, 1024): (25.69, 23.78), (8, 4096): (51.43, 53.63), (8, 8192): (82.50, 85.35),
+    (8, 16384): (147.34, 149.79), (8, 32768): (281.44, 281.99), (8, 65536): (542.14, 540.61),
+    (8, 131072): (1067.24, 1062.32), (8, 262144): (2122.10, 2113.33), (8, 524288): (4234.79, 4214.84),
+    (8, 1048576): (8440.05, 8418.63),
+    (32, 1024): (55.50, 56.97), (32, 4096): (156.82, 155.54), (32, 8192): (287.58, 283.46),
+    (32, 16384): (548.73, 547.20), (32, 32768): (1072.93, 1067.28), (32, 65536): (2133.71, 2124.10),
+    (32, 131072): (4236.96, 4225.35), (32, 262144): (8449.30, 8426.35), (32, 524288): (16880.19, 16827.11),
+    (32, 1048576): (33701.48, 33609.17),
+}
+
+
+def grid_split(B: int, n_list: int, target: int = 1024) -> int:
+    """Key split (tokens) giving about `target` work items over B sequences of
+    n_list 32-key list tiles (at least 64 tokens per split)."""
+    per = max(2, -(-B * n_list // target))
+    return 32 * per
+
+
+def paper_grid(args):
+    """Attention latency over the paper's grid: decode + combine, L2 flushed
+    (a 512 MiB write) before every sample, HIP events on the launch stream."""
+    import torch
+
+    from paper_2609_36760_amd import _binding as mb
+    from paper_2609_36760_amd import synthetic as syn
+    from paper_2609_36760_amd.runner import DecodeRun
+    contexts = [int(x) for x in args.grid_contexts.split(",")]
+    batches = [int(x) for x in args.grid_batches.split(",")]
+    pol = mb.protect_policy(4, 128)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    rows = []
+    for B in batches:
+        for N in contexts:
+            rec = {"batch": B, "context": N}
+            for label, kind, protect in (("c4r4", "lowbit", pol), ("bf16", "bf16", None)):
+                n_list = (-(-(N - 128) // 32) + 5) if protect is not None else -(-N // 32)
+                split = grid_split(B, n_list)
+                w = syn.Workload(f"paper_h16_b{B}_{N}", 60, B=B, H=16, s_q=1, context=N)
+                t0 = time.perf_counter()
+                run = DecodeRun(w, kind=kind, protect=protect, split_tokens=split, device_tokens=True)
+                run.append_new_tokens()
+                torch.cuda.synchronize()
+                setup = time.perf_counter() - t0
+                lat = []
+                for i in range(args.grid_warmup + args.grid_samples):
+                    flush.fill_(i & 0xFF)
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    run.attend()
+                    e1.record(stream)
+                    torch.cuda.synchronize()
+                    if i >= args.grid_warmup:
+                        lat.append(e0.elapsed_time(e1) * 1e3)
+                us = float(np.mean(lat))
+                nbytes = algorithmic_bytes(run)
+                rec[label] = {"us": us, "us_min": float(np.min(lat)), "splits": run.num_splits,
+                              "split_tokens": split, "bytes": nbytes, "gbs": nbytes / (us * 1e-6) / 1e9,
+                              "hbm_frac": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+                log(f"[grid B={B} N={N} {label}] setup {setup:.1f}s, {us:.1f} us (min {np.min(lat):.1f}), "
+                    f"{run.num_splits} splits of {split}, {rec[label]['gbs']:.0f} GB/s")
+                del run
+                torch.cuda.empty_cache()
+            rec["speedup_vs_bf16"] = rec["bf16"]["us"] / rec["c4r4"]["us"]
+            paper = PAPER_GRID_US.get((B, N))
+            rec["paper_us"] = None if paper is None else {"bf16": paper[0], "c4r4": paper[1]}
+            rows.append(rec)
+            print(json.dumps(rec), flush=True)
+    print(json.dumps({"metric": "attention latency, 16 heads, C4R4 sink4/local128 vs BF16",
+                      "unit": "us", "grid": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,6 +278,12 @@ def main():
                     help="key split of the protected step (0: as many splits per sequence as the unprotected plan)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="first copy a 256 MiB buffer once (reference for HBM traffic counters)")
+    ap.add_argument("--paper-grid", action="store_true",
+                    help="instead of the step benchmark: the paper's 16-head attention latency grid")
+    ap.add_argument("--grid-batches", default="8,32")
+    ap.add_argument("--grid-contexts", default="1024,4096,8192,16384,32768,65536,131072,262144,524288,1048576")
+    ap.add_argument("--grid-samples", type=int, default=30)
+    ap.add_argument("--grid-warmup", type=int, default=5)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no multi-GPU path; "
@@ -212,6 +294,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
 
+    if args.paper_grid:
+        paper_grid(args)
+        return
     if args.calib_copy:
         src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)

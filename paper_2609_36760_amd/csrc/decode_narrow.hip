@@ -116,38 +116,28 @@ __device__ __forceinline__ float sum4(float v) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-__device__ __forceinline__ void scale_acc4(f32x4& acc, float alpha) {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-        float t;
-        asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
-                     : "+a"(acc[v]), "=&v"(t)
-                     : "v"(alpha));
-    }
-}
-
 // Staging of one low-bit tile: load k (of NCfg::loads) covers slot units
 // 64 k .. 64 k + 63 (lane = unit - 64 k).  Tokens at or past nvalid re-read
 // token nvalid - 1 (the RoPE pairs: four tokens per chunk, read as they are).
+// The content codes fill whole loads (cc / 64 of them); the next load carries
+// the RoPE codes (lanes 0-31) and the metadata (lanes 32-63); with fp16
+// metadata a last load brings the RoPE pairs (lanes 0-3).
 template <int KIND>
 __device__ __forceinline__ void stage_narrow_lowbit(int k, const uint8_t* page, int po, int nvalid,
                                                     const PageGeom& g, uint32_t lds, int lane) {
     using C = NCfg<KIND>;
-    const int u = 64 * k + lane;
-    if (u >= C::units) return;     // only in the last load; lane 0 of every load is active
-    int off;
-    if (u < C::u_rc) {
-        off = (po + min(u & 15, nvalid - 1)) * C::cc + 16 * (u >> 4);
-    } else if (u < C::u_mc) {
-        const int v = u - C::u_rc;
-        off = g.off_cr + (po + min(v & 15, nvalid - 1)) * 32 + 16 * (v >> 4);
-    } else if (u < C::u_mr) {
-        const int v = u - C::u_mc;
-        off = g.off_mc + (po + min(v & 15, nvalid - 1)) * 32 + 16 * (v >> 4);
-    } else {
-        off = g.off_mr + po * 4 + 16 * (u - C::u_mr);
+    static_assert(C::u_rc % 64 == 0 && C::u_mr == C::u_rc + 64, "region boundaries on load boundaries");
+    const int last = nvalid - 1;
+    if (k < C::u_rc / 64) {
+        const int u = 64 * k + lane;
+        dma16(page, (po + min(u & 15, last)) * C::cc + 16 * (u >> 4), lds + 64 * 16 * k);
+    } else if (k == C::u_rc / 64) {
+        const int v = lane & 31;
+        const int base = lane < 32 ? g.off_cr : g.off_mc;
+        dma16(page, base + (po + min(v & 15, last)) * 32 + 16 * (v >> 4), lds + 64 * 16 * k);
+    } else if (lane < 4) {
+        dma16(page, g.off_mr + po * 4 + 16 * lane, lds + 64 * 16 * k);
     }
-    dma16(page, off, lds + 64 * 16 * k);
 }
 
 // Staging of one raw bf16 tile (576 channels per row) into the padded layout:
@@ -301,65 +291,10 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
 #pragma unroll
         for (int j = 0; j < C::D; ++j) issue_tile(j);
 
-        for (int it = 0; it < n_tiles; ++it) {
-            // tile it has landed (tiles it+1 .. it+D-1 may still be in flight) and
-            // every LDS access of the previous step is done; then stage tile it+D
-            // into the slot tile it-1 used
-            wait_loads<(C::D - 1) * C::loads>();
-            issue_tile(it + C::D);
-            const uint8_t* st = slot_base(it);
-
-            // ---- scores
-            f32x4 s = f32x4{};
-            if constexpr (C::lowbit) {
-                uint8_t* tile = smem + C::NS * C::stage_bytes;
-                const uint4 mc0 = *reinterpret_cast<const uint4*>(st + 16 * (C::u_mc + li));
-                const uint4 mc1 = *reinterpret_cast<const uint4*>(st + 16 * (C::u_mc + 16 + li));
-                f16x2 rz, rs;
-                if constexpr (C::pmeta) {
-                    pmeta_to_f16(__uint_as_float(mc1.z), mc1.w & 0xFFu, rz, rs);
-                } else {
-                    meta_to_f16(*reinterpret_cast<const uint32_t*>(st + 16 * C::u_mr + 4 * li), rz, rs);
-                }
-#pragma unroll
-                for (int kk = 0; kk < kQSteps; ++kk) {
-                    uint32_t word;
-                    f16x2 zz = rz, ss = rs;
-                    if (kk < 16) {
-                        if constexpr (C::cbits == 4) {
-                            word = *reinterpret_cast<const uint32_t*>(st + 16 * (16 * kk + li) + 4 * g);
-                        } else {
-                            word = *reinterpret_cast<const uint16_t*>(st + 16 * (16 * (kk >> 1) + li) + 8 * (kk & 1) +
-                                                                      2 * g);
-                        }
-                        const int grp = kk >> 1;
-                        if constexpr (C::pmeta) {
-                            const uint32_t sw = grp < 4 ? (grp < 2 ? mc0.x : mc0.y) : (grp < 6 ? mc0.z : mc0.w);
-                            const uint32_t sbits = (sw >> (16 * (grp & 1))) & 0xFFFFu;
-                            const uint32_t zw = grp < 4 ? mc1.x : mc1.y;
-                            pmeta_to_f16(__uint_as_float(sbits << 16), (zw >> (8 * (grp & 3))) & 0xFFu, zz, ss);
-                        } else {
-                            const uint32_t mw = grp < 4 ? (grp < 2 ? (grp == 0 ? mc0.x : mc0.y) : (grp == 2 ? mc0.z : mc0.w))
-                                                        : (grp < 6 ? (grp == 4 ? mc1.x : mc1.y) : (grp == 6 ? mc1.z : mc1.w));
-                            meta_to_f16(mw, zz, ss);
-                        }
-                    } else {
-                        word = *reinterpret_cast<const uint32_t*>(st + 16 * (C::u_rc + 16 * (kk - 16) + li) + 4 * g);
-                    }
-                    const f16x8 kv = kk < 16 ? dequant8<C::cbits>(word, zz, ss) : dequant8<4>(word, zz, ss);
-                    if (kk < 16)
-                        *reinterpret_cast<f16x8*>(tile + 16 * (f16_row(li) + 4 * kk + g)) = kv;
-                    s = __builtin_amdgcn_mfma_f32_16x16x32_f16(kv, qf[kk], s, 0, 0, 0);
-                }
-            } else {
-#pragma unroll
-                for (int kk = 0; kk < kQSteps; ++kk) {
-                    const bf16x8 kv = *reinterpret_cast<const bf16x8*>(st + 16 * (bf_row(li) + 4 * kk + g));
-                    s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qf[kk], s, 0, 0, 0);
-                }
-            }
-
-            // ---- mask and online softmax (lane: tokens 4g+v of its row)
+        // online softmax of one tile's scores (lane: tokens 4g+v of row li):
+        // masks, moves the reference (rescaling the accumulators, which hold
+        // every earlier tile) when needed, returns the weights
+        auto softmax = [&](int it, f32x4 s, float p[4]) __attribute__((always_inline)) {
             const int t0 = t_begin + it * kTok;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
@@ -379,42 +314,146 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
                 m_ref = m_new;
                 l_run *= alpha;
 #pragma unroll
-                for (int m = 0; m < 32; ++m) scale_acc4(acc[m], alpha);
+                for (int m = 0; m < 32; ++m) acc[m] *= alpha;
             }
             const float nref = m_ref == -INFINITY ? 0.0f : -m_ref;
-            float p[4];
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 p[v] = __builtin_amdgcn_exp2f(fmaf(s[v], a.scale_log2, nref));
                 l_run += p[v];
             }
+        };
 
-            // ---- aggregation: O^T[16 channels][16 rows] += V^T . P^T per block
-            const uint8_t* vt;
-            int vrow;
-            if constexpr (C::lowbit) {
-                vt = smem + C::NS * C::stage_bytes;
-                vrow = f16_row(4 * g + (li >> 2));
-            } else {
-                vt = st;
-                vrow = bf_row(4 * g + (li >> 2));
-            }
-            const uint8_t* vbase = vt + 16 * vrow + 8 * (li & 3);
-            if constexpr (C::lowbit) {
-                const f16x4 pb = {static_cast<_Float16>(p[0]), static_cast<_Float16>(p[1]),
-                                  static_cast<_Float16>(p[2]), static_cast<_Float16>(p[3])};
+        if constexpr (C::lowbit) {
+            // Software pipeline: step it computes the scores of tile it (its
+            // operands dequantized in registers) interleaved with the aggregation
+            // of tile it-1 (read transposed from the fp16 tile); once the
+            // aggregation's reads are done, tile it's content channels replace
+            // tile it-1's in the fp16 tile.
+            uint8_t* tile = smem + C::NS * C::stage_bytes;
+            const uint8_t* vbase = tile + 16 * f16_row(4 * g + (li >> 2)) + 8 * (li & 3);
+            uint32_t words[kQSteps];
+            uint4 mc0, mc1;
+            uint32_t rmw = 0;
+            auto read_stage = [&](const uint8_t* st) __attribute__((always_inline)) {
 #pragma unroll
-                for (int m = 0; m < 32; ++m) {
-                    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + 32 * m));
-                    acc[m] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, v), pb, acc[m], 0, 0, 0);
+                for (int kk = 0; kk < kQSteps; ++kk) {
+                    if (kk >= 16)
+                        words[kk] = *reinterpret_cast<const uint32_t*>(st + 16 * (C::u_rc + 16 * (kk - 16) + li) + 4 * g);
+                    else if constexpr (C::cbits == 4)
+                        words[kk] = *reinterpret_cast<const uint32_t*>(st + 16 * (16 * kk + li) + 4 * g);
+                    else
+                        words[kk] = *reinterpret_cast<const uint16_t*>(st + 16 * (16 * (kk >> 1) + li) + 8 * (kk & 1) +
+                                                                       2 * g);
                 }
-            } else {
-                const uint32_t p01 = pack_bf16x2(p[0], p[1]), p23 = pack_bf16x2(p[2], p[3]);
-                const s16x4 pb = __builtin_bit_cast(s16x4, make_uint2(p01, p23));
+                mc0 = *reinterpret_cast<const uint4*>(st + 16 * (C::u_mc + li));
+                mc1 = *reinterpret_cast<const uint4*>(st + 16 * (C::u_mc + 16 + li));
+                if constexpr (!C::pmeta) rmw = *reinterpret_cast<const uint32_t*>(st + 16 * C::u_mr + 4 * li);
+            };
+            auto dq = [&](int kk) __attribute__((always_inline)) {
+                f16x2 zz, ss;
+                if (kk >= 16) {
+                    if constexpr (C::pmeta) pmeta_to_f16(__uint_as_float(mc1.z), mc1.w & 0xFFu, zz, ss);
+                    else meta_to_f16(rmw, zz, ss);
+                    return dequant8<4>(words[kk], zz, ss);
+                }
+                const int grp = kk >> 1;
+                if constexpr (C::pmeta) {
+                    const uint32_t sw = grp < 4 ? (grp < 2 ? mc0.x : mc0.y) : (grp < 6 ? mc0.z : mc0.w);
+                    const uint32_t sbits = (sw >> (16 * (grp & 1))) & 0xFFFFu;
+                    const uint32_t zw = grp < 4 ? mc1.x : mc1.y;
+                    pmeta_to_f16(__uint_as_float(sbits << 16), (zw >> (8 * (grp & 3))) & 0xFFu, zz, ss);
+                } else {
+                    const uint32_t mw = grp < 4 ? (grp < 2 ? (grp == 0 ? mc0.x : mc0.y) : (grp == 2 ? mc0.z : mc0.w))
+                                                : (grp < 6 ? (grp == 4 ? mc1.x : mc1.y) : (grp == 6 ? mc1.z : mc1.w));
+                    meta_to_f16(mw, zz, ss);
+                }
+                return dequant8<C::cbits>(words[kk], zz, ss);
+            };
+            f16x8 kv[kQSteps];
+            float p[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            constexpr int kVAhead = 8;
+            s16x4 vb[kVAhead];
+            auto vread = [&](int m) {
+                return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + 32 * m));
+            };
+            auto pv = [&](int m, f16x4 pbh) __attribute__((always_inline)) {
+                acc[m] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, vb[m % kVAhead]), pbh, acc[m],
+                                                               0, 0, 0);
+                if (m + kVAhead < 32) vb[m % kVAhead] = vread(m + kVAhead);
+            };
+            // one step: scores of tile it (QK) and aggregation of tile it-1 (PV)
+            auto step = [&](int it, auto QK, auto PV) __attribute__((always_inline)) {
+                constexpr bool kQK = decltype(QK)::value, kPV = decltype(PV)::value;
+                const f16x4 pbh = {static_cast<_Float16>(p[0]), static_cast<_Float16>(p[1]),
+                                   static_cast<_Float16>(p[2]), static_cast<_Float16>(p[3])};
+                f32x4 s = f32x4{};
+                if constexpr (kQK) {
+                    // tile it has landed; every LDS access before this point is done
+                    wait_loads<(C::D - 1) * C::loads>();
+                    read_stage(slot_base(it));
+                    issue_tile(it + C::D);
+                }
+                if constexpr (kPV) {
+#pragma unroll
+                    for (int m = 0; m < kVAhead; ++m) vb[m] = vread(m);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int kk = 0; kk < kQSteps; ++kk) {
+                    if constexpr (kQK) {
+                        kv[kk] = dq(kk);
+                        s = __builtin_amdgcn_mfma_f32_16x16x32_f16(kv[kk], qf[kk], s, 0, 0, 0);
+                    }
+                    if constexpr (kPV) {
+                        if (kk < 16) {
+                            pv(2 * kk, pbh);
+                            pv(2 * kk + 1, pbh);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                if constexpr (kQK) {
+                    // tile it-1's transposing reads are all consumed: overwrite it
+#pragma unroll
+                    for (int kk = 0; kk < 16; ++kk)
+                        *reinterpret_cast<f16x8*>(tile + 16 * (f16_row(li) + 4 * kk + g)) = kv[kk];
+                    softmax(it, s, p);
+                }
+            };
+            step(0, std::true_type{}, std::false_type{});
+            for (int it = 1; it < n_tiles; ++it) step(it, std::true_type{}, std::true_type{});
+            step(n_tiles, std::false_type{}, std::true_type{});
+        } else {
+            // raw bf16 rows: both products read the staged tile directly
+            for (int it = 0; it < n_tiles; ++it) {
+                // tile it has landed and every LDS access of the previous step is
+                // done; then stage tile it+D into the slot tile it-1 used
+                wait_loads<(C::D - 1) * C::loads>();
+                issue_tile(it + C::D);
+                const uint8_t* st = slot_base(it);
+                bf16x8 kv[kQSteps];
+#pragma unroll
+                for (int kk = 0; kk < kQSteps; ++kk)
+                    kv[kk] = *reinterpret_cast<const bf16x8*>(st + 16 * (bf_row(li) + 4 * kk + g));
+                f32x4 s = f32x4{};
+#pragma unroll
+                for (int kk = 0; kk < kQSteps; ++kk) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv[kk], qf[kk], s, 0, 0, 0);
+                float p[4];
+                softmax(it, s, p);
+                // aggregation: O^T[16 channels][16 rows] += V^T . P^T per block,
+                // transposing reads eight blocks ahead of the products
+                const uint8_t* vbase = st + 16 * bf_row(4 * g + (li >> 2)) + 8 * (li & 3);
+                constexpr int kVAhead = 8;
+                s16x4 vb[kVAhead];
+#pragma unroll
+                for (int m = 0; m < kVAhead; ++m) vb[m] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + 32 * m));
+                const s16x4 pbb = __builtin_bit_cast(s16x4, make_uint2(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])));
 #pragma unroll
                 for (int m = 0; m < 32; ++m) {
-                    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + 32 * m));
-                    acc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(v, pb, acc[m], 0, 0, 0);
+                    acc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vb[m % kVAhead], pbb, acc[m], 0, 0, 0);
+                    if (m + kVAhead < 32)
+                        vb[m % kVAhead] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + 32 * (m + kVAhead)));
                 }
             }
         }

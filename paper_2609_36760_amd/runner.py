@@ -26,11 +26,14 @@ def _dev(a, device):
 class DecodeRun:
     def __init__(self, w: syn.Workload, layer: int = 0, kind: str = "lowbit", device: str = "cuda",
                  split_tokens: int | None = None, seq_lens=None, threads: int = 16, prefill: bool = True,
-                 token_cache: dict | None = None, protect=None, prot_slots=None, meta: str = "fp16"):
+                 token_cache: dict | None = None, protect=None, prot_slots=None, meta: str = "fp16",
+                 device_tokens: bool = False):
         """``protect``: an ``mla_protect_policy`` to keep sink/recent tokens in
         bf16 (low-bit caches only); ``prot_slots``: the protection buffer of
         each sequence (default: buffer b for sequence b); ``meta``: "fp16"
-        (fp16 scale and zero) or "paper" (the paper's bf16 / fp32 scales)."""
+        (fp16 scale and zero) or "paper" (the paper's bf16 / fp32 scales);
+        ``device_tokens``: draw the tokens on the GPU
+        (:func:`synthetic.device_sequence_tokens`, for long contexts)."""
         if kind not in ("lowbit", "bf16"):
             raise ValueError(kind)
         if protect is not None and kind != "lowbit":
@@ -84,16 +87,18 @@ class DecodeRun:
         self.out = torch.empty((self.B, self.s_q, self.H, 512), dtype=torch.int16, device=device)
         self.lse = torch.empty((self.B, self.s_q, self.H), dtype=torch.float32, device=device)
         # the step's new tokens (the last s_q positions of every sequence)
-        new_c, new_k, new_slots = [], [], []
-        for b in range(self.B):
-            L = int(lens[b])
-            c, k = syn.sequence_tokens(w, layer, b, L, start=L - self.s_q)
-            new_c.append(c)
-            new_k.append(k)
-            new_slots.append(syn.slots_of(bt[b], np.arange(L - self.s_q, L)))
-        self.new_c = _dev(np.concatenate(new_c).view(np.int16), device)
-        self.new_k = _dev(np.concatenate(new_k).view(np.int16), device)
+        new_slots = [syn.slots_of(bt[b], np.arange(int(lens[b]) - self.s_q, int(lens[b]))) for b in range(self.B)]
         self.new_slots = _dev(np.concatenate(new_slots), device)
+        self.device_tokens = device_tokens
+        if not device_tokens:
+            new_c, new_k = [], []
+            for b in range(self.B):
+                L = int(lens[b])
+                c, k = syn.sequence_tokens(w, layer, b, L, start=L - self.s_q)
+                new_c.append(c)
+                new_k.append(k)
+            self.new_c = _dev(np.concatenate(new_c).view(np.int16), device)
+            self.new_k = _dev(np.concatenate(new_k).view(np.int16), device)
         if protect is not None:
             self.new_seq = _dev(np.repeat(np.arange(self.B, dtype=np.int32), self.s_q), device)
             self.new_pos = _dev(np.concatenate([np.arange(int(l) - self.s_q, int(l), dtype=np.int32)
@@ -101,8 +106,29 @@ class DecodeRun:
             hist = np.maximum(lens.astype(np.int64) - self.s_q, 0).astype(np.int32)
             self.hist_lens = _dev(hist, device)
         self.token_cache = token_cache
-        if prefill:
+        if device_tokens:
+            self._device_fill(prefill)
+        elif prefill:
             self._prefill(threads)
+
+    def _device_fill(self, prefill: bool):
+        """Draw every sequence on the GPU, write its history, keep its last s_q tokens."""
+        new_c, new_k = [], []
+        for b in range(self.B):
+            L = int(self.lens[b])
+            hist = L - self.s_q
+            c, k = syn.device_sequence_tokens(self.w, self.layer, b, L, self.device)
+            new_c.append(c[hist:].clone())
+            new_k.append(k[hist:].clone())
+            if prefill and hist > 0:
+                slots = _dev(syn.slots_of(self.block_table_host[b], np.arange(hist)), self.device)
+                seq = torch.full((hist,), b, dtype=torch.int32, device=self.device)
+                pos = torch.arange(hist, dtype=torch.int32, device=self.device)
+                self._append(c[:hist].view(torch.int16), k[:hist].view(torch.int16), slots, seq, pos)
+            del c, k
+        torch.cuda.synchronize()
+        self.new_c = torch.cat(new_c).view(torch.int16)
+        self.new_k = torch.cat(new_k).view(torch.int16)
 
     def _append(self, c, k, slots, seq=None, pos=None):
         if self.protect is not None:

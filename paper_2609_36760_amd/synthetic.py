@@ -18,7 +18,10 @@ Recipe (DeepSeek-V3-class MLA shapes: latent 512, RoPE key 64):
   * every value is rounded to bf16 (round-half-to-even) and handled as its
     uint16 bit pattern;
   * physical pages are a seeded permutation, so no sequence owns a contiguous
-    range of pages.
+    range of pages;
+  * contexts too long for the host (the 16-head grid up to 1M tokens) draw the
+    same distributions on the GPU from a seeded torch generator
+    (:func:`device_sequence_tokens`).
 """
 from __future__ import annotations
 
@@ -162,6 +165,33 @@ def slots_of(block_table_row: np.ndarray, positions: np.ndarray) -> np.ndarray:
     """Slot ``page * 64 + offset`` of each token position of one sequence."""
     positions = np.asarray(positions, np.int64)
     return block_table_row[positions // PAGE].astype(np.int64) * PAGE + positions % PAGE
+
+
+def device_sequence_tokens(w: Workload, layer: int, b: int, L: int, device: str = "cuda"):
+    """Tokens ``[0, L)`` of sequence ``b`` drawn on the GPU (for contexts too long
+    to draw on the host): the same distributions as :func:`sequence_tokens`
+    (content ``N(0, 1)`` with the outlier channels scaled; RoPE pairs
+    ``N(0, sigma_i^2)`` rotated by the position angle), from a torch generator
+    seeded by ``(cfg, layer, b)``; a different stream from the host recipe.
+    Returns bf16 tensors ``c_kv [L, 512]``, ``k_rope [L, 64]`` on ``device``.
+    """
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed((1000 * w.cfg + 7) * 1_000_003 + layer * 65_537 + b)
+    c = torch.randn((L, D_C), generator=gen, device=device, dtype=torch.float32)
+    c[:, torch.from_numpy(outlier_channels(w)).to(device)] *= w.outlier_mult
+    c_kv = c.to(torch.bfloat16)
+    del c
+    i = torch.arange(D_R // 2, device=device, dtype=torch.float64)
+    sigma = (0.1 * 50.0 ** (i / 31.0)).to(torch.float32)
+    xy = torch.randn((L, D_R // 2, 2), generator=gen, device=device, dtype=torch.float32) * sigma[None, :, None]
+    theta = 10000.0 ** (-2.0 * i / D_R)
+    ang = (torch.arange(L, device=device, dtype=torch.float64)[:, None] * theta[None, :]).to(torch.float32)
+    cs, sn = torch.cos(ang), torch.sin(ang)
+    kr = torch.empty((L, D_R), device=device, dtype=torch.float32)
+    kr[:, 0::2] = xy[..., 0] * cs - xy[..., 1] * sn
+    kr[:, 1::2] = xy[..., 0] * sn + xy[..., 1] * cs
+    return c_kv, kr.to(torch.bfloat16)
 
 
 def generate_sequences(w: Workload, layer: int, lens, batch=None, threads: int = 8):

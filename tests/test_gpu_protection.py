@@ -126,3 +126,34 @@ def test_protected_decode_paper_attention_shape():
     for b in range(w.B):
         check_sequence_protected(stats, run, b)
     stats.check("paper_h16_b8_4k protected")
+
+
+def test_device_drawn_inputs_sixteen_heads():
+    """Long-context inputs drawn on the GPU (the 16-head latency grid's path):
+    prefill through the protected writer and decode, every row of two 3000-token
+    sequences against the oracle on the same drawn tokens (copied to the host)."""
+    import torch
+
+    from gpu_support import bf16_bits_to_f64, elem_bound, lse_bound
+    from oracle import attention as at
+    from oracle import paged_cache as pc
+    from paper_2609_36760_amd import _binding as mb
+    from paper_2609_36760_amd.runner import DecodeRun
+    w = syn.Workload("dev_h16_b2_3000", 340, B=2, H=16, s_q=1, context=3000, split_tokens=256)
+    pol = mb.protect_policy()
+    run = DecodeRun(w, protect=pol, device_tokens=True)
+    run.step()
+    torch.cuda.synchronize()
+    stats = AttnStats()
+    for b in range(w.B):
+        c, k = syn.device_sequence_tokens(w, 0, b, 3000)
+        cb = c.view(torch.int16).cpu().numpy().view(np.uint16)
+        kb = k.view(torch.int16).cpu().numpy().view(np.uint16)
+        c_rep, k_rep = pr.representation(pc.CacheFormat(), cb, kb, pol.sink, pol.recent)
+        ql, qr = syn.queries(w, 0, batch=[b])
+        want, want_lse = at.decode_sequence(ql[0], qr[0], c_rep, k_rep, w.tau)
+        got = bf16_bits_to_f64(run.out[b].cpu().numpy())
+        bound = lse_bound(ql[0], qr[0], c_rep, k_rep, w.tau, 3000, 1)
+        tol = elem_bound(ql[0], qr[0], c_rep, k_rep, w.tau, 3000, 1, want, bound)
+        stats.add(got, want, run.lse[b].cpu().numpy(), want_lse, bound, tol)
+    stats.check("device-drawn 16 heads protected")
