@@ -126,6 +126,7 @@ template <> struct Cfg<KIND_C2R4P> : Cfg<KIND_C2R4> {
 };
 template <> struct Cfg<KIND_BF16> {
     static constexpr bool lowbit = false;
+    static constexpr int cc = 0, code_rounds = 0;
     static constexpr int stage_bytes = 0;
     static constexpr int NT = 4, NS = 0, D = 2, loads = 10;   // 2432 chunks: 9 rounds of 256 + 128
     static constexpr int SC = 76;
@@ -157,6 +158,29 @@ static_assert(lds_bytes<KIND_BF16>() <= 160 * 1024, "LDS budget of a gfx950 CU")
 
 // max / sum of a value and its copy in lane ^ 32 (v_permlane32_swap hands each
 // lane the pair {own value, partner's value} in its two results)
+// Score products accumulate in vector registers: the 256 accumulation
+// registers hold the output tiles, and a score tile kept there would be copied
+// out for the softmax (and an output tile copied in) on every step.  Issued as
+// inline assembly, so the compiler inserts no hazard waits for these: the
+// chain's first product writes the tile without reading it, the following
+// ones accumulate back to back (no wait needed between products of one shape),
+// and score_ready() supplies the wait before vector instructions read the
+// result.
+__device__ __forceinline__ void mfma_v(f32x16& c, f16x8 a, f16x8 b, bool first) {
+    if (first)
+        asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, %2, 0" : "=&v"(c) : "v"(a), "v"(b));
+    else
+        asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void mfma_v(f32x16& c, bf16x8 a, bf16x8 b, bool first) {
+    if (first)
+        asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(c) : "v"(a), "v"(b));
+    else
+        asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void score_ready(f32x16& c) {
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" : "+v"(c));
+}
 __device__ __forceinline__ float max_halves(float v) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
     return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
@@ -517,17 +541,57 @@ void decode_kernel(DecodeArgs a) {
             }
         }
 
-        // Staging.  Tile j is staged into staging slot j % NS (low-bit) or tile
-        // slot j % NT (BF16).  Step it stages tile it + D -- clamped to the last
-        // tile, whose bytes then land once more in a free slot -- so that every
-        // step issues Cfg::loads loads.  Cursor: first token and page-table index
-        // of that tile (uniform).
+        // Staging.  Step it stages tile it + D -- clamped to the last tile,
+        // whose bytes then land once more in a free slot -- so that every step
+        // issues Cfg::loads loads.  Buffer slots rotate with the step: tofs[q]
+        // is the byte offset of the tile slot of tile it + q (q < NT), sofs[q]
+        // that of the staging slot of tile it + q (low-bit, q < NS); both move
+        // on by one slot at the end of a step, so the loop does no divisions.
         const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-        auto slot_lds = [&](int j) {
-            return C::lowbit ? lds_addr(stages + slot_offset(j, C::NS, C::stage_bytes))
-                             : lds_addr(tiles + slot_offset(j, C::NT, kTileBytes));
-        };
-        auto issue = [&](int k, int pid, int t0, int j) __attribute__((always_inline)) {
+        int tofs[C::NT], sofs[C::NS > 0 ? C::NS : 1];
+#pragma unroll
+        for (int q = 0; q < C::NT; ++q) tofs[q] = q * kTileBytes;
+#pragma unroll
+        for (int q = 0; q < (C::NS > 0 ? C::NS : 1); ++q) sofs[q] = q * C::stage_bytes;
+        const uint32_t tiles_lds = lds_addr(tiles), stages_lds = lds_addr(stages);
+
+        // Per-lane parts of the staging addresses, fixed for the whole run.
+        // Packed: content chunk i of load k < code_rounds (i = 256 k + 64 wave +
+        // lane) is chunk i % cpt of token i / cpt of the tile; a small region
+        // (RoPE codes, metadata) is read 16 bytes per lane from its start.  BF16
+        // rows: row and column of the lane's chunk, two loads per register.
+        // Tokens at or past the range's end re-read its last token (nvalid - 1),
+        // so the address is one clamp and one shift-add per load.
+        constexpr int cpt = C::lowbit ? C::cc / 16 : 1;           // content chunks per token
+        constexpr int kBfPairs = C::lowbit ? 1 : (C::loads + 1) / 2;
+        uint32_t c_tok = 0, c_col = 0, s_tok = 0, s_col = 0;
+        uint32_t bf_rc[kBfPairs];
+        int s_reg = 0, s_shift = 0, dst_small = 0;
+        if constexpr (C::lowbit) {
+            c_tok = static_cast<uint32_t>(wave * 64 + lane) / cpt;
+            c_col = (static_cast<uint32_t>(wave * 64 + lane) % cpt) * 16u;
+            s_tok = wave_u < 2 ? static_cast<uint32_t>(lane >> 1) : 0u;
+            s_col = static_cast<uint32_t>(wave_u < 2 ? (lane & 1) : (lane & 7)) * 16u;
+            s_reg = wave_u == 0 ? a.g.off_cr : wave_u == 1 ? a.g.off_mc : a.g.off_mr;
+            s_shift = wave_u < 2 ? 5 : 2;
+            dst_small = wave_u == 0 ? C::rcodes : wave_u == 1 ? C::meta : (wave_u == 2 && !C::pmeta ? C::rmeta : C::spare);
+        } else {
+#pragma unroll
+            for (int k = 0; k < kBfPairs; ++k) bf_rc[k] = 0;
+#pragma unroll
+            for (int k = 0; k < C::loads; ++k) {
+                const int i = (k < 9 ? k * kThreads + wave * 64 : 2304 + 64 * (wave & 1)) + lane;
+                int row = static_cast<int>((static_cast<unsigned>(i) * 3450u) >> 18);   // i / 76 for i < 2432
+                if (i < row_off(76, row) / 16) --row;
+                const int col = min(i - row_off(76, row) / 16, 71);
+                bf_rc[k >> 1] |= static_cast<uint32_t>(row | (col << 5)) << (16 * (k & 1));
+            }
+        }
+        const bool small_lane = wave_u < 2 || lane < 8;
+
+        // Load k of the tile starting at token t0 (offset po in page pid), into
+        // the slot at LDS address slot_lds.
+        auto issue = [&](int k, int pid, int t0, int po, uint32_t slot_lds) __attribute__((always_inline)) {
             const int nvalid = min(t_end - t0, kTile);
             if constexpr (kRing) {
                 // protected position order: the sink rows, then the window from the ring
@@ -537,18 +601,26 @@ void decode_kernel(DecodeArgs a) {
                     const int r = v < ring_nsink ? v : a.sink + (x >= a.recent ? x - a.recent : x);
                     return min(r, ring_rows - 1) * 1152;
                 };
-                stage_bf16(k, ring_base, row_start, nvalid, slot_lds(j), wave, wave_u, lane);
+                stage_bf16(k, ring_base, row_start, nvalid, slot_lds, wave, wave_u, lane);
             } else {
                 pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
                 const uint8_t* page = a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
-                const int po = t0 % P;
-                if constexpr (C::lowbit)
-                    stage_lowbit<PK>(k, page, po, nvalid, a.g, slot_lds(j), wave, wave_u, lane);
-                else
-                    stage_bf16(k, page, [&](int tok) { return (po + tok) * 1152; }, nvalid, slot_lds(j), wave,
-                               wave_u, lane);
+                const uint32_t nv1 = static_cast<uint32_t>(nvalid - 1);
+                if constexpr (C::lowbit) {
+                    if (k < C::code_rounds) {
+                        const uint32_t tok = min(c_tok + static_cast<uint32_t>(k * (kThreads / cpt)), nv1);
+                        dma16_m0(page + po * C::cc, tok * C::cc + c_col, slot_lds + (k * kThreads + wave_u * 64) * 16);
+                    } else if (small_lane) {
+                        dma16_m0(page + s_reg + (po << s_shift), (min(s_tok, nv1) << 5) + s_col, slot_lds + dst_small);
+                    }
+                } else {
+                    const uint32_t rc = (bf_rc[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
+                    const int base_u = k < 9 ? k * kThreads + wave_u * 64 : 2304 + 64 * (wave_u & 1);
+                    dma16_m0(page + po * 1152, min(rc & 31u, nv1) * 1152u + (rc >> 5) * 16u, slot_lds + base_u * 16);
+                }
             }
         };
+        auto stage_slot = [&](int q) { return C::lowbit ? stages_lds + sofs[q] : tiles_lds + tofs[q]; };
         // prologue: the first D tiles
 #pragma unroll
         for (int j = 0; j < C::D; ++j) {
@@ -556,11 +628,12 @@ void decode_kernel(DecodeArgs a) {
                 const int t0 = t_begin + j * kTile;
                 const int pid = kRing ? 0 : load_page_id(bt, t0 / P);
 #pragma unroll
-                for (int k = 0; k < C::loads; ++k) issue(k, pid, t0, j);
+                for (int k = 0; k < C::loads; ++k) issue(k, pid, t0, t0 % P, stage_slot(j));
             }
         }
         int cur_t0 = t_begin + min(C::D, n_tiles - 1) * kTile;     // tile staged by the current step
         int cur_page = cur_t0 / P;
+        int cur_po = cur_t0 - cur_page * P;
 
         // per-lane addressing of the transposing V^T reads: lane (group g, index i)
         // supplies the address of tile row k0 + i/4, channels n0 + 4(i%4) .. +3
@@ -591,29 +664,32 @@ void decode_kernel(DecodeArgs a) {
                 else pid = step_barrier<C::loads>(bt, cur_page);
             }
             const int stage_j = it + C::D;
+            constexpr int kStageQ = C::D % (C::lowbit ? C::NS : C::NT);    // slot of tile it + D
 
-            f32x16 s = f32x16{};
+            f32x16 s;
             if constexpr (kQK) {
-                const uint8_t* kt = tiles + slot_offset(it, C::NT, kTileBytes);
+                const uint8_t* kt = tiles + tofs[0];
                 // every wave computes, also one whose rows all lie past the end
                 // (its results are never stored): a branch here would force the
                 // accumulators through a register-class join.
-                // Scores S^T[token][row], K = 576 in 36 steps, the operand reads
-                // kAhead steps ahead of the matrix instructions.  Low-bit: the 36
-                // pieces of the next tile's dequantization (reading staging slot
-                // (it+1) % NS, writing tile slot (it+1) % NT, which the aggregation
-                // of tile it-2 released before this step's barrier) fill the
-                // matrix pipe's shadow, one per k-step.
+                // Scores S^T[token][row], K = 576 in 36 steps, the operands read
+                // two k-steps ahead of the matrix instructions, in pairs: the pair
+                // (2p, 2p+1) is multiplied in the order 2p+1, 2p, so that one wait
+                // for the later read covers both.  Low-bit: the 36 pieces of the
+                // next tile's dequantization (reading the staging slot of tile
+                // it+1, writing its tile slot, which the aggregation of tile it-2
+                // released before this step's barrier) fill the matrix pipe's
+                // shadow, one per k-step.
                 Dq<kDqKind> dq;
-                uint8_t* next_tile = tiles + slot_offset(it + 1, C::NT, kTileBytes);
+                uint8_t* next_tile = tiles + tofs[1];
                 if constexpr (C::lowbit) {
-                    dq_read<kDqKind>(dq, stages + slot_offset(it + 1, C::NS, C::stage_bytes), tid);
+                    dq_read<kDqKind>(dq, stages + sofs[1], tid);
                     dq_split<kDqKind>(dq, 0);
                 }
                 // k-step kk reads logical chunk 2kk + half: physical 2kk + half (+ kk/4 grouped)
                 const uint8_t* krow = kt + row_off(C::SC, qk_row) + 16 * half;
                 auto kread_off = [](int kk) { return 16 * (2 * kk + (C::grouped ? kk >> 2 : 0)); };
-                constexpr int kAhead = 3;
+                constexpr int kAhead = 4;
                 OpT kb[kAhead];
 #pragma unroll
                 for (int j = 0; j < kAhead; ++j) kb[j] = *reinterpret_cast<const OpT*>(krow + kread_off(j));
@@ -623,11 +699,17 @@ void decode_kernel(DecodeArgs a) {
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int kk = 0; kk < kKSteps; ++kk) {
-                    s = mfma(kb[kk % kAhead], qf[kk], s);
-                    if (kk + kAhead < kKSteps) kb[kk % kAhead] = *reinterpret_cast<const OpT*>(krow + kread_off(kk + kAhead));
+                    const int ko = kk ^ 1;          // 2p+1 first, then 2p
+                    mfma_v(s, kb[ko % kAhead], qf[ko], kk == 0);
+                    if (kk & 1) {
+#pragma unroll
+                        for (int j = kk - 1; j <= kk; ++j)
+                            if (j + kAhead < kKSteps) kb[j % kAhead] = *reinterpret_cast<const OpT*>(krow + kread_off(j + kAhead));
+                    }
                     if constexpr (C::lowbit) dq_step<kDqKind>(dq, kk, next_tile, tid);
                     __builtin_amdgcn_sched_barrier(0);
                 }
+                score_ready(s);
                 if constexpr (C::lowbit) {
 #pragma unroll
                     for (int s = kKSteps; s < kKSteps + 3; ++s) dq_step<kDqKind>(dq, s, next_tile, tid);
@@ -709,7 +791,7 @@ void decode_kernel(DecodeArgs a) {
                 // that of row + 2 (tr_kbase < 8), of row + 16 that of the row;
                 // channels 32 m + tr_col ..: logical chunk 4m + (0..3), physical
                 // + m/2 in the grouped layout
-                const uint8_t* vt = tiles + slot_offset(it + C::NT - 1, C::NT, kTileBytes);
+                const uint8_t* vt = tiles + tofs[C::NT - 1];
                 const uint8_t* vbase = vt + row_off(C::SC, tr_kbase) + 2 * tr_col;
                 auto vread = [&](int stp) __attribute__((always_inline)) {
                     const int ks = stp >> 4, m = stp & 15;
@@ -718,22 +800,29 @@ void decode_kernel(DecodeArgs a) {
                     const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 16 * C::SC * 8 + 32));
                     return __builtin_bit_cast(OpT, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
                 };
-                constexpr int kVAhead = 2;
+                // operands read in pairs one pair ahead; the pair (2p, 2p+1) is
+                // multiplied in the order 2p+1, 2p (one wait covers both)
+                constexpr int kVAhead = 4;
                 OpT vb[kVAhead];
 #pragma unroll
                 for (int j = 0; j < kVAhead; ++j) vb[j] = vread(j);
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int stp = 0; stp < 32; ++stp) {
-                    const int m = stp & 15;
-                    acc[m] = mfma(vb[stp % kVAhead], pb_prev[stp >> 4], acc[m]);
-                    if (stp + kVAhead < 32) vb[stp % kVAhead] = vread(stp + kVAhead);
+                    const int so = stp ^ 1;
+                    const int m = so & 15;
+                    acc[m] = mfma(vb[so % kVAhead], pb_prev[so >> 4], acc[m]);
+                    if (stp & 1) {
+#pragma unroll
+                        for (int j = stp - 1; j <= stp; ++j)
+                            if (j + kVAhead < 32) vb[j % kVAhead] = vread(j + kVAhead);
+                    }
                     if constexpr (kQK) {
                         softmax_piece(stp);
                         // the staging of tile it+D, one load per kStageGap k-steps
                         const int k = (stp - kStageSlot0) / kStageGap;
                         if (stp >= kStageSlot0 && (stp - kStageSlot0) % kStageGap == 0 && k < C::loads)
-                            issue(k, pid, cur_t0, stage_j);
+                            issue(k, pid, cur_t0, cur_po, stage_slot(kStageQ));
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }
@@ -741,7 +830,7 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
                 for (int q = 0; q < 11; ++q) softmax_piece(q);
 #pragma unroll
-                for (int k = 0; k < C::loads; ++k) issue(k, pid, cur_t0, stage_j);
+                for (int k = 0; k < C::loads; ++k) issue(k, pid, cur_t0, cur_po, stage_slot(kStageQ));
             }
             if constexpr (kQK) {
                 pb_prev[0] = __builtin_bit_cast(OpT, make_uint4(pw[0], pw[1], pw[2], pw[3]));
@@ -751,8 +840,25 @@ void decode_kernel(DecodeArgs a) {
                 // advance the staging cursor (it stays on the last tile)
                 if (stage_j + 1 < n_tiles) {
                     cur_t0 += kTile;
-                    if (cur_t0 % P == 0) ++cur_page;
+                    cur_po += kTile;
+                    if (cur_po == P) {
+                        cur_po = 0;
+                        ++cur_page;
+                    }
                 }
+            }
+            // the buffer slots move on by one tile
+            {
+                const int t = tofs[0];
+#pragma unroll
+                for (int q = 0; q + 1 < C::NT; ++q) tofs[q] = tofs[q + 1];
+                tofs[C::NT - 1] = t;
+            }
+            if constexpr (C::NS > 1) {
+                const int t = sofs[0];
+#pragma unroll
+                for (int q = 0; q + 1 < C::NS; ++q) sofs[q] = sofs[q + 1];
+                sofs[C::NS - 1] = t;
             }
         };
 

@@ -59,6 +59,13 @@ __device__ __forceinline__ void dma16(const uint8_t* base, uint32_t voff, uint32
         : "memory");
 }
 
+// The same load with its LDS destination handed to the compiler as M0 (which
+// the compiler then sets and knows to be in use; the leading wait state covers
+// the M0 write before the load reads it).
+__device__ __forceinline__ void dma16_m0(const uint8_t* base, uint32_t voff, uint32_t lds) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(base), "{m0}"(lds) : "memory");
+}
+
 // 32-bit LDS address of a pointer into shared memory (uniform).
 __device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
     return __builtin_amdgcn_readfirstlane(
