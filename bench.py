@@ -41,12 +41,13 @@ def log(*a):
 
 def algorithmic_bytes(run) -> int:
     """HBM bytes one decode launch must move: every attended key once, queries,
-    and partials (written, then read by the combine) or the output."""
+    and the split partials (fp16 normalized latent, fp32 max and sum) or the
+    output."""
     keys = run.key_bytes()
     q = run.B * run.s_q * run.H * (512 + 64) * 2
     rows = run.B * run.s_q * run.H
     if run.split_tokens:
-        parts = run.num_splits * run.s_q * run.H * (512 + 2) * 4
+        parts = run.num_splits * run.s_q * run.H * (512 * 2 + 2 * 4)   # fp16 latent, fp32 max and sum
         return keys + q + parts
     return keys + q + rows * 512 * 2
 

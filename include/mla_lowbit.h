@@ -163,12 +163,14 @@ int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens
  * Split (split_tokens > 0): split_indptr (device, int32 [B+1]) and
  *   num_splits = split_indptr[B] come from mla_plan_splits; writes for every
  *   split j and row (i, h) the partials of Appendix C.5 "Global attention
- *   normalization", in natural-log units:
- *     part_m[j][i][h]    = max_t z_t over the split's visible keys
- *     part_s[j][i][h]    = sum_t e^{z_t - part_m}
- *     part_o[j][i][h][:] = sum_t e^{z_t - part_m} C_hat[t,:]
- *   (all fp32, device; a split with no visible key gives (-inf, 0, 0)); out
- *   and lse are not touched -- call mla_splitkv_combine.
+ *   normalization", in natural-log units, with the weighted sum stored
+ *   normalized by the split's own exponential sum:
+ *     part_m[j][i][h]    = max_t z_t over the split's visible keys      (fp32)
+ *     part_s[j][i][h]    = sum_t e^{z_t - part_m}                        (fp32)
+ *     part_o[j][i][h][:] = fp16( sum_t e^{z_t - part_m} C_hat[t,:] / part_s )
+ *   (device; a split with no visible key gives (-inf, 0, 0)); the paper's
+ *   unnormalized sum is part_s * part_o.  out and lse are not touched -- call
+ *   mla_splitkv_combine.
  * Scores and latent aggregation run as fp16 matrix products with fp32
  * accumulation: the dequantized cache (x_hat, one fp16 rounding) and the
  * softmax weights are fp16 operands, so queries and x_hat must lie within the
@@ -184,14 +186,15 @@ int mla_lowbit_decode_attn(const mla_cache_format* f,
                            float softmax_scale,
                            int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
                            uint16_t* out, float* lse,
-                           float* part_m, float* part_s, float* part_o,
+                           float* part_m, float* part_s, uint16_t* part_o,
                            hipStream_t stream);
 
 /*
  * Same computation over a BF16 cache (the unquantized comparison; row layout
  * in mla_bf16_page_bytes).  Arguments as for mla_lowbit_decode_attn.  The
  * products run in bf16 (cache rows and queries exact), the softmax weights
- * rounded to bf16.
+ * rounded to bf16.  With split partials, the cache values must lie within the
+ * fp16 range (part_o is fp16).
  */
 int mla_bf16_decode_attn(const mla_cache_format* f,
                          const uint16_t* q_lat, const uint16_t* q_rope,
@@ -201,19 +204,20 @@ int mla_bf16_decode_attn(const mla_cache_format* f,
                          float softmax_scale,
                          int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
                          uint16_t* out, float* lse,
-                         float* part_m, float* part_s, float* part_o,
+                         float* part_m, float* part_s, uint16_t* part_o,
                          hipStream_t stream);
 
 /*
  * Split-KV combine (Appendix C.5, "Global attention normalization"):
  *   m = max_j part_m[j],  s = sum_j e^{part_m[j]-m} part_s[j],
- *   out = (sum_j e^{part_m[j]-m} part_o[j]) / s  as bf16,  lse = m + ln s
+ *   out = (sum_j e^{part_m[j]-m} part_s[j] part_o[j]) / s  as bf16,
+ *   lse = m + ln s
  * over the splits j of each sequence; splits with part_m = -inf are skipped.
  *   part_*  device, as written by the decode call (num_splits = split_indptr[B])
  *   out     device, bf16 [B][s_q][H][d_c];  lse device fp32 [B][s_q][H] or NULL
  * Every row must have at least one split with a visible key.  B = 0 is a no-op.
  */
-int mla_splitkv_combine(const float* part_m, const float* part_s, const float* part_o,
+int mla_splitkv_combine(const float* part_m, const float* part_s, const uint16_t* part_o,
                         const int32_t* split_indptr, int32_t B, int32_t s_q, int32_t H,
                         int32_t d_c, uint16_t* out, float* lse, hipStream_t stream);
 
@@ -307,7 +311,7 @@ int mla_lowbit_decode_attn_protected(const mla_cache_format* f, const mla_protec
                                      const void* prot, int64_t num_prot, const int32_t* prot_slot,
                                      int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
                                      uint16_t* out, float* lse,
-                                     float* part_m, float* part_s, float* part_o,
+                                     float* part_m, float* part_s, uint16_t* part_o,
                                      hipStream_t stream);
 
 /*

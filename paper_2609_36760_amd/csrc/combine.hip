@@ -2,11 +2,12 @@
 // (Appendix C.5, "Global attention normalization"):
 //   m = max_j m_j,  s = sum_j e^{m_j - m} s_j,  O = (sum_j e^{m_j - m} o_j) / s,
 //   lse = m + ln s,
-// skipping splits with m_j = -inf (no visible key).
+// skipping splits with m_j = -inf (no visible key).  A split's aggregation is
+// stored normalized, u_j = o_j / s_j in fp16, so o_j = s_j u_j.
 //
 // One workgroup of 128 threads per output row (sequence, query token, head);
 // each thread owns 4 of the 512 latent channels, so every split's partial row
-// is read as one coalesced 2 KiB sweep.  The kernel is bound by HBM reads of
+// is read as one coalesced 1 KiB sweep.  The kernel is bound by HBM reads of
 // the partials.
 #include <hip/hip_runtime.h>
 
@@ -19,6 +20,7 @@ namespace {
 
 constexpr int kDc = 512;
 constexpr int kThreads = kDc / 4;
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -48,13 +50,14 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
         const int64_t pr = static_cast<int64_t>(j) * rows_per_seq + r;
         const float mj = a.part_m[pr];
         if (mj == -INFINITY) continue;
-        const float wgt = expf(mj - mx);
-        s += wgt * a.part_s[pr];
-        const float4 v = *reinterpret_cast<const float4*>(a.part_o + pr * kDc + threadIdx.x * 4);
-        o.x += wgt * v.x;
-        o.y += wgt * v.y;
-        o.z += wgt * v.z;
-        o.w += wgt * v.w;
+        const float ws = expf(mj - mx) * a.part_s[pr];
+        s += ws;
+        const uint2 u = *reinterpret_cast<const uint2*>(a.part_o + pr * kDc + threadIdx.x * 4);
+        const f16x2 u0 = __builtin_bit_cast(f16x2, u.x), u1 = __builtin_bit_cast(f16x2, u.y);
+        o.x += ws * static_cast<float>(u0[0]);
+        o.y += ws * static_cast<float>(u0[1]);
+        o.z += ws * static_cast<float>(u1[0]);
+        o.w += ws * static_cast<float>(u1[1]);
     }
     const float inv = s > 0.0f ? 1.0f / s : 0.0f;
     *reinterpret_cast<uint2*>(a.out + row * kDc + threadIdx.x * 4) =

@@ -473,19 +473,33 @@ void decode_kernel(DecodeArgs a) {
     if (w >= a.num_work) return;
 
     const int P = a.g.page_size;
-    int b, split = 0;
+    int b, split = 0, Lraw;
     if (a.split_tokens == 0) {
         b = w;
+        Lraw = a.seq_lens[b];
     } else {
-        int lo = 0, hi = a.B;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (a.split_indptr[mid] <= w) lo = mid; else hi = mid - 1;
+        // The sequence of work item w is the last b with split_indptr[b] <= w
+        // (the index is non-decreasing from 0): count those entries 64 at a
+        // time, one lane per entry, loading the lengths alongside, so that the
+        // search costs one round of loads instead of a chain of dependent ones.
+        int cnt = 0, start = 0;
+        Lraw = 0;
+        for (int base = 0; base <= a.B; base += 64) {
+            const int idx = base + lane;
+            const int ip = idx <= a.B ? a.split_indptr[idx] : 0x7FFFFFFF;
+            const int sl = idx < a.B ? a.seq_lens[idx] : 0;
+            const int c = __builtin_popcountll(__builtin_amdgcn_ballot_w64(ip <= w));
+            const int last = cnt + c - 1 - base;     // lane of the last such entry in this chunk
+            if (c > 0 && last >= 0 && last < 64) {
+                start = __builtin_amdgcn_readlane(ip, last);
+                Lraw = __builtin_amdgcn_readlane(sl, last);
+            }
+            cnt += c;
         }
-        b = lo < a.B ? lo : a.B - 1;
-        split = w - a.split_indptr[b];
+        b = min(cnt - 1, a.B - 1);
+        split = w - start;
     }
-    const int L = min(max(a.seq_lens[b], 0), a.max_pages * P);
+    const int L = min(max(Lraw, 0), a.max_pages * P);
     const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_pages;
 
     // this lane's query row
@@ -522,24 +536,6 @@ void decode_kernel(DecodeArgs a) {
         uint8_t* stages = smem + C::NT * kTileBytes;        // NS x stage_bytes (low-bit only)
         const int n_tiles = t_end > t_begin ? (t_end - t_begin + kTile - 1) / kTile : 0;
         (void)t_lo;
-
-        // queries as B operands: k-step kk holds channels 16kk + 8*half .. +8
-        OpT qf[kKSteps];
-        {
-            const int64_t qrow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
-            const uint16_t* ql = a.q_lat + qrow * kDc + 8 * half;
-            const uint16_t* qr = a.q_rope + qrow * 64 + 8 * half;
-#pragma unroll
-            for (int kk = 0; kk < kKSteps; ++kk) {
-                // rows past the end read row 0 of the sequence; they are never stored
-                const uint4 v = *reinterpret_cast<const uint4*>(kk < 32 ? ql + 16 * kk : qr + 16 * (kk - 32));
-                if constexpr (C::lowbit)
-                    qf[kk] = __builtin_bit_cast(f16x8, make_uint4(bf16x2_to_f16x2(v.x), bf16x2_to_f16x2(v.y),
-                                                                  bf16x2_to_f16x2(v.z), bf16x2_to_f16x2(v.w)));
-                else
-                    qf[kk] = __builtin_bit_cast(bf16x8, v);
-            }
-        }
 
         // Staging.  Step it stages tile it + D -- clamped to the last tile,
         // whose bytes then land once more in a free slot -- so that every step
@@ -621,16 +617,43 @@ void decode_kernel(DecodeArgs a) {
             }
         };
         auto stage_slot = [&](int q) { return C::lowbit ? stages_lds + sofs[q] : tiles_lds + tofs[q]; };
-        // prologue: the first D tiles
+        // prologue: the first D tiles (their page ids fetched together), then
+        // the queries, whose loads and conversion overlap the staging
+        static_assert(C::D <= 3, "prologue page ids");
+        {
+            int pids[3] = {0, 0, 0};
+            if constexpr (!kRing) {
+                auto pidx = [&](int j) { return (t_begin + (j < n_tiles ? j : 0) * kTile) / P; };
+                load_page_ids3(bt, pidx(0), pidx(1), pidx(2), pids[0], pids[1], pids[2]);
+            }
 #pragma unroll
-        for (int j = 0; j < C::D; ++j) {
-            if (j < n_tiles) {
-                const int t0 = t_begin + j * kTile;
-                const int pid = kRing ? 0 : load_page_id(bt, t0 / P);
+            for (int j = 0; j < C::D; ++j) {
+                if (j < n_tiles) {
+                    const int t0 = t_begin + j * kTile;
 #pragma unroll
-                for (int k = 0; k < C::loads; ++k) issue(k, pid, t0, t0 % P, stage_slot(j));
+                    for (int k = 0; k < C::loads; ++k) issue(k, pids[j], t0, t0 % P, stage_slot(j));
+                }
             }
         }
+
+        // queries as B operands: k-step kk holds channels 16kk + 8*half .. +8
+        OpT qf[kKSteps];
+        {
+            const int64_t qrow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
+            const uint16_t* ql = a.q_lat + qrow * kDc + 8 * half;
+            const uint16_t* qr = a.q_rope + qrow * 64 + 8 * half;
+#pragma unroll
+            for (int kk = 0; kk < kKSteps; ++kk) {
+                // rows past the end read row 0 of the sequence; they are never stored
+                const uint4 v = *reinterpret_cast<const uint4*>(kk < 32 ? ql + 16 * kk : qr + 16 * (kk - 32));
+                if constexpr (C::lowbit)
+                    qf[kk] = __builtin_bit_cast(f16x8, make_uint4(bf16x2_to_f16x2(v.x), bf16x2_to_f16x2(v.y),
+                                                                  bf16x2_to_f16x2(v.z), bf16x2_to_f16x2(v.w)));
+                else
+                    qf[kk] = __builtin_bit_cast(bf16x8, v);
+            }
+        }
+
         int cur_t0 = t_begin + min(C::D, n_tiles - 1) * kTile;     // tile staged by the current step
         int cur_page = cur_t0 / P;
         int cur_po = cur_t0 - cur_page * P;
@@ -926,41 +949,54 @@ void decode_kernel(DecodeArgs a) {
         }
     }
 
-    if (!row_ok) return;
+    // Epilogue.  A lane holds row (lane & 31) of its wave, channels 32 m +
+    // 8 q + 4 half .. +3 of the accumulators.  The rows go out through LDS so
+    // that each store writes one whole row (1 KiB, 64 lanes x 16 bytes) instead
+    // of 16-byte pieces of 32 rows: wave w stages its 32 rows at 1040-byte
+    // pitch (the 16-byte shift per row spreads the 32 rows of a write over the
+    // banks), then reads them back row by row.
     const float l_tot = sum_halves(l_run);
-    const int64_t orow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
-    if (a.split_tokens == 0) {
-        const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
-        uint16_t* op = a.out + orow * kDc + 4 * half;
+    const bool split_out = a.split_tokens != 0;
+    const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+    __syncthreads();        // every wave is done with the tiles (no staging load is in flight)
+    constexpr int kRowPitch = 1040;
+    static_assert(kWaves * 32 * kRowPitch <= kLds, "epilogue rows fit the LDS");
+    uint8_t* ep = smem + wave * 32 * kRowPitch;
 #pragma unroll
-        for (int m = 0; m < 16; ++m) {
+    for (int m = 0; m < 16; ++m) {
 #pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int c = 32 * m + 8 * q4;
-                *reinterpret_cast<uint2*>(op + c) =
-                    make_uint2(pack_bf16x2(acc[m][4 * q4] * inv, acc[m][4 * q4 + 1] * inv),
-                               pack_bf16x2(acc[m][4 * q4 + 2] * inv, acc[m][4 * q4 + 3] * inv));
-            }
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const float x0 = acc[m][4 * q4] * inv, x1 = acc[m][4 * q4 + 1] * inv;
+            const float x2 = acc[m][4 * q4 + 2] * inv, x3 = acc[m][4 * q4 + 3] * inv;
+            // partials: the split's normalized aggregation in fp16 (the combine
+            // weighs it by part_s); unsplit: the output in bf16
+            const uint2 u = split_out ? make_uint2(pack_f16x2(x0, x1), pack_f16x2(x2, x3))
+                                      : make_uint2(pack_bf16x2(x0, x1), pack_bf16x2(x2, x3));
+            *reinterpret_cast<uint2*>(ep + (lane & 31) * kRowPitch + 2 * (32 * m + 8 * q4 + 4 * half)) = u;
         }
-        if (a.lse != nullptr && half == 0)
+    }
+    // rows r = row block + 32 wave + i are (b, i, h) rows of the output, or of
+    // work item w's partials
+    const int row0 = rb * kRowsPerBlock + wave * 32;
+    uint16_t* dst = split_out ? a.part_o + (static_cast<int64_t>(w) * rows_total + row0) * kDc
+                              : a.out + (static_cast<int64_t>(b) * rows_total + row0) * kDc;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+        if (row0 + i < rows_total)
+            *reinterpret_cast<uint4*>(dst + i * kDc + 8 * lane) =
+                *reinterpret_cast<const uint4*>(ep + i * kRowPitch + 16 * lane);
+    }
+    if (!row_ok || half != 0) return;
+    if (!split_out) {
+        if (a.lse != nullptr) {
+            const int64_t orow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
             a.lse[orow] = l_tot > 0.0f ? (m_ref + log2f(l_tot)) * kLn2 : -INFINITY;
+        }
     } else {
         const int64_t prow = (static_cast<int64_t>(w) * a.s_q + qi) * a.H + h;
         const float f = m_true == -INFINITY ? 0.0f : exp2f(m_ref - m_true);
-        float* op = a.part_o + prow * kDc + 4 * half;
-#pragma unroll
-        for (int m = 0; m < 16; ++m) {
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int c = 32 * m + 8 * q4;
-                *reinterpret_cast<float4*>(op + c) = make_float4(acc[m][4 * q4] * f, acc[m][4 * q4 + 1] * f,
-                                                                 acc[m][4 * q4 + 2] * f, acc[m][4 * q4 + 3] * f);
-            }
-        }
-        if (half == 0) {
-            a.part_m[prow] = m_true * kLn2;
-            a.part_s[prow] = l_tot * f;
-        }
+        a.part_m[prow] = m_true * kLn2;
+        a.part_s[prow] = l_tot * f;
     }
 }
 

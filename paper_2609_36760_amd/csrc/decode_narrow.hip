@@ -520,11 +520,12 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
     } else {
         const int64_t prow = (static_cast<int64_t>(w) * a.s_q + qi) * a.H + h;
         const float f = m_true == -INFINITY ? 0.0f : exp2f(m_ref - m_true);
-        float* op = a.part_o + prow * kDc + 4 * g;
+        const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+        uint16_t* op = a.part_o + prow * kDc + 4 * g;
 #pragma unroll
         for (int m = 0; m < 32; ++m)
-            *reinterpret_cast<float4*>(op + 16 * m) =
-                make_float4(acc[m][0] * f, acc[m][1] * f, acc[m][2] * f, acc[m][3] * f);
+            *reinterpret_cast<uint2*>(op + 16 * m) =
+                make_uint2(pack_f16x2(acc[m][0] * inv, acc[m][1] * inv), pack_f16x2(acc[m][2] * inv, acc[m][3] * inv));
         if (g == 0) {
             a.part_m[prow] = m_true * kLn2;
             a.part_s[prow] = l_tot * f;

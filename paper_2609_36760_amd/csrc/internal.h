@@ -62,7 +62,7 @@ struct DecodeArgs {
     float* lse;
     float* part_m;
     float* part_s;
-    float* part_o;
+    uint16_t* part_o;       // fp16, normalized by part_s
     PageGeom g;             // for BF16: page_size and page_bytes only
     // BF16 protection (decode_kernel<KIND, true> only)
     const uint8_t* prot;    // protection buffers, num_prot x (sink + recent) rows of 1152 bytes
@@ -74,7 +74,7 @@ struct DecodeArgs {
 struct CombineArgs {
     const float* part_m;
     const float* part_s;
-    const float* part_o;
+    const uint16_t* part_o;
     const int32_t* split_indptr;
     int32_t B, s_q, H;
     uint16_t* out;

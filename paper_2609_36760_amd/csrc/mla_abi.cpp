@@ -148,7 +148,7 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
                   const void* cache, int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
                   const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H, float softmax_scale,
                   int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits, uint16_t* out,
-                  float* lse, float* part_m, float* part_s, float* part_o, const ProtDecode* pd,
+                  float* lse, float* part_m, float* part_s, uint16_t* part_o, const ProtDecode* pd,
                   hipStream_t stream) {
     int st = lowbit ? check_lowbit_format(f) : check_shape(f);
     if (st != MLA_OK) return st;
@@ -316,7 +316,7 @@ int mla_lowbit_decode_attn_protected(const mla_cache_format* f, const mla_protec
                                      float softmax_scale, const void* prot, int64_t num_prot,
                                      const int32_t* prot_slot, int32_t split_tokens, const int32_t* split_indptr,
                                      int32_t num_splits, uint16_t* out, float* lse, float* part_m, float* part_s,
-                                     float* part_o, hipStream_t stream) {
+                                     uint16_t* part_o, hipStream_t stream) {
     const ProtDecode pd{p, prot, num_prot, prot_slot};
     return decode_common(f, true, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
                          s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
@@ -342,7 +342,7 @@ int mla_lowbit_decode_attn(const mla_cache_format* f, const uint16_t* q_lat, con
                            int32_t max_pages_per_seq, const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
                            float softmax_scale, int32_t split_tokens, const int32_t* split_indptr,
                            int32_t num_splits, uint16_t* out, float* lse, float* part_m, float* part_s,
-                           float* part_o, hipStream_t stream) {
+                           uint16_t* part_o, hipStream_t stream) {
     return decode_common(f, true, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
                          s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
                          part_o, nullptr, stream);
@@ -352,13 +352,13 @@ int mla_bf16_decode_attn(const mla_cache_format* f, const uint16_t* q_lat, const
                          const void* cache, int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
                          const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H, float softmax_scale,
                          int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits, uint16_t* out,
-                         float* lse, float* part_m, float* part_s, float* part_o, hipStream_t stream) {
+                         float* lse, float* part_m, float* part_s, uint16_t* part_o, hipStream_t stream) {
     return decode_common(f, false, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
                          s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
                          part_o, nullptr, stream);
 }
 
-int mla_splitkv_combine(const float* part_m, const float* part_s, const float* part_o, const int32_t* split_indptr,
+int mla_splitkv_combine(const float* part_m, const float* part_s, const uint16_t* part_o, const int32_t* split_indptr,
                         int32_t B, int32_t s_q, int32_t H, int32_t d_c, uint16_t* out, float* lse,
                         hipStream_t stream) {
     if (B < 0 || d_c <= 0) return MLA_EINVAL;

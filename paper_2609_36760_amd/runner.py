@@ -80,7 +80,7 @@ class DecodeRun:
             R = self.s_q * self.H
             self.part_m = torch.empty(total * R, dtype=torch.float32, device=device)
             self.part_s = torch.empty(total * R, dtype=torch.float32, device=device)
-            self.part_o = torch.empty(total * R * 512, dtype=torch.float32, device=device)
+            self.part_o = torch.empty(total * R * 512, dtype=torch.float16, device=device)
         else:
             self.split_indptr = self.part_m = self.part_s = self.part_o = None
             self.num_splits = 0

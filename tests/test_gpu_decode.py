@@ -77,7 +77,7 @@ def test_split_partials_match_oracle_chunks():
     R = 2 * 128
     pm = run.part_m.cpu().numpy().reshape(-1, R)
     ps = run.part_s.cpu().numpy().reshape(-1, R)
-    po = run.part_o.cpu().numpy().reshape(-1, R, 512)
+    po = run.part_o.float().cpu().numpy().reshape(-1, R, 512)     # normalized by part_s
     from gpu_support import reconstructed_sequence
     for b in range(2):
         L = int(lens[b])
@@ -112,7 +112,7 @@ def test_split_partials_match_oracle_chunks():
             A = wts @ np.abs(c_hat[a:e].astype(np.float64))
             want = o[j][live] / s[j][live, None]
             tol = 1.25 * (2.0 ** -9 * np.abs(want) + (2.0 ** -8 + 2.1 * dz[live, None]) * A)
-            assert np.all(np.abs(go[live] / gs[live, None] - want) <= tol)
+            assert np.all(np.abs(go[live] - want) <= tol)
 
 
 def test_large_score_jump_rescale():
