@@ -78,9 +78,12 @@ typedef struct mla_cache_format {
  *          zero-points [8] (16-23), fp32 RoPE scale (24-27), byte RoPE
  *          zero-point (28), zero (29-31)
  * The page size is rounded up to 256 bytes; the cache is num_pages such
- * pages back to back from a 256-byte aligned base.  Inside a byte, codes are
- * little-endian fields: 4-bit channel 2j in bits 0-3 of byte j and 2j+1 in
- * bits 4-7; 2-bit channel 4j+k in bits 2k..2k+1.  Token t of page p is slot
+ * pages back to back from a 256-byte aligned base.  Codes form little-endian
+ * 32-bit words of 32/bits consecutive channels (8 at 4 bits, 16 at 2 bits);
+ * in a word, channel 2i occupies bits [bits*i, bits*(i+1)) and channel 2i+1
+ * the same bits of the upper 16-bit half, so that a decoder extracts a
+ * channel pair with one shift and one mask (a 4-bit word holds channels
+ * 0, 2, 4, 6 in bytes 0-1 and 1, 3, 5, 7 in bytes 2-3).  Token t of page p is slot
  * p*P + t.  For d_c=512, d_r=64, P=64: 20736 bytes per page with 4-bit
  * content (324 B/token), 12544 with 2-bit content (196 B/token); with the
  * paper's metadata 20480 (320 B/token, the paper's figure) and 12288.

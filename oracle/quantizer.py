@@ -116,29 +116,39 @@ def dequantize(q: np.ndarray, scale16: np.ndarray, zero16: np.ndarray) -> np.nda
 
 
 def pack_codes(q: np.ndarray, bits: int) -> np.ndarray:
-    """Pack integer codes along the last axis into bytes (little-endian fields)."""
+    """Pack integer codes along the last axis into little-endian 32-bit words of
+    32 / bits consecutive channels (the library's byte layout): of the channel
+    pair (2i, 2i+1) of a word, channel 2i occupies bits [bits*i, bits*(i+1))
+    of the word and channel 2i+1 the same bits of its upper 16-bit half."""
     q = np.asarray(q, dtype=np.uint8)
-    per = 8 // bits
+    per = 32 // bits
     if q.shape[-1] % per:
-        raise ValueError("channel count must fill whole bytes")
-    mask = np.uint8((1 << bits) - 1)
-    if np.any(q > mask):
+        raise ValueError("channel count must fill whole 32-bit words")
+    if np.any(q > (1 << bits) - 1):
         raise ValueError("code out of range")
-    q = q.reshape(q.shape[:-1] + (q.shape[-1] // per, per))
-    out = np.zeros(q.shape[:-1], dtype=np.uint8)
-    for k in range(per):
-        out |= (q[..., k] & mask) << np.uint8(bits * k)
-    return out
+    q = q.reshape(q.shape[:-1] + (q.shape[-1] // per, per)).astype(np.uint32)
+    word = np.zeros(q.shape[:-1], dtype=np.uint32)
+    for i in range(per // 2):
+        word |= q[..., 2 * i] << np.uint32(bits * i)
+        word |= q[..., 2 * i + 1] << np.uint32(16 + bits * i)
+    out = word.astype("<u4").view(np.uint8)
+    return out.reshape(q.shape[:-2] + (q.shape[-2] * 4,))
 
 
 def unpack_codes(packed: np.ndarray, bits: int) -> np.ndarray:
     """Inverse of :func:`pack_codes`."""
-    packed = np.asarray(packed, dtype=np.uint8)
-    per = 8 // bits
-    mask = np.uint8((1 << bits) - 1)
-    parts = [(packed >> np.uint8(bits * k)) & mask for k in range(per)]
-    out = np.stack(parts, axis=-1)
-    return out.reshape(packed.shape[:-1] + (packed.shape[-1] * per,))
+    packed = np.ascontiguousarray(np.asarray(packed, dtype=np.uint8))
+    if packed.shape[-1] % 4:
+        raise ValueError("packed codes come in whole 32-bit words")
+    word = packed.view("<u4").astype(np.uint32)
+    mask = np.uint32((1 << bits) - 1)
+    per = 32 // bits
+    parts = []
+    for i in range(per // 2):
+        parts.append((word >> np.uint32(bits * i)) & mask)
+        parts.append((word >> np.uint32(16 + bits * i)) & mask)
+    out = np.stack(parts, axis=-1).astype(np.uint8)
+    return out.reshape(word.shape[:-1] + (word.shape[-1] * per,))
 
 
 def quantize_token_path(x_bits: np.ndarray, bits: int, meta: str = "fp16", rope: bool = False):

@@ -304,13 +304,13 @@ __device__ __forceinline__ void stage_bf16(int k, const uint8_t* src, RowStart r
 // eight threads of a row and the row two further on share a 16-lane store
 // group (conflict-free in the grouped layout).
 //
-// The 36 fp16 pairs (chunk j, pair p; task 4j + p) go through four stages --
-// A unpack, B bias, C subtract the biased zero, D scale (and store the chunk
-// after its last pair) -- one stage per k-step of the score products, task t
-// in stage A at step t: a step runs four independent operations (stages of
-// four different tasks), which issue without waiting on each other while the
-// matrix pipe works.  Steps 0..38; the staged bytes are read, and chunk 0's
-// code word split, before step 0.
+// The 36 fp16 pairs (chunk j, pair p; task 4j + p) go through three stages --
+// A extract the pair as 1024 + q (shift, mask-and-or), B subtract the biased
+// zero, C scale (and store the chunk after its last pair) -- one stage per
+// k-step of the score products, task t in stage A at step t: a step runs
+// independent operations of three different tasks, which issue without
+// waiting on each other while the matrix pipe works.  Steps 0..37; the staged
+// bytes are read before step 0.
 __device__ __forceinline__ int dq_row(int tid) {
     const int g16 = tid >> 4;
     return 4 * (g16 >> 1) + (g16 & 1) + 2 * ((tid >> 3) & 1);
@@ -323,7 +323,6 @@ template <int KIND> struct Dq {
                                     // rmeta = fp32 scale bits, rzero)
     uint32_t rzero;
     f16x2 zz, ss, rz, rs;           // metadata as fp16 (zero + 1024, scale)
-    uint32_t lo[2], hi[2];          // nibbles of the 4-bit code words of chunks j (index j & 1)
     uint32_t pr[4];                 // pairs in flight (index task & 3)
     uint32_t o[4];                  // finished pairs of the chunk being stored
 };
@@ -358,26 +357,31 @@ __device__ __forceinline__ void dq_read(Dq<KIND>& d, const uint8_t* st, int tid)
 template <int KIND>
 __device__ __forceinline__ constexpr bool dq_is4(int j) { return Cfg<KIND>::cc == 256 || j == 8; }
 
+// Code word holding chunk j (8 channels): 4-bit content, one word per chunk;
+// 2-bit content, one word per two chunks; chunk 8 is the RoPE chunk (4-bit).
 template <int KIND>
 __device__ __forceinline__ uint32_t dq_word(const Dq<KIND>& d, int j) {
     if constexpr (Cfg<KIND>::cc == 256) {
         const uint32_t cw[9] = {d.c0.x, d.c0.y, d.c0.z, d.c0.w, d.c1.x, d.c1.y, d.c1.z, d.c1.w, d.rcode};
         return cw[j];
     } else {
-        // 2-bit codes: 8 per 16 bits
         const uint32_t cw[4] = {d.c0.x, d.c0.y, d.c0.z, d.c0.w};
-        return j < 8 ? cw[j >> 1] >> (16 * (j & 1)) : d.rcode;
+        return j < 8 ? cw[j >> 1] : d.rcode;
     }
 }
 
+// Pair p (channels 2p, 2p+1) of chunk j as fp16 bits 0x6400 | q = 1024 + q:
+// in the code layout a channel pair sits at one bit offset of the two 16-bit
+// halves of a word, so one shift and one mask-and-or extract it.
 template <int KIND>
-__device__ __forceinline__ void dq_split(Dq<KIND>& d, int j) {
-    if (dq_is4<KIND>(j)) {
-        const uint32_t w = dq_word<KIND>(d, j);
-        d.lo[j & 1] = w & 0x0F0F0F0Fu;          // channels 0, 2, 4, 6
-        d.hi[j & 1] = (w >> 4) & 0x0F0F0F0Fu;   // channels 1, 3, 5, 7
-    }
+__device__ __forceinline__ uint32_t dq_pair(const Dq<KIND>& d, int j, int p) {
+    const bool is4 = dq_is4<KIND>(j);
+    const int sh = is4 ? 4 * p : 8 * (j & 1) + 2 * p;
+    return and_or(dq_word<KIND>(d, j) >> sh, is4 ? 0x000F000Fu : 0x00030003u, 0x64006400u);
 }
+
+// Dequantization steps 0 .. kDqSteps - 1 (36 pairs through three stages).
+constexpr int kDqSteps = 38;
 
 template <int KIND>
 __device__ __forceinline__ void dq_step(Dq<KIND>& d, int s, uint8_t* tile, int tid) {
@@ -390,8 +394,8 @@ __device__ __forceinline__ void dq_step(Dq<KIND>& d, int s, uint8_t* tile, int t
             meta_to_f16(d.rmeta, d.rz, d.rs);
         }
     }
-    if (s >= 3 && s - 3 < 36) {                 // D: scale; store a finished chunk
-        const int t = s - 3, j = t >> 2, p = t & 3;
+    if (s >= 2 && s - 2 < 36) {                 // C: scale; store a finished chunk
+        const int t = s - 2, j = t >> 2, p = t & 3;
         d.o[p] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, d.pr[t & 3]) * (j < 8 ? d.ss : d.rs));
         if (p == 3) {
             const int row = dq_row(tid), part = tid & 7;
@@ -400,26 +404,13 @@ __device__ __forceinline__ void dq_step(Dq<KIND>& d, int s, uint8_t* tile, int t
                 make_uint4(d.o[0], d.o[1], d.o[2], d.o[3]);
         }
     }
-    if (s >= 2 && s - 2 < 36) {                 // C: (1024 + q) - (1024 + zero) = q - zero, exact
-        const int t = s - 2, j = t >> 2;
+    if (s >= 1 && s - 1 < 36) {                 // B: (1024 + q) - (1024 + zero) = q - zero, exact
+        const int t = s - 1, j = t >> 2;
         d.pr[t & 3] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, d.pr[t & 3]) - (j < 8 ? d.zz : d.rz));
     }
-    if (s >= 1 && s - 1 < 36) {                 // B: fp16 bits 0x6400 | q = 1024 + q
-        const int t = s - 1, j = t >> 2;
-        if (dq_is4<KIND>(j)) d.pr[t & 3] |= 0x64006400u;
-    }
-    if (s < 36) {                               // A: unpack pair p of chunk j
-        const int t = s, j = t >> 2, p = t & 3;
-        if (dq_is4<KIND>(j)) {
-            // bytes [lo.b_p, 0, hi.b_p, 0]: channels 2p, 2p+1
-            const uint32_t sel = static_cast<uint32_t>(p) | 0x0C000C00u | (static_cast<uint32_t>(4 + p) << 16);
-            d.pr[t & 3] = __builtin_amdgcn_perm(d.hi[j & 1], d.lo[j & 1], sel);
-        } else {
-            // channel 4i+k in bits 2k..2k+1 of byte i; pair p: channels 2p, 2p+1
-            const uint32_t w = dq_word<KIND>(d, j);
-            d.pr[t & 3] = ((w >> (4 * p)) & 3u) | (((w >> (4 * p + 2)) & 3u) << 16) | 0x64006400u;
-        }
-        if (p == 3 && j + 1 < 9) dq_split<KIND>(d, j + 1);
+    if (s < 36) {                               // A: extract pair p of chunk j
+        const int t = s;
+        d.pr[t & 3] = dq_pair<KIND>(d, t >> 2, t & 3);
     }
 }
 
@@ -427,9 +418,8 @@ template <int KIND>
 __device__ __forceinline__ void dequant_tile(const uint8_t* st, uint8_t* tile, int tid) {
     Dq<KIND> d;
     dq_read<KIND>(d, st, tid);
-    dq_split<KIND>(d, 0);
 #pragma unroll
-    for (int s = 0; s < 39; ++s) dq_step<KIND>(d, s, tile, tid);
+    for (int s = 0; s < kDqSteps; ++s) dq_step<KIND>(d, s, tile, tid);
 }
 
 // ---------------------------------------------------------------------------
@@ -707,7 +697,6 @@ void decode_kernel(DecodeArgs a) {
                 uint8_t* next_tile = tiles + tofs[1];
                 if constexpr (C::lowbit) {
                     dq_read<kDqKind>(dq, stages + sofs[1], tid);
-                    dq_split<kDqKind>(dq, 0);
                 }
                 // k-step kk reads logical chunk 2kk + half: physical 2kk + half (+ kk/4 grouped)
                 const uint8_t* krow = kt + row_off(C::SC, qk_row) + 16 * half;
@@ -735,7 +724,7 @@ void decode_kernel(DecodeArgs a) {
                 score_ready(s);
                 if constexpr (C::lowbit) {
 #pragma unroll
-                    for (int s = kKSteps; s < kKSteps + 3; ++s) dq_step<kDqKind>(dq, s, next_tile, tid);
+                    for (int s = kKSteps; s < kDqSteps; ++s) dq_step<kDqKind>(dq, s, next_tile, tid);
                 }
                 // rows see every key of the tile except in the last tile of the
                 // range or the tile holding the newest key (block-uniform test)

@@ -153,24 +153,18 @@ __device__ __forceinline__ void stage_narrow_bf16(int k, const uint8_t* src, Row
     dma16(src, row_start(min(r, nvalid - 1)) + 16 * col, lds + 64 * 16 * k);
 }
 
-// Dequantize 8 channels (one code word) into fp16: pairs (2p, 2p+1).
+// Dequantize 8 channels into fp16 pairs (2p, 2p+1).  In the code layout a
+// channel pair sits at one bit offset of the two 16-bit halves of a word: the
+// 8 channels are the word's pairs at bit offsets sh0 + CBITS p (a 4-bit word
+// holds exactly 8 channels, sh0 = 0; a 2-bit word 16, sh0 = 0 or 8).
 template <int CBITS>
-__device__ __forceinline__ f16x8 dequant8(uint32_t w, f16x2 zz, f16x2 ss) {
+__device__ __forceinline__ f16x8 dequant8(uint32_t w, int sh0, f16x2 zz, f16x2 ss) {
+    constexpr uint32_t kMask = CBITS == 4 ? 0x000F000Fu : 0x00030003u;
     uint32_t o[4];
-    if constexpr (CBITS == 4) {
-        const uint32_t lo = w & 0x0F0F0F0Fu, hi = (w >> 4) & 0x0F0F0F0Fu;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-            const uint32_t sel = static_cast<uint32_t>(p) | 0x0C000C00u | (static_cast<uint32_t>(4 + p) << 16);
-            const uint32_t b = __builtin_amdgcn_perm(hi, lo, sel) | 0x64006400u;   // 1024 + q
-            o[p] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, b) - zz) * ss);
-        }
-    } else {
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-            const uint32_t b = ((w >> (4 * p)) & 3u) | (((w >> (4 * p + 2)) & 3u) << 16) | 0x64006400u;
-            o[p] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, b) - zz) * ss);
-        }
+    for (int p = 0; p < 4; ++p) {
+        const uint32_t b = and_or(w >> (sh0 + CBITS * p), kMask, 0x64006400u);   // 1024 + q
+        o[p] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, b) - zz) * ss);
     }
     return __builtin_bit_cast(f16x8, make_uint4(o[0], o[1], o[2], o[3]));
 }
@@ -342,9 +336,9 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
                         words[kk] = *reinterpret_cast<const uint32_t*>(st + 16 * (C::u_rc + 16 * (kk - 16) + li) + 4 * g);
                     else if constexpr (C::cbits == 4)
                         words[kk] = *reinterpret_cast<const uint32_t*>(st + 16 * (16 * kk + li) + 4 * g);
-                    else
-                        words[kk] = *reinterpret_cast<const uint16_t*>(st + 16 * (16 * (kk >> 1) + li) + 8 * (kk & 1) +
-                                                                       2 * g);
+                    else    // channels 32 kk + 8 g ..: word 2 kk + g / 2, upper or lower 8 (sh0)
+                        words[kk] = *reinterpret_cast<const uint32_t*>(st + 16 * (16 * (kk >> 1) + li) + 8 * (kk & 1) +
+                                                                       4 * (g >> 1));
                 }
                 mc0 = *reinterpret_cast<const uint4*>(st + 16 * (C::u_mc + li));
                 mc1 = *reinterpret_cast<const uint4*>(st + 16 * (C::u_mc + 16 + li));
@@ -355,7 +349,7 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
                 if (kk >= 16) {
                     if constexpr (C::pmeta) pmeta_to_f16(__uint_as_float(mc1.z), mc1.w & 0xFFu, zz, ss);
                     else meta_to_f16(rmw, zz, ss);
-                    return dequant8<4>(words[kk], zz, ss);
+                    return dequant8<4>(words[kk], 0, zz, ss);
                 }
                 const int grp = kk >> 1;
                 if constexpr (C::pmeta) {
@@ -368,7 +362,7 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
                                                 : (grp < 6 ? (grp == 4 ? mc1.x : mc1.y) : (grp == 6 ? mc1.z : mc1.w));
                     meta_to_f16(mw, zz, ss);
                 }
-                return dequant8<C::cbits>(words[kk], zz, ss);
+                return dequant8<C::cbits>(words[kk], C::cbits == 4 ? 0 : 8 * (g & 1), zz, ss);
             };
             f16x8 kv[kQSteps];
             float p[4] = {0.0f, 0.0f, 0.0f, 0.0f};

@@ -66,6 +66,14 @@ __device__ __forceinline__ void dma16_m0(const uint8_t* base, uint32_t voff, uin
     asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(base), "{m0}"(lds) : "memory");
 }
 
+// (x & m) | o in one v_and_or_b32 (the compiler otherwise splits it in two
+// when both constants are literals); m is a scalar, o a vector register.
+__device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t m, uint32_t o) {
+    uint32_t r;
+    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "s"(m), "v"(o));
+    return r;
+}
+
 // 32-bit LDS address of a pointer into shared memory (uniform).
 __device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
     return __builtin_amdgcn_readfirstlane(

@@ -105,13 +105,22 @@ __global__ __launch_bounds__(kThreads) void lowbit_append_kernel(AppendArgs a) {
     // integer zero-point in [0, m]; "+ 0.0f" turns a -0 from rint into +0
     const float z = fminf(fmaxf(rintf(-lo / s), 0.0f), m) + 0.0f;
 
+    // Code layout: little-endian 32-bit words of 32 / bits consecutive
+    // channels; channel 2i of a word in bits [bits i, bits (i+1)), channel
+    // 2i+1 at the same place in the upper half (a decoder extracts a channel
+    // pair with one shift and one mask).  A lane's 8 channels fill a 4-bit
+    // word, or one half of each 16-bit half of a 2-bit word: the two lanes of
+    // a 2-bit word merge their parts.
     uint32_t packed = 0;
+    const int sh2 = 8 * (lig & 1);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const float t = __fadd_rn(__fdiv_rn(x[i], s), z);
         const uint32_t q = static_cast<uint32_t>(fminf(fmaxf(rintf(t), 0.0f), m));
-        packed |= q << (bits * i);
+        const int pos = bits == 4 ? 4 * (i >> 1) : sh2 + 2 * (i >> 1);
+        packed |= q << (pos + 16 * (i & 1));
     }
+    const uint32_t word2 = packed | static_cast<uint32_t>(__shfl_xor(static_cast<int>(packed), 1, kLanesPerGroup));
 
     const int64_t page = slot / a.g.page_size;
     const int64_t off = slot % a.g.page_size;
@@ -120,9 +129,8 @@ __global__ __launch_bounds__(kThreads) void lowbit_append_kernel(AppendArgs a) {
         *reinterpret_cast<uint32_t*>(base + a.g.off_cr + off * a.g.cr_bytes + lig * 4) = packed;
     } else if (CBITS == 4) {
         *reinterpret_cast<uint32_t*>(base + off * a.g.cc_bytes + g * 32 + lig * 4) = packed;
-    } else {
-        *reinterpret_cast<uint16_t*>(base + off * a.g.cc_bytes + g * 16 + lig * 2) =
-            static_cast<uint16_t>(packed);
+    } else if ((lig & 1) == 0) {
+        *reinterpret_cast<uint32_t*>(base + off * a.g.cc_bytes + g * 16 + lig * 2) = word2;
     }
     if (lig == 0) {
         if constexpr (kPaper) {

@@ -55,13 +55,27 @@ def test_hand_cases(case):
 
 @pytest.mark.parametrize("bits", [2, 4])
 def test_pack_unpack_all_bytes(bits):
-    every = np.arange(256, dtype=np.uint8)[None, :]
-    codes = qz.unpack_codes(every, bits)
-    assert codes.shape == (1, 256 * 8 // bits)
+    # every byte value in every byte position of a word, and random words
+    every = np.zeros((4, 256, 4), np.uint8)
+    for pos in range(4):
+        every[pos, :, pos] = np.arange(256)
+    rnd = np.random.default_rng(3).integers(0, 256, (512, 4), dtype=np.uint8)
+    packed = np.concatenate([every.reshape(1024, 4), rnd]).reshape(1, -1)
+    codes = qz.unpack_codes(packed, bits)
+    assert codes.shape == (1, packed.shape[1] * 8 // bits)
     assert codes.max() == (1 << bits) - 1
-    assert np.array_equal(qz.pack_codes(codes, bits), every)
-    # field order: the first code of each byte lives in its lowest bits
-    assert np.array_equal(codes[0, 0::8 // bits], every[0] & ((1 << bits) - 1))
+    assert np.array_equal(qz.pack_codes(codes, bits), packed)
+    # field order, written out per byte: byte 0 of a word holds the even
+    # channels 0, 2, .. (lowest bits first), byte 2 the odd channels 1, 3, ..
+    per = 32 // bits
+    words = codes.reshape(-1, per)
+    mask = (1 << bits) - 1
+    b = packed.reshape(-1, 4)
+    for k in range(8 // bits):
+        assert np.array_equal(words[:, 2 * k], (b[:, 0] >> (bits * k)) & mask)
+        assert np.array_equal(words[:, 2 * k + 1], (b[:, 2] >> (bits * k)) & mask)
+        assert np.array_equal(words[:, 2 * (k + 8 // bits)], (b[:, 1] >> (bits * k)) & mask)
+        assert np.array_equal(words[:, 2 * (k + 8 // bits) + 1], (b[:, 3] >> (bits * k)) & mask)
 
 
 @pytest.mark.parametrize("bits", [2, 4])
@@ -136,9 +150,9 @@ def test_page_write_places_hand_case_bytes():
     pc.write_tokens(cache, f, [slot, -1], np.vstack([to_bits(c), to_bits(c)]), np.vstack([to_bits(kr), to_bits(kr)]))
     base = 2 * f.page_bytes
     codes = cache[base + 5 * 256: base + 6 * 256]
-    assert codes[32:37].tobytes() == bytes.fromhex("f0886a7677")
+    assert codes[32:37].tobytes() == bytes.fromhex("806a8f7677")
     rope = cache[base + 16384 + 5 * 32: base + 16384 + 6 * 32]
-    assert rope[:2].tobytes() == bytes.fromhex("f055")
+    assert rope[:4].tobytes() == bytes.fromhex("50555f55")
     meta_c = cache[base + 18432 + 5 * 32: base + 18432 + 6 * 32].view("<u2")
     assert meta_c[2] == 0x3C00 and meta_c[3] == 0x4700            # group 1: scale 1, zero 7
     meta_r = cache[base + 20480 + 5 * 4: base + 20480 + 6 * 4].view("<u2")
