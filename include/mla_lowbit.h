@@ -17,6 +17,8 @@
  *     except a per-thread copy of the last HIP error.
  *   - bf16 tensors are passed as uint16_t bit patterns.  All tensors are dense
  *     and row-major in the index order given, unless a stride is an argument.
+ *     Query, output and partial tensors must be 16-byte aligned (else
+ *     MLA_ENOTSUP).
  *   - GPU work is enqueued on `stream` (0 = the null stream) and is
  *     asynchronous; no call synchronizes.
  *   - Arguments are validated on the host before any HIP call.  Return codes:

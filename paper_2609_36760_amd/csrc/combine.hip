@@ -5,10 +5,12 @@
 // skipping splits with m_j = -inf (no visible key).  A split's aggregation is
 // stored normalized, u_j = o_j / s_j in fp16, so o_j = s_j u_j.
 //
-// One workgroup of 128 threads per output row (sequence, query token, head);
-// each thread owns 4 of the 512 latent channels, so every split's partial row
-// is read as one coalesced 1 KiB sweep.  The kernel is bound by HBM reads of
-// the partials.
+// One wave per output row (sequence, query token, head), four rows per
+// workgroup; each lane owns 8 of the 512 latent channels, so a split's
+// partial row is one coalesced 1 KiB read (16 bytes per lane).  The kernel is
+// bound by the reads of the partials: every split's loads of a batch are
+// issued before any is used (an empty split holds zeros and its weight
+// e^{-inf} s = 0 vanishes, so no branch separates the loads).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -19,7 +21,8 @@ namespace mla {
 namespace {
 
 constexpr int kDc = 512;
-constexpr int kThreads = kDc / 4;
+constexpr int kRowsPerBlock = 4;
+constexpr int kBatch = 8;       // splits whose loads are in flight together
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -28,13 +31,16 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
-__global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
+__global__ __launch_bounds__(64 * kRowsPerBlock) void combine_kernel(CombineArgs a) {
     // rows (b * s_q + i) * H + h in 8 contiguous ranges, range x on XCD x
     // (block id mod 8), the XCD whose decode workgroups wrote most of them
     const int64_t rows_all = static_cast<int64_t>(a.B) * a.s_q * a.H;
-    const int64_t per_xcd = (rows_all + 7) / 8;
-    const int64_t row = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-    if (row >= rows_all) return;
+    const int64_t blocks_all = (rows_all + kRowsPerBlock - 1) / kRowsPerBlock;
+    const int64_t per_xcd = (blocks_all + 7) / 8;
+    const int64_t blk = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    const int lane = threadIdx.x & 63;
+    const int64_t row = blk * kRowsPerBlock + (threadIdx.x >> 6);
+    if (blk >= blocks_all || row >= rows_all) return;
     const int rows_per_seq = a.s_q * a.H;
     const int b = static_cast<int>(row / rows_per_seq);
     const int r = static_cast<int>(row % rows_per_seq);
@@ -45,24 +51,36 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
     for (int j = j0; j < j1; ++j) mx = fmaxf(mx, a.part_m[static_cast<int64_t>(j) * rows_per_seq + r]);
 
     float s = 0.0f;
-    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int j = j0; j < j1; ++j) {
-        const int64_t pr = static_cast<int64_t>(j) * rows_per_seq + r;
-        const float mj = a.part_m[pr];
-        if (mj == -INFINITY) continue;
-        const float ws = expf(mj - mx) * a.part_s[pr];
-        s += ws;
-        const uint2 u = *reinterpret_cast<const uint2*>(a.part_o + pr * kDc + threadIdx.x * 4);
-        const f16x2 u0 = __builtin_bit_cast(f16x2, u.x), u1 = __builtin_bit_cast(f16x2, u.y);
-        o.x += ws * static_cast<float>(u0[0]);
-        o.y += ws * static_cast<float>(u0[1]);
-        o.z += ws * static_cast<float>(u1[0]);
-        o.w += ws * static_cast<float>(u1[1]);
+    float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (mx != -INFINITY) {
+        for (int jb = j0; jb < j1; jb += kBatch) {
+            uint4 u[kBatch];
+            float ws[kBatch];
+#pragma unroll
+            for (int k = 0; k < kBatch; ++k) {
+                const int j = min(jb + k, j1 - 1);
+                const int64_t pr = static_cast<int64_t>(j) * rows_per_seq + r;
+                u[k] = *reinterpret_cast<const uint4*>(a.part_o + pr * kDc + lane * 8);
+                ws[k] = jb + k < j1 ? expf(a.part_m[pr] - mx) * a.part_s[pr] : 0.0f;
+            }
+#pragma unroll
+            for (int k = 0; k < kBatch; ++k) {
+                s += ws[k];
+                const uint32_t w4[4] = {u[k].x, u[k].y, u[k].z, u[k].w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const f16x2 h2 = __builtin_bit_cast(f16x2, w4[q]);
+                    o[2 * q] += ws[k] * static_cast<float>(h2[0]);
+                    o[2 * q + 1] += ws[k] * static_cast<float>(h2[1]);
+                }
+            }
+        }
     }
     const float inv = s > 0.0f ? 1.0f / s : 0.0f;
-    *reinterpret_cast<uint2*>(a.out + row * kDc + threadIdx.x * 4) =
-        make_uint2(pack_bf16x2(o.x * inv, o.y * inv), pack_bf16x2(o.z * inv, o.w * inv));
-    if (a.lse != nullptr && threadIdx.x == 0) a.lse[row] = s > 0.0f ? mx + logf(s) : -INFINITY;
+    *reinterpret_cast<uint4*>(a.out + row * kDc + lane * 8) =
+        make_uint4(pack_bf16x2(o[0] * inv, o[1] * inv), pack_bf16x2(o[2] * inv, o[3] * inv),
+                   pack_bf16x2(o[4] * inv, o[5] * inv), pack_bf16x2(o[6] * inv, o[7] * inv));
+    if (a.lse != nullptr && lane == 0) a.lse[row] = s > 0.0f ? mx + logf(s) : -INFINITY;
 }
 
 }  // namespace
@@ -70,7 +88,9 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(CombineArgs a) {
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
     const int64_t rows = static_cast<int64_t>(a.B) * a.s_q * a.H;
     if (rows == 0) return hipSuccess;
-    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((rows + 7) / 8 * 8)), dim3(kThreads), 0, stream, a);
+    const int64_t blocks = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
+    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((blocks + 7) / 8 * 8)), dim3(64 * kRowsPerBlock), 0,
+                       stream, a);
     return hipGetLastError();
 }
 

@@ -174,7 +174,7 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
     }
     if (split_tokens == 0) {
         if (out == nullptr) return MLA_EINVAL;
-        if (!aligned(out, 8)) return MLA_ENOTSUP;
+        if (!aligned(out, 16)) return MLA_ENOTSUP;
     } else {
         if (split_indptr == nullptr || part_m == nullptr || part_s == nullptr || part_o == nullptr || num_splits < 0)
             return MLA_EINVAL;
@@ -368,7 +368,7 @@ int mla_splitkv_combine(const float* part_m, const float* part_s, const uint16_t
     if (B == 0) return MLA_OK;   // nothing is read or written
     if (part_m == nullptr || part_s == nullptr || part_o == nullptr || split_indptr == nullptr || out == nullptr)
         return MLA_EINVAL;
-    if (!aligned(part_o, 16) || !aligned(out, 8)) return MLA_ENOTSUP;
+    if (!aligned(part_o, 16) || !aligned(out, 16)) return MLA_ENOTSUP;
     mla::CombineArgs a{};
     a.part_m = part_m;
     a.part_s = part_s;
