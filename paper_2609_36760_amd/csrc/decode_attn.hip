@@ -753,7 +753,8 @@ void decode_kernel(DecodeArgs a) {
             }
 
             // Softmax of tile it in pieces (interleaved with the aggregation of
-            // tile it-1 when there is one): 0-1 the tile maximum, 2 the reference
+            // tile it-1 when there is one, a piece every second product, the
+            // staging loads after them): 0-1 the tile maximum, 2 the reference
             // (a move reaches the accumulators in the next step), 3-10 the
             // weights, two per piece.
             float mr = -INFINITY, nref = 0.0f;
@@ -794,7 +795,7 @@ void decode_kernel(DecodeArgs a) {
                     asm volatile("" : "+v"(pw[v2]), "+v"(l_run));
                 }
             };
-            constexpr int kStageSlot0 = 12, kStageGap = C::lowbit ? 4 : 2;
+            constexpr int kStageSlot0 = C::lowbit ? 23 : 13, kStageGap = C::lowbit ? 3 : 2;
 
             if constexpr (kPV) {
                 // latent aggregation of tile it-1: O^T[channel][row] += V^T . P^T;
@@ -830,7 +831,7 @@ void decode_kernel(DecodeArgs a) {
                             if (j + kVAhead < 32) vb[j % kVAhead] = vread(j + kVAhead);
                     }
                     if constexpr (kQK) {
-                        softmax_piece(stp);
+                        if (stp % 2 == 0) softmax_piece(stp / 2);
                         // the staging of tile it+D, one load per kStageGap k-steps
                         const int k = (stp - kStageSlot0) / kStageGap;
                         if (stp >= kStageSlot0 && (stp - kStageSlot0) % kStageGap == 0 && k < C::loads)
