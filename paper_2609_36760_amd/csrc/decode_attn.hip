@@ -607,9 +607,19 @@ void decode_kernel(DecodeArgs a) {
             }
         };
         auto stage_slot = [&](int q) { return C::lowbit ? stages_lds + sofs[q] : tiles_lds + tofs[q]; };
-        // prologue: the first D tiles (their page ids fetched together), then
-        // the queries, whose loads and conversion overlap the staging
+        // prologue: the queries' loads, then the first D tiles (their page ids
+        // fetched together) while the queries are in flight, then the queries'
+        // conversion (rows past the end read row 0 of the sequence; they are
+        // never stored)
         static_assert(C::D <= 3, "prologue page ids");
+        const int64_t qrow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
+        uint4 rawq[kKSteps];
+        {
+            const uint16_t* ql = a.q_lat + qrow * kDc + 8 * half;
+            const uint16_t* qr = a.q_rope + qrow * 64 + 8 * half;
+#pragma unroll
+            for (int kk = 0; kk < kKSteps; ++kk) rawq[kk] = *reinterpret_cast<const uint4*>(kk < 32 ? ql + 16 * kk : qr + 16 * (kk - 32));
+        }
         {
             int pids[3] = {0, 0, 0};
             if constexpr (!kRing) {
@@ -629,13 +639,9 @@ void decode_kernel(DecodeArgs a) {
         // queries as B operands: k-step kk holds channels 16kk + 8*half .. +8
         OpT qf[kKSteps];
         {
-            const int64_t qrow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
-            const uint16_t* ql = a.q_lat + qrow * kDc + 8 * half;
-            const uint16_t* qr = a.q_rope + qrow * 64 + 8 * half;
 #pragma unroll
             for (int kk = 0; kk < kKSteps; ++kk) {
-                // rows past the end read row 0 of the sequence; they are never stored
-                const uint4 v = *reinterpret_cast<const uint4*>(kk < 32 ? ql + 16 * kk : qr + 16 * (kk - 32));
+                const uint4 v = rawq[kk];
                 if constexpr (C::lowbit)
                     qf[kk] = __builtin_bit_cast(f16x8, make_uint4(bf16x2_to_f16x2(v.x), bf16x2_to_f16x2(v.y),
                                                                   bf16x2_to_f16x2(v.z), bf16x2_to_f16x2(v.w)));
