@@ -68,32 +68,35 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
     log(f"[{name} {kind}] setup {time.perf_counter() - t0:.1f}s, cache {run.cache.numel() / 1e6:.1f} MB x {layers}")
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
-    dec = mb.mla_lowbit_decode_attn if kind == "lowbit" else mb.mla_bf16_decode_attn
-    app = mb.mla_lowbit_quant_append if kind == "lowbit" else mb.mla_bf16_append
+
+    fused = mb.mla_lowbit_append_decode_attn if kind == "lowbit" else mb.mla_bf16_append_decode_attn
 
     def one_step(i, ev=None):
         cache, prot = caches[i % layers], prots[i % layers]
         if protect is None:
-            app(run.fmt, run.new_c, run.new_k, run.new_slots, cache, run.num_pages, stream=sh)
+            # the append runs inside the decode launch (the same cache bytes and
+            # outputs as the writer launch followed by the decode)
+            if ev is not None:
+                ev[0].record(stream)
+            fused(run.fmt, run.new_c, run.new_k, run.new_slots, run.q_lat, run.q_rope, cache, run.num_pages,
+                  run.block_table, run.seq_lens, run.s_q, run.H, run.tau, split_tokens=run.split_tokens,
+                  split_indptr=run.split_indptr, num_splits=run.num_splits, out=run.out, lse=run.lse,
+                  part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
+            if ev is not None:
+                ev[1].record(stream)
         else:
             mb.mla_lowbit_quant_append_protected(run.fmt, protect, run.new_c, run.new_k, run.new_slots, cache,
                                                  run.num_pages, run.new_seq, run.new_pos, run.seq_lens,
                                                  run.prot_slot, prot, run.num_prot, stream=sh)
-        if ev is not None:
-            ev[0].record(stream)
-        if protect is None:
-            dec(run.fmt, run.q_lat, run.q_rope, cache, run.num_pages, run.block_table, run.seq_lens, run.s_q,
-                run.H, run.tau, split_tokens=run.split_tokens, split_indptr=run.split_indptr,
-                num_splits=run.num_splits, out=run.out, lse=run.lse, part_m=run.part_m, part_s=run.part_s,
-                part_o=run.part_o, stream=sh)
-        else:
+            if ev is not None:
+                ev[0].record(stream)
             mb.mla_lowbit_decode_attn_protected(
                 run.fmt, protect, run.q_lat, run.q_rope, cache, run.num_pages, run.block_table, run.seq_lens,
                 run.s_q, run.H, run.tau, prot, run.num_prot, run.prot_slot, split_tokens=run.split_tokens,
                 split_indptr=run.split_indptr, num_splits=run.num_splits, out=run.out, lse=run.lse,
                 part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
-        if ev is not None:
-            ev[1].record(stream)
+            if ev is not None:
+                ev[1].record(stream)
         if run.split_tokens:
             mb.mla_splitkv_combine(run.part_m, run.part_s, run.part_o, run.split_indptr, run.B, run.s_q, run.H,
                                    run.out, run.lse, stream=sh)

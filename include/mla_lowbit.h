@@ -213,6 +213,48 @@ int mla_bf16_decode_attn(const mla_cache_format* f,
                          hipStream_t stream);
 
 /*
+ * The step's append and decode in one call (Appendix C.5, "Cache update and
+ * tile reuse": the writer's quantization and insertion, then the fused
+ * decode): equivalent to mla_lowbit_quant_append (or mla_bf16_append) of the
+ * n = B * s_q new tokens followed by mla_lowbit_decode_attn (or
+ * mla_bf16_decode_attn), with identical cache bytes and outputs.  New token
+ * (b, i), row b * s_q + i of c_kv / k_rope (bf16, strides as for the append),
+ * is position seq_lens[b] - s_q + i of sequence b and is written at slot
+ * slot_mapping[b * s_q + i] (device, int64; < 0 skips the token), which must
+ * be that position's slot under block_table (a device-resident precondition).
+ * For s_q * H > 32 the writer runs inside the decode launch: the workgroups
+ * that read a new token's tile quantize and store it first.  Otherwise the
+ * writer is launched separately first.  Arguments and errors as for the two
+ * calls.
+ */
+int mla_lowbit_append_decode_attn(const mla_cache_format* f,
+                                  const uint16_t* c_kv, int64_t c_kv_stride,
+                                  const uint16_t* k_rope, int64_t k_rope_stride,
+                                  const int64_t* slot_mapping,
+                                  const uint16_t* q_lat, const uint16_t* q_rope,
+                                  void* cache, int64_t num_pages,
+                                  const int32_t* block_table, int32_t max_pages_per_seq,
+                                  const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
+                                  float softmax_scale,
+                                  int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
+                                  uint16_t* out, float* lse,
+                                  float* part_m, float* part_s, uint16_t* part_o,
+                                  hipStream_t stream);
+int mla_bf16_append_decode_attn(const mla_cache_format* f,
+                                const uint16_t* c_kv, int64_t c_kv_stride,
+                                const uint16_t* k_rope, int64_t k_rope_stride,
+                                const int64_t* slot_mapping,
+                                const uint16_t* q_lat, const uint16_t* q_rope,
+                                void* cache, int64_t num_pages,
+                                const int32_t* block_table, int32_t max_pages_per_seq,
+                                const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
+                                float softmax_scale,
+                                int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
+                                uint16_t* out, float* lse,
+                                float* part_m, float* part_s, uint16_t* part_o,
+                                hipStream_t stream);
+
+/*
  * Split-KV combine (Appendix C.5, "Global attention normalization"):
  *   m = max_j part_m[j],  s = sum_j e^{part_m[j]-m} part_s[j],
  *   out = (sum_j e^{part_m[j]-m} part_s[j] part_o[j]) / s  as bf16,

@@ -23,6 +23,7 @@ SYMBOLS = (
     "mla_plan_splits", "mla_lowbit_decode_attn", "mla_bf16_decode_attn", "mla_splitkv_combine",
     "mla_status_str", "mla_last_hip_error", "mla_protect_buffer_bytes", "mla_lowbit_quant_append_protected",
     "mla_plan_splits_protected", "mla_lowbit_decode_attn_protected", "mla_persistent_cache_bytes",
+    "mla_lowbit_append_decode_attn", "mla_bf16_append_decode_attn",
 )
 
 
@@ -83,6 +84,10 @@ def library() -> ctypes.CDLL:
         "mla_bf16_decode_attn": (ctypes.c_int, [FMT, P, P, P, I64, P, I32, P, I32, I32, I32, F32,
                                                 I32, P, I32, P, P, P, P, P, P]),
         "mla_splitkv_combine": (ctypes.c_int, [P, P, P, P, I32, I32, I32, I32, P, P, P]),
+        "mla_lowbit_append_decode_attn": (ctypes.c_int, [FMT, P, I64, P, I64, P, P, P, P, I64, P, I32, P, I32, I32,
+                                                         I32, F32, I32, P, I32, P, P, P, P, P, P]),
+        "mla_bf16_append_decode_attn": (ctypes.c_int, [FMT, P, I64, P, I64, P, P, P, P, I64, P, I32, P, I32, I32,
+                                                       I32, F32, I32, P, I32, P, P, P, P, P, P]),
         "mla_protect_buffer_bytes": (I64, [FMT, POL]),
         "mla_persistent_cache_bytes": (I64, [FMT, POL, I64]),
         "mla_lowbit_quant_append_protected": (ctypes.c_int, [FMT, POL, P, I64, P, I64, P, I32, P, I64,
@@ -183,6 +188,37 @@ def mla_bf16_decode_attn(fmt, q_lat, q_rope, cache, num_pages, block_table, seq_
                          lse=None, part_m=None, part_s=None, part_o=None, stream=None):
     _decode("mla_bf16_decode_attn", fmt, q_lat, q_rope, cache, num_pages, block_table, seq_lens, s_q, H,
             softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s, part_o, stream)
+
+
+def _append_decode(name, fmt, c_kv, k_rope, slot_mapping, q_lat, q_rope, cache, num_pages, block_table, seq_lens,
+                   s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s, part_o,
+                   stream):
+    B = q_lat.shape[0]
+    fn = getattr(library(), name)
+    _check(name, fn(ctypes.byref(fmt), _ptr(c_kv), c_kv.stride(0), _ptr(k_rope), k_rope.stride(0),
+                    _ptr(slot_mapping), _ptr(q_lat), _ptr(q_rope), _ptr(cache), num_pages,
+                    _ptr(block_table), block_table.shape[1], _ptr(seq_lens), B, s_q, H,
+                    float(softmax_scale), split_tokens, _ptr(split_indptr), num_splits,
+                    _ptr(out), _ptr(lse), _ptr(part_m), _ptr(part_s), _ptr(part_o), _stream(stream)))
+
+
+def mla_lowbit_append_decode_attn(fmt, c_kv, k_rope, slot_mapping, q_lat, q_rope, cache, num_pages, block_table,
+                                  seq_lens, s_q, H, softmax_scale, split_tokens=0, split_indptr=None,
+                                  num_splits=0, out=None, lse=None, part_m=None, part_s=None, part_o=None,
+                                  stream=None):
+    """The step's new tokens (rows b * s_q + i of c_kv / k_rope) appended, then decode."""
+    _append_decode("mla_lowbit_append_decode_attn", fmt, c_kv, k_rope, slot_mapping, q_lat, q_rope, cache,
+                   num_pages, block_table, seq_lens, s_q, H, softmax_scale, split_tokens, split_indptr, num_splits,
+                   out, lse, part_m, part_s, part_o, stream)
+
+
+def mla_bf16_append_decode_attn(fmt, c_kv, k_rope, slot_mapping, q_lat, q_rope, cache, num_pages, block_table,
+                                seq_lens, s_q, H, softmax_scale, split_tokens=0, split_indptr=None,
+                                num_splits=0, out=None, lse=None, part_m=None, part_s=None, part_o=None,
+                                stream=None):
+    _append_decode("mla_bf16_append_decode_attn", fmt, c_kv, k_rope, slot_mapping, q_lat, q_rope, cache,
+                   num_pages, block_table, seq_lens, s_q, H, softmax_scale, split_tokens, split_indptr, num_splits,
+                   out, lse, part_m, part_s, part_o, stream)
 
 
 def mla_splitkv_combine(part_m, part_s, part_o, split_indptr, B, s_q, H, out, lse=None, stream=None):

@@ -73,6 +73,7 @@
 
 #include "internal.h"
 #include "kernel_common.h"
+#include "writer_common.h"
 
 namespace mla {
 namespace {
@@ -420,6 +421,52 @@ __device__ __forceinline__ void dequant_tile(const uint8_t* st, uint8_t* tile, i
     dq_read<KIND>(d, st, tid);
 #pragma unroll
     for (int s = 0; s < kDqSteps; ++s) dq_step<KIND>(d, s, tile, tid);
+}
+
+// ---------------------------------------------------------------------------
+// In-launch append (the writer of mla_lowbit_quant_append / mla_bf16_append
+// for the step's new tokens, run by the decode workgroups that read them).
+// Token (b, i) sits at position L - s_q + i; the workgroup whose key range
+// holds that position writes it (72 threads per token: 8 per group of 64
+// channels, 9 groups; BF16: 72 16-byte pieces of the row) before its tile is
+// staged.  A tile is read only by the work item that owns it, so no other
+// workgroup waits for the write: every row block of a work item writes the
+// same bytes itself.  The stores are older than every staging load of the
+// work item, so the counted wait at the barrier before a tile's staging covers
+// them; a tile staged in the prologue waits for them explicitly first.
+template <int KIND>
+__device__ __forceinline__ void append_in_launch(const DecodeArgs& a, int b, int L, int t_begin, int t_end,
+                                                 int tid) {
+    using C = Cfg<KIND>;
+    constexpr int kDpro = C::D;                 // tiles staged in the prologue
+    bool early = false;
+    for (int i = 0; i < a.s_q; ++i) {
+        const int pos = L - a.s_q + i;
+        if (pos >= t_begin && pos < t_end && (pos - t_begin) / kTile < kDpro) early = true;
+    }
+    const int i = tid / 72, r = tid % 72;
+    const int pos = L - a.s_q + i;
+    if (i < a.s_q && pos >= 0 && pos >= t_begin && pos < t_end) {
+        const int64_t tok = static_cast<int64_t>(b) * a.s_q + i;
+        const int64_t slot = a.new_slots[tok];
+        const int64_t num_slots = a.num_pages * a.g.page_size;
+        if (slot >= 0 && slot < num_slots) {
+            uint8_t* base = const_cast<uint8_t*>(a.cache) + slot / a.g.page_size * a.g.page_bytes;
+            const int64_t off = slot % a.g.page_size;
+            const bool rope = r >= 64;
+            const uint16_t* src = rope ? a.new_k + tok * a.new_k_stride + (r - 64) * 8
+                                       : a.new_c + tok * a.new_c_stride + r * 8;
+            const uint4 raw = *reinterpret_cast<const uint4*>(src);
+            if constexpr (C::lowbit)
+                wc::quantize_store<C::cc == 256 ? 4 : 2, C::pmeta>(raw, rope, r >> 3, r & 7, base, off, a.g);
+            else
+                *reinterpret_cast<uint4*>(base + off * 1152 + r * 16) = raw;
+        }
+    }
+    if (early) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -904,6 +951,7 @@ void decode_kernel(DecodeArgs a) {
         }
         const int lim = row_ok ? min(L - a.s_q + qi + 1, t_end) : t_begin;   // keys t < lim are visible
         const int full_lim = min(L - a.s_q + 1, t_end);    // every valid row sees keys t < full_lim
+        if (a.new_c != nullptr) append_in_launch<KIND>(a, b, L, t_begin, t_end, tid);
         run(std::integral_constant<int, KIND>{}, std::false_type{}, t_begin, t_end, t_begin, lim, full_lim);
     } else {
         const int sink = a.sink, recent = a.recent;

@@ -69,6 +69,15 @@ struct DecodeArgs {
     int64_t num_prot;
     const int32_t* prot_slot;   // [B] buffer of each sequence
     int32_t sink, recent;
+    // In-launch append (decode_kernel<KIND, false> only; new_c == nullptr: none):
+    // token (b, i) of [B][s_q], position seq_lens[b] - s_q + i of sequence b,
+    // quantized (or copied, BF16) into slot new_slots[b * s_q + i] before it is
+    // read.
+    const uint16_t* new_c;
+    int64_t new_c_stride;
+    const uint16_t* new_k;
+    int64_t new_k_stride;
+    const int64_t* new_slots;
 };
 
 struct CombineArgs {

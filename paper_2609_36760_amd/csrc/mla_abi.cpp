@@ -144,12 +144,20 @@ int append_common(const mla_cache_format* f, bool lowbit, const uint16_t* c_kv, 
     return hip_status(lowbit ? mla::launch_lowbit_append(a, stream) : mla::launch_bf16_append(a, stream));
 }
 
+struct NewTokens {
+    const uint16_t* c_kv;
+    int64_t c_kv_stride;
+    const uint16_t* k_rope;
+    int64_t k_rope_stride;
+    const int64_t* slot_mapping;
+};
+
 int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat, const uint16_t* q_rope,
                   const void* cache, int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
                   const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H, float softmax_scale,
                   int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits, uint16_t* out,
                   float* lse, float* part_m, float* part_s, uint16_t* part_o, const ProtDecode* pd,
-                  hipStream_t stream) {
+                  hipStream_t stream, const NewTokens* nt = nullptr) {
     int st = lowbit ? check_lowbit_format(f) : check_shape(f);
     if (st != MLA_OK) return st;
     if (pd != nullptr) {
@@ -206,6 +214,20 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
                                 : f->c_bits == 4 ? (paper ? mla::KIND_C4R4P : mla::KIND_C4R4)
                                                  : (paper ? mla::KIND_C2R4P : mla::KIND_C2R4);
     const bool narrow = s_q * H <= mla::kNarrowRows;
+    if (nt != nullptr && B > 0) {
+        if (narrow) {
+            // few query rows: the writer runs as its own launch first
+            st = append_common(f, lowbit, nt->c_kv, nt->c_kv_stride, nt->k_rope, nt->k_rope_stride,
+                               nt->slot_mapping, B * s_q, const_cast<void*>(cache), num_pages, stream);
+            if (st != MLA_OK) return st;
+        } else {
+            a.new_c = nt->c_kv;
+            a.new_c_stride = nt->c_kv_stride;
+            a.new_k = nt->k_rope;
+            a.new_k_stride = nt->k_rope_stride;
+            a.new_slots = nt->slot_mapping;
+        }
+    }
     if (pd == nullptr)
         return hip_status(narrow ? mla::launch_decode_narrow(kind, a, stream) : mla::launch_decode(kind, a, stream));
     a.prot = static_cast<const uint8_t*>(pd->prot);
@@ -218,6 +240,24 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
 }
 
 }  // namespace
+
+// Append the step's new tokens, then decode (one launch for the wide kernel).
+static int append_decode(const mla_cache_format* f, bool lowbit, const uint16_t* c_kv, int64_t c_kv_stride,
+                  const uint16_t* k_rope, int64_t k_rope_stride, const int64_t* slot_mapping, const uint16_t* q_lat,
+                  const uint16_t* q_rope, void* cache, int64_t num_pages, const int32_t* block_table,
+                  int32_t max_pages_per_seq, const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
+                  float softmax_scale, int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
+                  uint16_t* out, float* lse, float* part_m, float* part_s, uint16_t* part_o, hipStream_t stream) {
+    int st = lowbit ? check_lowbit_format(f) : check_shape(f);
+    if (st != MLA_OK) return st;
+    if (B < 0 || s_q < 0) return MLA_EINVAL;
+    st = check_append(c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, B * s_q, cache, num_pages);
+    if (st != MLA_OK) return st;
+    const NewTokens nt{c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping};
+    return decode_common(f, lowbit, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
+                         s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
+                         part_o, nullptr, stream, &nt);
+}
 
 extern "C" {
 
@@ -356,6 +396,30 @@ int mla_bf16_decode_attn(const mla_cache_format* f, const uint16_t* q_lat, const
     return decode_common(f, false, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
                          s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
                          part_o, nullptr, stream);
+}
+
+int mla_lowbit_append_decode_attn(const mla_cache_format* f, const uint16_t* c_kv, int64_t c_kv_stride,
+                                  const uint16_t* k_rope, int64_t k_rope_stride, const int64_t* slot_mapping,
+                                  const uint16_t* q_lat, const uint16_t* q_rope, void* cache, int64_t num_pages,
+                                  const int32_t* block_table, int32_t max_pages_per_seq, const int32_t* seq_lens,
+                                  int32_t B, int32_t s_q, int32_t H, float softmax_scale, int32_t split_tokens,
+                                  const int32_t* split_indptr, int32_t num_splits, uint16_t* out, float* lse,
+                                  float* part_m, float* part_s, uint16_t* part_o, hipStream_t stream) {
+    return append_decode(f, true, c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, q_lat, q_rope, cache,
+                         num_pages, block_table, max_pages_per_seq, seq_lens, B, s_q, H, softmax_scale, split_tokens,
+                         split_indptr, num_splits, out, lse, part_m, part_s, part_o, stream);
+}
+
+int mla_bf16_append_decode_attn(const mla_cache_format* f, const uint16_t* c_kv, int64_t c_kv_stride,
+                                const uint16_t* k_rope, int64_t k_rope_stride, const int64_t* slot_mapping,
+                                const uint16_t* q_lat, const uint16_t* q_rope, void* cache, int64_t num_pages,
+                                const int32_t* block_table, int32_t max_pages_per_seq, const int32_t* seq_lens,
+                                int32_t B, int32_t s_q, int32_t H, float softmax_scale, int32_t split_tokens,
+                                const int32_t* split_indptr, int32_t num_splits, uint16_t* out, float* lse,
+                                float* part_m, float* part_s, uint16_t* part_o, hipStream_t stream) {
+    return append_decode(f, false, c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, q_lat, q_rope, cache,
+                         num_pages, block_table, max_pages_per_seq, seq_lens, B, s_q, H, softmax_scale, split_tokens,
+                         split_indptr, num_splits, out, lse, part_m, part_s, part_o, stream);
 }
 
 int mla_splitkv_combine(const float* part_m, const float* part_s, const uint16_t* part_o, const int32_t* split_indptr,

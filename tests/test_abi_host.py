@@ -32,7 +32,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(mb):
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 17
     lib = ctypes.CDLL(mb.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -207,3 +207,29 @@ def test_persistent_cache_bytes_reproduce_the_printed_ratios(mb):
     assert mb.mla_persistent_cache_bytes(paper, pol, -1) == -1
     assert mb.mla_persistent_cache_bytes(bf16, pol, 10) == -1
     assert mb.mla_persistent_cache_bytes(mb.cache_format(c_bits=3), None, 10) == -1
+
+
+def _append_decode_status(mb, **over):
+    lib = mb.library()
+    fmt = mb.cache_format()
+    args = dict(c_kv=16, c_stride=512, k_rope=16, k_stride=64, slots=16, q_lat=16, q_rope=16, cache=256,
+                num_pages=4, block_table=16, max_pages=2, seq_lens=16, B=1, s_q=1, H=128, scale=0.07,
+                split_tokens=0, split_indptr=None, num_splits=0, out=16, lse=None, part_m=None, part_s=None,
+                part_o=None)
+    args.update(over)
+    return lib.mla_lowbit_append_decode_attn(
+        ctypes.byref(fmt), args["c_kv"], args["c_stride"], args["k_rope"], args["k_stride"], args["slots"],
+        args["q_lat"], args["q_rope"], args["cache"], args["num_pages"], args["block_table"], args["max_pages"],
+        args["seq_lens"], args["B"], args["s_q"], args["H"], args["scale"], args["split_tokens"],
+        args["split_indptr"], args["num_splits"], args["out"], args["lse"], args["part_m"], args["part_s"],
+        args["part_o"], None)
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(c_kv=None), 1), (dict(slots=None), 1), (dict(c_stride=500), 1), (dict(c_kv=8), 2),
+    (dict(k_stride=68), 2), (dict(q_lat=None), 1), (dict(out=8), 2), (dict(s_q=3), 1), (dict(H=24), 1),
+    (dict(B=0), 0), (dict(B=0, c_kv=None, q_lat=None, cache=None, out=None), 0),
+])
+def test_append_decode_rejects_before_any_hip_call(mb, over, status):
+    """The append-and-decode call validates the writer's and the decode's arguments on the host."""
+    assert _append_decode_status(mb, **over) == status
