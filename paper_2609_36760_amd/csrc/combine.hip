@@ -8,9 +8,10 @@
 // One wave per output row (sequence, query token, head), four rows per
 // workgroup; each lane owns 8 of the 512 latent channels, so a split's
 // partial row is one coalesced 1 KiB read (16 bytes per lane).  The kernel is
-// bound by the reads of the partials: every split's loads of a batch are
-// issued before any is used (an empty split holds zeros and its weight
-// e^{-inf} s = 0 vanishes, so no branch separates the loads).
+// bound by the reads of the partials and their latency: every load of a batch
+// of splits (maximum, sum, latent row) is issued before any is used, so a
+// row costs two dependent rounds of loads (the split range, then the batch);
+// an empty split holds zeros and weighs e^{-inf} s = 0.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -47,32 +48,42 @@ __global__ __launch_bounds__(64 * kRowsPerBlock) void combine_kernel(CombineArgs
     const int j0 = a.split_indptr[b];
     const int j1 = a.split_indptr[b + 1];
 
-    float mx = -INFINITY;
-    for (int j = j0; j < j1; ++j) mx = fmaxf(mx, a.part_m[static_cast<int64_t>(j) * rows_per_seq + r]);
-
-    float s = 0.0f;
+    // Splits in batches of kBatch: all loads of a batch (maxima, sums and the
+    // latent rows) are issued together, then the running maximum moves to the
+    // batch's and the running sums are rescaled (online, as within a split).
+    float mx = -INFINITY, s = 0.0f;
     float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    if (mx != -INFINITY) {
-        for (int jb = j0; jb < j1; jb += kBatch) {
-            uint4 u[kBatch];
-            float ws[kBatch];
+    for (int jb = j0; jb < j1; jb += kBatch) {
+        uint4 u[kBatch];
+        float mk[kBatch], sk[kBatch];
 #pragma unroll
-            for (int k = 0; k < kBatch; ++k) {
-                const int j = min(jb + k, j1 - 1);
-                const int64_t pr = static_cast<int64_t>(j) * rows_per_seq + r;
-                u[k] = *reinterpret_cast<const uint4*>(a.part_o + pr * kDc + lane * 8);
-                ws[k] = jb + k < j1 ? expf(a.part_m[pr] - mx) * a.part_s[pr] : 0.0f;
-            }
+        for (int k = 0; k < kBatch; ++k) {
+            const int j = min(jb + k, j1 - 1);
+            const int64_t pr = static_cast<int64_t>(j) * rows_per_seq + r;
+            u[k] = *reinterpret_cast<const uint4*>(a.part_o + pr * kDc + lane * 8);
+            mk[k] = jb + k < j1 ? a.part_m[pr] : -INFINITY;
+            sk[k] = a.part_s[pr];
+        }
+        float bm = mk[0];
 #pragma unroll
-            for (int k = 0; k < kBatch; ++k) {
-                s += ws[k];
-                const uint32_t w4[4] = {u[k].x, u[k].y, u[k].z, u[k].w};
+        for (int k = 1; k < kBatch; ++k) bm = fmaxf(bm, mk[k]);
+        const float nm = fmaxf(mx, bm);
+        if (nm == -INFINITY) continue;          // no visible key so far
+        const float c = expf(mx - nm);          // 0 while mx = -inf
+        s *= c;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const f16x2 h2 = __builtin_bit_cast(f16x2, w4[q]);
-                    o[2 * q] += ws[k] * static_cast<float>(h2[0]);
-                    o[2 * q + 1] += ws[k] * static_cast<float>(h2[1]);
-                }
+        for (int q = 0; q < 8; ++q) o[q] *= c;
+        mx = nm;
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) {
+            const float ws = expf(mk[k] - mx) * sk[k];     // an empty split weighs 0
+            s += ws;
+            const uint32_t w4[4] = {u[k].x, u[k].y, u[k].z, u[k].w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const f16x2 h2 = __builtin_bit_cast(f16x2, w4[q]);
+                o[2 * q] += ws * static_cast<float>(h2[0]);
+                o[2 * q + 1] += ws * static_cast<float>(h2[1]);
             }
         }
     }
