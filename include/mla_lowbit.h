@@ -50,7 +50,7 @@ enum { MLA_OK = 0, MLA_EINVAL = 1, MLA_ENOTSUP = 2, MLA_EHIP = 3 };
 /*
  * Cache format (Appendix C.4 "Affine group quantization", Appendix C.5
  * "Storage layout").  Supported: d_c = 512, d_r = 64, group = 64,
- * c_bits in {4, 2}, r_bits = 4, page_size a positive multiple of 32,
+ * c_bits in {4, 2}, r_bits = 4, page_size a positive multiple of 32 (at most 2^20),
  * meta in {MLA_META_FP16, MLA_META_PAPER}.  The BF16 cache calls read only
  * d_c, d_r and page_size.
  */

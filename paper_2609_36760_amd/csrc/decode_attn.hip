@@ -399,10 +399,14 @@ __device__ __forceinline__ void dq_step(Dq<KIND>& d, int s, uint8_t* tile, int t
         const int t = s - 2, j = t >> 2, p = t & 3;
         d.o[p] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, d.pr[t & 3]) * (j < 8 ? d.ss : d.rs));
         if (p == 3) {
+            // content chunk 8 part + j sits at physical chunk 9 part + j of the
+            // row, the RoPE chunk 64 + part at 72 + part: one per-thread base
+            // each, the chunk index an immediate offset
             const int row = dq_row(tid), part = tid & 7;
-            const int chunk = j < 8 ? part * 8 + j : 64 + part;
-            *reinterpret_cast<uint4*>(tile + row_off(Cfg<KIND>::SC, row) + 16 * phys_chunk(true, chunk)) =
-                make_uint4(d.o[0], d.o[1], d.o[2], d.o[3]);
+            static_assert(phys_chunk(true, 8 * 7 + 5) == 9 * 7 + 5 && phys_chunk(true, 64 + 7) == 72 + 7,
+                          "grouped layout");
+            const int base = row_off(Cfg<KIND>::SC, row) + 16 * (j < 8 ? 9 * part : 72 + part);
+            *reinterpret_cast<uint4*>(tile + base + 16 * (j < 8 ? j : 0)) = make_uint4(d.o[0], d.o[1], d.o[2], d.o[3]);
         }
     }
     if (s >= 1 && s - 1 < 36) {                 // B: (1024 + q) - (1024 + zero) = q - zero, exact
@@ -637,19 +641,23 @@ void decode_kernel(DecodeArgs a) {
                 stage_bf16(k, ring_base, row_start, nvalid, slot_lds, wave, wave_u, lane);
             } else {
                 pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
-                const uint8_t* page = a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
+                // page_bytes < 2^31: one 32 x 32 -> 64-bit product, unsigned offsets
+                const uint8_t* page = a.cache + static_cast<uint64_t>(static_cast<uint32_t>(pid)) *
+                                                    static_cast<uint32_t>(a.g.page_bytes);
+                const uint32_t upo = static_cast<uint32_t>(po);
                 const uint32_t nv1 = static_cast<uint32_t>(nvalid - 1);
                 if constexpr (C::lowbit) {
                     if (k < C::code_rounds) {
                         const uint32_t tok = min(c_tok + static_cast<uint32_t>(k * (kThreads / cpt)), nv1);
-                        dma16_m0(page + po * C::cc, tok * C::cc + c_col, slot_lds + (k * kThreads + wave_u * 64) * 16);
+                        dma16_m0(page + upo * C::cc, tok * C::cc + c_col, slot_lds + (k * kThreads + wave_u * 64) * 16);
                     } else if (small_lane) {
-                        dma16_m0(page + s_reg + (po << s_shift), (min(s_tok, nv1) << 5) + s_col, slot_lds + dst_small);
+                        dma16_m0(page + (static_cast<uint32_t>(s_reg) + (upo << s_shift)), (min(s_tok, nv1) << 5) + s_col,
+                                 slot_lds + dst_small);
                     }
                 } else {
                     const uint32_t rc = (bf_rc[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
                     const int base_u = k < 9 ? k * kThreads + wave_u * 64 : 2304 + 64 * (wave_u & 1);
-                    dma16_m0(page + po * 1152, min(rc & 31u, nv1) * 1152u + (rc >> 5) * 16u, slot_lds + base_u * 16);
+                    dma16_m0(page + upo * 1152u, min(rc & 31u, nv1) * 1152u + (rc >> 5) * 16u, slot_lds + base_u * 16);
                 }
             }
         };
@@ -843,8 +851,15 @@ void decode_kernel(DecodeArgs a) {
                     const int v2 = q - 3;
                     const float p0 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2], a.scale_log2, nref));
                     const float p1 = __builtin_amdgcn_exp2f(fmaf(s[2 * v2 + 1], a.scale_log2, nref));
-                    l_run += p0 + p1;
-                    pw[v2] = C::lowbit ? pack_f16x2(p0, p1) : pack_bf16x2(p0, p1);
+                    if constexpr (C::lowbit) {
+                        // the sum of the fp16 weights the aggregation uses, one dot2 per pair
+                        pw[v2] = pack_f16x2(p0, p1);
+                        l_run = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, pw[v2]), f16x2{1.0f16, 1.0f16}, l_run,
+                                                       false);
+                    } else {
+                        l_run += p0 + p1;
+                        pw[v2] = pack_bf16x2(p0, p1);
+                    }
                     asm volatile("" : "+v"(pw[v2]), "+v"(l_run));
                 }
             };

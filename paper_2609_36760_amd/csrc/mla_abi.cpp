@@ -53,6 +53,8 @@ struct ProtDecode {
     const int32_t* prot_slot;
 };
 
+constexpr int32_t kMaxPageSize = 1 << 20;
+
 // Structural checks shared by both cache kinds.
 int check_shape(const mla_cache_format* f) {
     if (f == nullptr) return MLA_EINVAL;
@@ -60,6 +62,7 @@ int check_shape(const mla_cache_format* f) {
     if (f->page_size % 16 != 0) return MLA_EINVAL;
     if (f->d_c != kDc || f->d_r != kDr) return MLA_ENOTSUP;
     if (f->page_size % kTile != 0) return MLA_ENOTSUP;
+    if (f->page_size > kMaxPageSize) return MLA_ENOTSUP;      // a page's bytes fit 31 bits
     return MLA_OK;
 }
 
