@@ -98,7 +98,8 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
             if ev is not None:
                 ev[1].record(stream)
         if run.split_tokens:
-            mb.mla_splitkv_combine(run.part_m, run.part_s, run.part_o, run.split_indptr, run.B, run.s_q, run.H,
+            mb.mla_splitkv_combine(run.part_m, run.part_s, run.part_o, run.split_indptr, run.num_splits, run.B,
+                                   run.s_q, run.H,
                                    run.out, run.lse, stream=sh)
 
     for i in range(warmup):

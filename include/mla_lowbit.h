@@ -260,12 +260,15 @@ int mla_bf16_append_decode_attn(const mla_cache_format* f,
  *   out = (sum_j e^{part_m[j]-m} part_s[j] part_o[j]) / s  as bf16,
  *   lse = m + ln s
  * over the splits j of each sequence; splits with part_m = -inf are skipped.
- *   part_*  device, as written by the decode call (num_splits = split_indptr[B])
+ *   part_*  device, as written by the decode call
+ *   split_indptr, num_splits  as passed to the decode call (num_splits =
+ *           split_indptr[B], from mla_plan_splits; host value, it chooses
+ *           how the rows' splits are spread over the waves)
  *   out     device, bf16 [B][s_q][H][d_c];  lse device fp32 [B][s_q][H] or NULL
  * Every row must have at least one split with a visible key.  B = 0 is a no-op.
  */
 int mla_splitkv_combine(const float* part_m, const float* part_s, const uint16_t* part_o,
-                        const int32_t* split_indptr, int32_t B, int32_t s_q, int32_t H,
+                        const int32_t* split_indptr, int32_t num_splits, int32_t B, int32_t s_q, int32_t H,
                         int32_t d_c, uint16_t* out, float* lse, hipStream_t stream);
 
 /*

@@ -83,7 +83,7 @@ def library() -> ctypes.CDLL:
                                                   I32, P, I32, P, P, P, P, P, P]),
         "mla_bf16_decode_attn": (ctypes.c_int, [FMT, P, P, P, I64, P, I32, P, I32, I32, I32, F32,
                                                 I32, P, I32, P, P, P, P, P, P]),
-        "mla_splitkv_combine": (ctypes.c_int, [P, P, P, P, I32, I32, I32, I32, P, P, P]),
+        "mla_splitkv_combine": (ctypes.c_int, [P, P, P, P, I32, I32, I32, I32, I32, P, P, P]),
         "mla_lowbit_append_decode_attn": (ctypes.c_int, [FMT, P, I64, P, I64, P, P, P, P, I64, P, I32, P, I32, I32,
                                                          I32, F32, I32, P, I32, P, P, P, P, P, P]),
         "mla_bf16_append_decode_attn": (ctypes.c_int, [FMT, P, I64, P, I64, P, P, P, P, I64, P, I32, P, I32, I32,
@@ -221,9 +221,9 @@ def mla_bf16_append_decode_attn(fmt, c_kv, k_rope, slot_mapping, q_lat, q_rope, 
                    out, lse, part_m, part_s, part_o, stream)
 
 
-def mla_splitkv_combine(part_m, part_s, part_o, split_indptr, B, s_q, H, out, lse=None, stream=None):
+def mla_splitkv_combine(part_m, part_s, part_o, split_indptr, num_splits, B, s_q, H, out, lse=None, stream=None):
     _check("mla_splitkv_combine", library().mla_splitkv_combine(
-        _ptr(part_m), _ptr(part_s), _ptr(part_o), _ptr(split_indptr), B, s_q, H, 512,
+        _ptr(part_m), _ptr(part_s), _ptr(part_o), _ptr(split_indptr), num_splits, B, s_q, H, 512,
         _ptr(out), _ptr(lse), _stream(stream)))
 
 

@@ -99,6 +99,7 @@ constexpr int kNarrowRows = 32;
 hipError_t launch_decode_narrow(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_decode_narrow_protected(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_lowbit_append_protected(const AppendArgs& a, hipStream_t stream);
-hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+// num_splits (split_indptr[B]) chooses between one wave per row and four waves sharing a row.
+hipError_t launch_combine(const CombineArgs& a, int32_t num_splits, hipStream_t stream);
 
 }  // namespace mla

@@ -426,9 +426,9 @@ int mla_bf16_append_decode_attn(const mla_cache_format* f, const uint16_t* c_kv,
 }
 
 int mla_splitkv_combine(const float* part_m, const float* part_s, const uint16_t* part_o, const int32_t* split_indptr,
-                        int32_t B, int32_t s_q, int32_t H, int32_t d_c, uint16_t* out, float* lse,
-                        hipStream_t stream) {
-    if (B < 0 || d_c <= 0) return MLA_EINVAL;
+                        int32_t num_splits, int32_t B, int32_t s_q, int32_t H, int32_t d_c, uint16_t* out,
+                        float* lse, hipStream_t stream) {
+    if (B < 0 || d_c <= 0 || num_splits < 0) return MLA_EINVAL;
     if (s_q != 1 && s_q != 2) return MLA_EINVAL;
     if (H <= 0 || H % 16 != 0) return MLA_EINVAL;
     if (d_c != kDc) return MLA_ENOTSUP;
@@ -446,7 +446,7 @@ int mla_splitkv_combine(const float* part_m, const float* part_s, const uint16_t
     a.H = H;
     a.out = out;
     a.lse = lse;
-    return hip_status(mla::launch_combine(a, stream));
+    return hip_status(mla::launch_combine(a, num_splits, stream));
 }
 
 const char* mla_status_str(int status) {

@@ -204,7 +204,8 @@ class DecodeRun:
                num_splits=self.num_splits, out=self.out, lse=self.lse, part_m=self.part_m,
                part_s=self.part_s, part_o=self.part_o, stream=stream)
         if self.split_tokens:
-            mb.mla_splitkv_combine(self.part_m, self.part_s, self.part_o, self.split_indptr, self.B, self.s_q,
+            mb.mla_splitkv_combine(self.part_m, self.part_s, self.part_o, self.split_indptr, self.num_splits, self.B,
+                                   self.s_q,
                                    self.H, self.out, self.lse, stream=stream)
 
     def step(self, stream=None):
@@ -220,7 +221,8 @@ class DecodeRun:
            split_indptr=self.split_indptr, num_splits=self.num_splits, out=self.out, lse=self.lse,
            part_m=self.part_m, part_s=self.part_s, part_o=self.part_o, stream=stream)
         if self.split_tokens:
-            mb.mla_splitkv_combine(self.part_m, self.part_s, self.part_o, self.split_indptr, self.B, self.s_q,
+            mb.mla_splitkv_combine(self.part_m, self.part_s, self.part_o, self.split_indptr, self.num_splits, self.B,
+                                   self.s_q,
                                    self.H, self.out, self.lse, stream=stream)
 
     # ---- accounting -------------------------------------------------------

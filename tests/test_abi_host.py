@@ -111,9 +111,10 @@ def test_append_and_combine_validation(mb):
     assert lib.mla_lowbit_quant_append(f, 16, 512, 16, 64, 16, -1, 256, 1, None) == 1
     assert lib.mla_lowbit_quant_append(f, None, 512, None, 64, None, 0, None, 0, None) == 0   # n = 0
     assert lib.mla_bf16_append(f, 16, 512, 16, 64, 16, 4, 256, 0, None) == 1             # no pages
-    assert lib.mla_splitkv_combine(16, 16, 16, 16, 1, 3, 128, 512, 16, None, None) == 1
-    assert lib.mla_splitkv_combine(16, 16, 16, 16, 1, 1, 128, 256, 16, None, None) == 2
-    assert lib.mla_splitkv_combine(16, 16, 16, 16, 0, 1, 128, 512, 16, None, None) == 0
+    assert lib.mla_splitkv_combine(16, 16, 16, 16, 1, 1, 3, 128, 512, 16, None, None) == 1
+    assert lib.mla_splitkv_combine(16, 16, 16, 16, 1, 1, 1, 128, 256, 16, None, None) == 2
+    assert lib.mla_splitkv_combine(16, 16, 16, 16, 0, 0, 1, 128, 512, 16, None, None) == 0
+    assert lib.mla_splitkv_combine(16, 16, 16, 16, -1, 1, 1, 128, 512, 16, None, None) == 1   # negative split count
     assert lib.mla_last_hip_error() == 0
 
 
