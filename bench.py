@@ -39,6 +39,57 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+class TimingEvents:
+    """A pair of HIP timing events per timed launch, recorded on the launch's
+    stream.  They are created with ``hipEventDisableSystemFence``, the runtime's
+    flag for events used only to measure time: recording one then writes its
+    timestamp without the system-scope cache writeback and invalidation that a
+    default event performs (about 4 us per record after a decode launch, which
+    would be charged to the step).  The HIP runtime is the one torch loaded
+    (same soname); the events are destroyed with the object."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self, n: int):
+        import ctypes
+        import torch
+        torch.cuda.init()
+        self._c = ctypes
+        hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD | os.RTLD_GLOBAL)
+        hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self._hip = hip
+        self.pairs = []
+        for _ in range(n):
+            pair = []
+            for _ in range(2):
+                e = ctypes.c_void_p()
+                rc = hip.hipEventCreateWithFlags(ctypes.byref(e), self.DISABLE_SYSTEM_FENCE)
+                if rc != 0:
+                    raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+                pair.append(e)
+            self.pairs.append(tuple(pair))
+
+    def record(self, i: int, which: int, stream_handle) -> None:
+        rc = self._hip.hipEventRecord(self.pairs[i][which], stream_handle)
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def elapsed_ms(self, i: int) -> float:
+        f = self._c.c_float()
+        rc = self._hip.hipEventElapsedTime(self._c.byref(f), self.pairs[i][0], self.pairs[i][1])
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return f.value
+
+    def __del__(self):
+        for pair in getattr(self, "pairs", []):
+            for e in pair:
+                self._hip.hipEventDestroy(e)
+
+
 def algorithmic_bytes(run) -> int:
     """HBM bytes one decode launch must move: every attended key once, queries,
     and the split partials (fp16 normalized latent, fp32 max and sum) or the
@@ -77,26 +128,26 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
             # the append runs inside the decode launch (the same cache bytes and
             # outputs as the writer launch followed by the decode)
             if ev is not None:
-                ev[0].record(stream)
+                ev.record(i - warmup, 0, sh)
             fused(run.fmt, run.new_c, run.new_k, run.new_slots, run.q_lat, run.q_rope, cache, run.num_pages,
                   run.block_table, run.seq_lens, run.s_q, run.H, run.tau, split_tokens=run.split_tokens,
                   split_indptr=run.split_indptr, num_splits=run.num_splits, out=run.out, lse=run.lse,
                   part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
             if ev is not None:
-                ev[1].record(stream)
+                ev.record(i - warmup, 1, sh)
         else:
             mb.mla_lowbit_quant_append_protected(run.fmt, protect, run.new_c, run.new_k, run.new_slots, cache,
                                                  run.num_pages, run.new_seq, run.new_pos, run.seq_lens,
                                                  run.prot_slot, prot, run.num_prot, stream=sh)
             if ev is not None:
-                ev[0].record(stream)
+                ev.record(i - warmup, 0, sh)
             mb.mla_lowbit_decode_attn_protected(
                 run.fmt, protect, run.q_lat, run.q_rope, cache, run.num_pages, run.block_table, run.seq_lens,
                 run.s_q, run.H, run.tau, prot, run.num_prot, run.prot_slot, split_tokens=run.split_tokens,
                 split_indptr=run.split_indptr, num_splits=run.num_splits, out=run.out, lse=run.lse,
                 part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
             if ev is not None:
-                ev[1].record(stream)
+                ev.record(i - warmup, 1, sh)
         if run.split_tokens:
             mb.mla_splitkv_combine(run.part_m, run.part_s, run.part_o, run.split_indptr, run.num_splits, run.B,
                                    run.s_q, run.H,
@@ -104,14 +155,14 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
 
     for i in range(warmup):
         one_step(i)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    evs = TimingEvents(steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(steps):
-        one_step(i, evs[i])
+    for i in range(warmup, warmup + steps):
+        one_step(i, evs)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    kern_ms = float(np.mean([evs.elapsed_ms(k) for k in range(steps)]))
     ms_step = wall * 1e3 / steps
     flops = run.flops()
     nbytes = algorithmic_bytes(run)
