@@ -153,6 +153,7 @@ static_assert(row_off(76, 16) - row_off(76, 15) >= 16 * 72, "plain rows do not o
 
 template <int KIND>
 constexpr int lds_bytes() { return Cfg<KIND>::NT * tile_bytes<KIND>() + Cfg<KIND>::NS * Cfg<KIND>::stage_bytes; }
+constexpr int kLdsMax = 160 * 1024;     // LDS of a gfx950 workgroup
 static_assert(lds_bytes<KIND_C4R4>() <= 160 * 1024, "LDS budget of a gfx950 CU");
 static_assert(lds_bytes<KIND_C4R4P>() == lds_bytes<KIND_C4R4>(), "same staging for both metadata layouts");
 static_assert(lds_bytes<KIND_BF16>() <= 160 * 1024, "LDS budget of a gfx950 CU");
@@ -491,8 +492,13 @@ __device__ __forceinline__ void append_in_launch(const DecodeArgs& a, int b, int
 template <int KIND, bool kProt>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void decode_kernel(DecodeArgs a) {
-    constexpr int kLds = kProt && lds_bytes<KIND_BF16>() > lds_bytes<KIND>() ? lds_bytes<KIND_BF16>()
-                                                                              : lds_bytes<KIND>();
+    // Low-bit kinds take the whole 160 KiB: the staging slots sit at the top,
+    // so that the tile slots and the spare bytes below them form one region of
+    // at least 128 KiB, which holds the workgroup's query rows in the prologue.
+    constexpr int kLds = Cfg<KIND>::lowbit ? kLdsMax
+                         : kProt && lds_bytes<KIND_BF16>() > lds_bytes<KIND>() ? lds_bytes<KIND_BF16>()
+                                                                                : lds_bytes<KIND>();
+    static_assert(lds_bytes<KIND>() <= kLds && lds_bytes<KIND_BF16>() <= kLdsMax, "LDS budget");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kLds];
 
     const int tid = threadIdx.x;
@@ -574,7 +580,8 @@ void decode_kernel(DecodeArgs a) {
         constexpr int kDqKind = C::lowbit ? PK : KIND_C4R4;     // unused by the BF16 pipeline
         constexpr int kTileBytes = tile_bytes<PK>();
         uint8_t* tiles = smem;                              // NT x kTileBytes
-        uint8_t* stages = smem + C::NT * kTileBytes;        // NS x stage_bytes (low-bit only)
+        uint8_t* stages = smem + kLds - C::NS * C::stage_bytes;   // NS x stage_bytes at the top (low-bit only)
+        static_assert(!C::lowbit || C::NT * kTileBytes <= kLds - C::NS * C::stage_bytes, "tiles below the stages");
         const int n_tiles = t_end > t_begin ? (t_end - t_begin + kTile - 1) / kTile : 0;
         (void)t_lo;
 
@@ -669,12 +676,47 @@ void decode_kernel(DecodeArgs a) {
         static_assert(C::D <= 3, "prologue page ids");
         const int64_t qrow = (static_cast<int64_t>(b) * a.s_q + qi) * a.H + h;
         uint4 rawq[kKSteps];
+        // The wave's 32 content rows (1 KiB each) are read whole, one
+        // direct-to-LDS load per row, into LDS that the prologue's staging
+        // leaves free: low-bit, the region below the staging slots (free until
+        // tile 0 is dequantized), all rows at once; BF16, the tile slots past
+        // the D being staged, 16 rows per round, in two rounds.  Lane l fetches
+        // chunk l ^ (row & 15), so that chunk c of row j sits at slot
+        // c ^ (j & 15) and the operand reads (32 rows, one chunk each) spread
+        // over all banks.  Read straight from memory, the operands take 32
+        // rows x 32 bytes per load, four loads per cache line.
+        constexpr int kQRounds = C::lowbit ? 1 : 2;
+        constexpr int kQRows = 32 / kQRounds;                  // rows per wave and round
+        constexpr int kQOff = C::lowbit ? 0 : C::D * kTileBytes;
+        static_assert(kQOff + kWaves * kQRows * kDc * 2 <= (C::lowbit ? kLds - C::NS * C::stage_bytes : kLds),
+                      "query rows fit the free LDS");
+        const uint8_t* qseq = reinterpret_cast<const uint8_t*>(a.q_lat) +
+                              static_cast<int64_t>(b) * rows_total * (kDc * 2);
+        const int qr0 = rb * kRowsPerBlock + wave_u * 32;
+        const uint32_t qdst = lds_addr(smem) + kQOff + static_cast<uint32_t>(wave_u * kQRows) * (kDc * 2);
+        auto q_round = [&](int r) __attribute__((always_inline)) {
+#pragma unroll
+            for (int j = 0; j < kQRows; ++j) {
+                const int jr = r * kQRows + j;
+                const uint32_t rr = qr0 + jr < rows_total ? static_cast<uint32_t>(qr0 + jr) : 0u;
+                dma16_m0(qseq, rr * (kDc * 2) + 16u * static_cast<uint32_t>(lane ^ (jr & 15)),
+                         qdst + static_cast<uint32_t>(j) * (kDc * 2));
+            }
+        };
+        const uint8_t* qrow_lds = smem + kQOff + (wave * kQRows + (lane & 31) % kQRows) * (kDc * 2);
+        auto q_read = [&](int r) __attribute__((always_inline)) {
+            if ((lane & 31) / kQRows == r) {
+#pragma unroll
+                for (int kk = 0; kk < 32; ++kk)
+                    rawq[kk] = *reinterpret_cast<const uint4*>(qrow_lds + 16 * ((2 * kk + half) ^ (lane & 15)));
+            }
+        };
         {
-            const uint16_t* ql = a.q_lat + qrow * kDc + 8 * half;
             const uint16_t* qr = a.q_rope + qrow * 64 + 8 * half;
 #pragma unroll
-            for (int kk = 0; kk < kKSteps; ++kk) rawq[kk] = *reinterpret_cast<const uint4*>(kk < 32 ? ql + 16 * kk : qr + 16 * (kk - 32));
+            for (int kk = 32; kk < kKSteps; ++kk) rawq[kk] = *reinterpret_cast<const uint4*>(qr + 16 * (kk - 32));
         }
+        q_round(0);
         {
             int pids[3] = {0, 0, 0};
             if constexpr (!kRing) {
@@ -689,6 +731,21 @@ void decode_kernel(DecodeArgs a) {
                     for (int k = 0; k < C::loads; ++k) issue(k, pids[j], t0, t0 % P, stage_slot(j));
                 }
             }
+        }
+
+        // every load issued after the first round of query rows is one of the
+        // prologue's staging loads (Cfg::loads per staged tile, every wave)
+        if (n_tiles >= C::D)
+            asm volatile("s_waitcnt vmcnt(%0)" : : "n"(C::D * C::loads) : "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        q_read(0);
+        if constexpr (kQRounds == 2) {
+            // the second round overwrites the first's rows once they are read
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            q_round(1);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            q_read(1);
         }
 
         // queries as B operands: k-step kk holds channels 16kk + 8*half .. +8
