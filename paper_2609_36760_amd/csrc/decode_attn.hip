@@ -669,8 +669,7 @@ void decode_kernel(DecodeArgs a) {
             }
         };
         auto stage_slot = [&](int q) { return C::lowbit ? stages_lds + sofs[q] : tiles_lds + tofs[q]; };
-        // prologue: the queries' loads, then the first D tiles (their page ids
-        // fetched together) while the queries are in flight, then the queries'
+        // prologue: the first D tiles' staging, the queries' loads and their
         // conversion (rows past the end read row 0 of the sequence; they are
         // never stored)
         static_assert(C::D <= 3, "prologue page ids");
@@ -711,34 +710,33 @@ void decode_kernel(DecodeArgs a) {
                     rawq[kk] = *reinterpret_cast<const uint4*>(qrow_lds + 16 * ((2 * kk + half) ^ (lane & 15)));
             }
         };
+        // Order: the page ids of the first D tiles (one scalar round trip),
+        // the tiles' staging loads (the HBM latency that bounds the prologue),
+        // then the query rows, which every workgroup fetches at the same time
+        // (128 KiB each, mostly from L2) and which would otherwise hold the
+        // staging loads behind them.
+        int pids[3] = {0, 0, 0};
+        if constexpr (!kRing) {
+            auto pidx = [&](int j) { return (t_begin + (j < n_tiles ? j : 0) * kTile) / P; };
+            issue_page_ids3(bt, pidx(0), pidx(1), pidx(2), pids[0], pids[1], pids[2]);
+        }
         {
             const uint16_t* qr = a.q_rope + qrow * 64 + 8 * half;
 #pragma unroll
             for (int kk = 32; kk < kKSteps; ++kk) rawq[kk] = *reinterpret_cast<const uint4*>(qr + 16 * (kk - 32));
         }
-        q_round(0);
-        {
-            int pids[3] = {0, 0, 0};
-            if constexpr (!kRing) {
-                auto pidx = [&](int j) { return (t_begin + (j < n_tiles ? j : 0) * kTile) / P; };
-                load_page_ids3(bt, pidx(0), pidx(1), pidx(2), pids[0], pids[1], pids[2]);
-            }
+        if constexpr (!kRing) wait_page_ids3(pids[0], pids[1], pids[2]);
 #pragma unroll
-            for (int j = 0; j < C::D; ++j) {
-                if (j < n_tiles) {
-                    const int t0 = t_begin + j * kTile;
+        for (int j = 0; j < C::D; ++j) {
+            if (j < n_tiles) {
+                const int t0 = t_begin + j * kTile;
 #pragma unroll
-                    for (int k = 0; k < C::loads; ++k) issue(k, pids[j], t0, t0 % P, stage_slot(j));
-                }
+                for (int k = 0; k < C::loads; ++k) issue(k, pids[j], t0, t0 % P, stage_slot(j));
             }
         }
-
-        // every load issued after the first round of query rows is one of the
-        // prologue's staging loads (Cfg::loads per staged tile, every wave)
-        if (n_tiles >= C::D)
-            asm volatile("s_waitcnt vmcnt(%0)" : : "n"(C::D * C::loads) : "memory");
-        else
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        q_round(0);
+        // the query rows are the youngest loads: every staged tile lands first
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         q_read(0);
         if constexpr (kQRounds == 2) {
             // the second round overwrites the first's rows once they are read
@@ -1096,11 +1094,15 @@ void decode_kernel(DecodeArgs a) {
     const int row0 = rb * kRowsPerBlock + wave * 32;
     uint16_t* dst = split_out ? a.part_o + (static_cast<int64_t>(w) * rows_total + row0) * kDc
                               : a.out + (static_cast<int64_t>(b) * rows_total + row0) * kDc;
+    // Non-temporal stores: every workgroup writes its rows at about the same
+    // time, at the end of the launch, and the write burst is the epilogue's
+    // bound; written as streaming data they cost less.
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 #pragma unroll
     for (int i = 0; i < 32; ++i) {
         if (row0 + i < rows_total)
-            *reinterpret_cast<uint4*>(dst + i * kDc + 8 * lane) =
-                *reinterpret_cast<const uint4*>(ep + i * kRowPitch + 16 * lane);
+            __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(ep + i * kRowPitch + 16 * lane),
+                                        reinterpret_cast<u32x4*>(dst + i * kDc + 8 * lane));
     }
     if (!row_ok || half != 0) return;
     if (!split_out) {

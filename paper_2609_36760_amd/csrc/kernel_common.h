@@ -90,14 +90,17 @@ __device__ __forceinline__ int load_page_id(const int32_t* table, int index) {
     return v;
 }
 
-// Entries idx[0..N) of a page table, fetched through the scalar cache
-// together and waited for once (the wait names the results, so that no use
-// is placed before it).
-__device__ __forceinline__ void load_page_ids3(const int32_t* table, int i0, int i1, int i2, int& p0, int& p1,
-                                               int& p2) {
+// Entries i0, i1, i2 of a page table, fetched through the scalar cache
+// together (issue_page_ids3) and waited for once (wait_page_ids3, which names
+// the results, so that no use is placed before it); other work can be issued
+// in between.
+__device__ __forceinline__ void issue_page_ids3(const int32_t* table, int i0, int i1, int i2, int& p0, int& p1,
+                                                int& p2) {
     asm volatile("s_load_dword %0, %1, %2" : "=&s"(p0) : "s"(table), "s"(__builtin_amdgcn_readfirstlane(i0 * 4)));
     asm volatile("s_load_dword %0, %1, %2" : "=&s"(p1) : "s"(table), "s"(__builtin_amdgcn_readfirstlane(i1 * 4)));
     asm volatile("s_load_dword %0, %1, %2" : "=&s"(p2) : "s"(table), "s"(__builtin_amdgcn_readfirstlane(i2 * 4)));
+}
+__device__ __forceinline__ void wait_page_ids3(int& p0, int& p1, int& p2) {
     asm volatile("s_waitcnt lgkmcnt(0)" : "+s"(p0), "+s"(p1), "+s"(p2) : : "memory");
 }
 
