@@ -40,13 +40,15 @@ def log(*a):
 
 
 class TimingEvents:
-    """A pair of HIP timing events per timed launch, recorded on the launch's
-    stream.  They are created with ``hipEventDisableSystemFence``, the runtime's
-    flag for events used only to measure time: recording one then writes its
-    timestamp without the system-scope cache writeback and invalidation that a
-    default event performs (about 4 us per record after a decode launch, which
-    would be charged to the step).  The HIP runtime is the one torch loaded
-    (same soname); the events are destroyed with the object."""
+    """A pair of HIP timing events per timed decode launch.  ``arm(i)`` hands
+    pair i to ``mla_time_next_decode_launch``: the library attaches it to the
+    decode kernel's own dispatch (hipExtLaunchKernel), on the launch's stream,
+    so the pair brackets the kernel's execution and not the dispatch latency
+    that events recorded around the call would add (about 6 us per launch at
+    32 x 4K).  The events are created with ``hipEventDisableSystemFence``, the
+    runtime's flag for events used only to measure time (no system-scope cache
+    writeback when their timestamp is written).  The HIP runtime is the one
+    torch loaded (same soname); the events are destroyed with the object."""
 
     DISABLE_SYSTEM_FENCE = 0x20000000
 
@@ -72,10 +74,9 @@ class TimingEvents:
                 pair.append(e)
             self.pairs.append(tuple(pair))
 
-    def record(self, i: int, which: int, stream_handle) -> None:
-        rc = self._hip.hipEventRecord(self.pairs[i][which], stream_handle)
-        if rc != 0:
-            raise RuntimeError(f"hipEventRecord failed ({rc})")
+    def arm(self, i: int) -> None:
+        from paper_2609_36760_amd import _binding as mb
+        mb.mla_time_next_decode_launch(self.pairs[i][0].value, self.pairs[i][1].value)
 
     def elapsed_ms(self, i: int) -> float:
         f = self._c.c_float()
@@ -128,26 +129,22 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
             # the append runs inside the decode launch (the same cache bytes and
             # outputs as the writer launch followed by the decode)
             if ev is not None:
-                ev.record(i - warmup, 0, sh)
+                ev.arm(i - warmup)
             fused(run.fmt, run.new_c, run.new_k, run.new_slots, run.q_lat, run.q_rope, cache, run.num_pages,
                   run.block_table, run.seq_lens, run.s_q, run.H, run.tau, split_tokens=run.split_tokens,
                   split_indptr=run.split_indptr, num_splits=run.num_splits, out=run.out, lse=run.lse,
                   part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
-            if ev is not None:
-                ev.record(i - warmup, 1, sh)
         else:
             mb.mla_lowbit_quant_append_protected(run.fmt, protect, run.new_c, run.new_k, run.new_slots, cache,
                                                  run.num_pages, run.new_seq, run.new_pos, run.seq_lens,
                                                  run.prot_slot, prot, run.num_prot, stream=sh)
             if ev is not None:
-                ev.record(i - warmup, 0, sh)
+                ev.arm(i - warmup)
             mb.mla_lowbit_decode_attn_protected(
                 run.fmt, protect, run.q_lat, run.q_rope, cache, run.num_pages, run.block_table, run.seq_lens,
                 run.s_q, run.H, run.tau, prot, run.num_prot, run.prot_slot, split_tokens=run.split_tokens,
                 split_indptr=run.split_indptr, num_splits=run.num_splits, out=run.out, lse=run.lse,
                 part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
-            if ev is not None:
-                ev.record(i - warmup, 1, sh)
         if run.split_tokens:
             mb.mla_splitkv_combine(run.part_m, run.part_s, run.part_o, run.split_indptr, run.num_splits, run.B,
                                    run.s_q, run.H,

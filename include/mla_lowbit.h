@@ -384,6 +384,19 @@ const char* mla_status_str(int status);
 /* hipError_t of this thread's last MLA_EHIP return (0 if none). */
 int mla_last_hip_error(void);
 
+/* Measurement hook (not part of the computation).  The next decode-kernel
+ * dispatch made by the calling host thread -- from any *_decode_attn entry
+ * point, the append-and-decode ones included -- carries `start` and `stop`
+ * on its own dispatch packet (hipExtLaunchKernel), so that
+ * hipEventElapsedTime(start, stop) is that kernel's execution time, free of
+ * the dispatch latency that events recorded around the call would include.
+ * Writer and combine launches do not consume it.  One-shot: the pair is
+ * cleared by that dispatch (a call that returns an error or has no work
+ * dispatches nothing and leaves it set); passing two nulls clears it.
+ * Both events belong to the caller, must stay valid until the dispatch has
+ * completed, and must be both null or both non-null (else MLA_EINVAL). */
+int mla_time_next_decode_launch(hipEvent_t start, hipEvent_t stop);
+
 #ifdef __cplusplus
 }
 #endif

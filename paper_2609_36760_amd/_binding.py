@@ -23,7 +23,7 @@ SYMBOLS = (
     "mla_plan_splits", "mla_lowbit_decode_attn", "mla_bf16_decode_attn", "mla_splitkv_combine",
     "mla_status_str", "mla_last_hip_error", "mla_protect_buffer_bytes", "mla_lowbit_quant_append_protected",
     "mla_plan_splits_protected", "mla_lowbit_decode_attn_protected", "mla_persistent_cache_bytes",
-    "mla_lowbit_append_decode_attn", "mla_bf16_append_decode_attn",
+    "mla_lowbit_append_decode_attn", "mla_bf16_append_decode_attn", "mla_time_next_decode_launch",
 )
 
 
@@ -97,6 +97,7 @@ def library() -> ctypes.CDLL:
                                                             P, I64, P, I32, P, I32, P, P, P, P, P, P]),
         "mla_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "mla_last_hip_error": (ctypes.c_int, []),
+        "mla_time_next_decode_launch": (ctypes.c_int, [P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -112,6 +113,12 @@ def mla_status_str(status: int) -> str:
 
 def mla_last_hip_error() -> int:
     return library().mla_last_hip_error()
+
+
+def mla_time_next_decode_launch(start, stop) -> None:
+    """Attach two HIP events (raw handles, or None for both) to this thread's
+    next decode-kernel dispatch."""
+    _check("mla_time_next_decode_launch", library().mla_time_next_decode_launch(start, stop))
 
 
 def _ptr(t):

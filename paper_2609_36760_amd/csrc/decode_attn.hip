@@ -1122,31 +1122,33 @@ void decode_kernel(DecodeArgs a) {
 
 hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream) {
     if (a.num_work == 0) return hipSuccess;
+    const LaunchEvents ev = take_launch_events();
     const int rows = a.s_q * a.H;
     const int RB = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
     const int blocks = ((a.num_work + 7) / 8) * 8 * RB;
     const dim3 grid(static_cast<unsigned>(blocks)), block(kThreads);
     switch (kind) {
-        case KIND_C4R4: hipLaunchKernelGGL((decode_kernel<KIND_C4R4, false>), grid, block, 0, stream, a); break;
-        case KIND_C2R4: hipLaunchKernelGGL((decode_kernel<KIND_C2R4, false>), grid, block, 0, stream, a); break;
-        case KIND_C4R4P: hipLaunchKernelGGL((decode_kernel<KIND_C4R4P, false>), grid, block, 0, stream, a); break;
-        case KIND_C2R4P: hipLaunchKernelGGL((decode_kernel<KIND_C2R4P, false>), grid, block, 0, stream, a); break;
-        case KIND_BF16: hipLaunchKernelGGL((decode_kernel<KIND_BF16, false>), grid, block, 0, stream, a); break;
+        case KIND_C4R4: dispatch_decode(decode_kernel<KIND_C4R4, false>, grid, block, stream, ev, a); break;
+        case KIND_C2R4: dispatch_decode(decode_kernel<KIND_C2R4, false>, grid, block, stream, ev, a); break;
+        case KIND_C4R4P: dispatch_decode(decode_kernel<KIND_C4R4P, false>, grid, block, stream, ev, a); break;
+        case KIND_C2R4P: dispatch_decode(decode_kernel<KIND_C2R4P, false>, grid, block, stream, ev, a); break;
+        case KIND_BF16: dispatch_decode(decode_kernel<KIND_BF16, false>, grid, block, stream, ev, a); break;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_decode_protected(CacheKind kind, const DecodeArgs& a, hipStream_t stream) {
     if (a.num_work == 0) return hipSuccess;
+    const LaunchEvents ev = take_launch_events();
     const int rows = a.s_q * a.H;
     const int RB = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
     const int blocks = ((a.num_work + 7) / 8) * 8 * RB;
     const dim3 grid(static_cast<unsigned>(blocks)), block(kThreads);
     switch (kind) {
-        case KIND_C4R4: hipLaunchKernelGGL((decode_kernel<KIND_C4R4, true>), grid, block, 0, stream, a); break;
-        case KIND_C2R4: hipLaunchKernelGGL((decode_kernel<KIND_C2R4, true>), grid, block, 0, stream, a); break;
-        case KIND_C4R4P: hipLaunchKernelGGL((decode_kernel<KIND_C4R4P, true>), grid, block, 0, stream, a); break;
-        case KIND_C2R4P: hipLaunchKernelGGL((decode_kernel<KIND_C2R4P, true>), grid, block, 0, stream, a); break;
+        case KIND_C4R4: dispatch_decode(decode_kernel<KIND_C4R4, true>, grid, block, stream, ev, a); break;
+        case KIND_C2R4: dispatch_decode(decode_kernel<KIND_C2R4, true>, grid, block, stream, ev, a); break;
+        case KIND_C4R4P: dispatch_decode(decode_kernel<KIND_C4R4P, true>, grid, block, stream, ev, a); break;
+        case KIND_C2R4P: dispatch_decode(decode_kernel<KIND_C2R4P, true>, grid, block, stream, ev, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

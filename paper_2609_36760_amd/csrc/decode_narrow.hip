@@ -530,16 +530,17 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
 template <bool kProt>
 hipError_t launch(CacheKind kind, const DecodeArgs& a, hipStream_t stream) {
     if (a.num_work == 0) return hipSuccess;
+    const LaunchEvents ev = take_launch_events();
     const int RB = (a.s_q * a.H + kRows - 1) / kRows;
     const dim3 grid(static_cast<unsigned>(((a.num_work + 7) / 8) * 8 * RB)), block(64);
     switch (kind) {
-        case KIND_C4R4: hipLaunchKernelGGL((narrow_kernel<KIND_C4R4, kProt>), grid, block, 0, stream, a); break;
-        case KIND_C2R4: hipLaunchKernelGGL((narrow_kernel<KIND_C2R4, kProt>), grid, block, 0, stream, a); break;
-        case KIND_C4R4P: hipLaunchKernelGGL((narrow_kernel<KIND_C4R4P, kProt>), grid, block, 0, stream, a); break;
-        case KIND_C2R4P: hipLaunchKernelGGL((narrow_kernel<KIND_C2R4P, kProt>), grid, block, 0, stream, a); break;
+        case KIND_C4R4: dispatch_decode(narrow_kernel<KIND_C4R4, kProt>, grid, block, stream, ev, a); break;
+        case KIND_C2R4: dispatch_decode(narrow_kernel<KIND_C2R4, kProt>, grid, block, stream, ev, a); break;
+        case KIND_C4R4P: dispatch_decode(narrow_kernel<KIND_C4R4P, kProt>, grid, block, stream, ev, a); break;
+        case KIND_C2R4P: dispatch_decode(narrow_kernel<KIND_C2R4P, kProt>, grid, block, stream, ev, a); break;
         case KIND_BF16:
             if constexpr (kProt) return hipErrorInvalidValue;
-            else hipLaunchKernelGGL((narrow_kernel<KIND_BF16, false>), grid, block, 0, stream, a);
+            else dispatch_decode(narrow_kernel<KIND_BF16, false>, grid, block, stream, ev, a);
             break;
     }
     return hipGetLastError();

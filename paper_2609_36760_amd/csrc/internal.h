@@ -90,6 +90,13 @@ struct CombineArgs {
     float* lse;
 };
 
+// Events for the next decode-kernel dispatch on this host thread (both null
+// when none); take_launch_events() returns them and clears them.
+struct LaunchEvents {
+    hipEvent_t start, stop;
+};
+LaunchEvents take_launch_events();
+
 hipError_t launch_lowbit_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_bf16_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream);

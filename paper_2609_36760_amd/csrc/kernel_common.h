@@ -2,6 +2,7 @@
 // Internal; not part of the public C ABI.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -126,6 +127,18 @@ __device__ __forceinline__ void meta_to_f16(uint32_t meta, f16x2& zz, f16x2& ss)
     const _Float16 zb = z + static_cast<_Float16>(1024.0f);    // exact: z is an integer in [0, 15]
     zz = f16x2{zb, zb};
     ss = f16x2{s, s};
+}
+
+// Host side: dispatch a decode kernel, attaching the events that
+// mla_time_next_decode_launch left for this thread (if any) to the dispatch
+// itself, so that they time the kernel's execution alone.
+template <typename Kernel, typename Args>
+void dispatch_decode(Kernel kernel, dim3 grid, dim3 block, hipStream_t stream, const LaunchEvents& ev,
+                     const Args& a) {
+    if (ev.start != nullptr)
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, ev.start, ev.stop, 0, a);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, 0, stream, a);
 }
 
 }  // namespace kc

@@ -13,6 +13,7 @@
 namespace {
 
 thread_local int g_last_hip_error = 0;
+thread_local mla::LaunchEvents g_launch_events{nullptr, nullptr};
 
 constexpr int32_t kDc = 512;
 constexpr int32_t kDr = 64;
@@ -244,6 +245,14 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
 
 }  // namespace
 
+namespace mla {
+LaunchEvents take_launch_events() {
+    const LaunchEvents e = g_launch_events;
+    g_launch_events = LaunchEvents{nullptr, nullptr};
+    return e;
+}
+}  // namespace mla
+
 // Append the step's new tokens, then decode (one launch for the wide kernel).
 static int append_decode(const mla_cache_format* f, bool lowbit, const uint16_t* c_kv, int64_t c_kv_stride,
                   const uint16_t* k_rope, int64_t k_rope_stride, const int64_t* slot_mapping, const uint16_t* q_lat,
@@ -460,5 +469,11 @@ const char* mla_status_str(int status) {
 }
 
 int mla_last_hip_error(void) { return g_last_hip_error; }
+
+int mla_time_next_decode_launch(hipEvent_t start, hipEvent_t stop) {
+    if ((start == nullptr) != (stop == nullptr)) return MLA_EINVAL;
+    g_launch_events = mla::LaunchEvents{start, stop};
+    return MLA_OK;
+}
 
 }  // extern "C"

@@ -32,7 +32,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(mb):
     names = declared_functions()
-    assert len(names) == 17
+    assert len(names) == 18
     lib = ctypes.CDLL(mb.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -234,3 +234,11 @@ def _append_decode_status(mb, **over):
 def test_append_decode_rejects_before_any_hip_call(mb, over, status):
     """The append-and-decode call validates the writer's and the decode's arguments on the host."""
     assert _append_decode_status(mb, **over) == status
+
+
+def test_timing_hook_takes_both_events_or_none(mb):
+    """mla_time_next_decode_launch: a pair of events or two nulls (clear)."""
+    lib = mb.library()
+    assert lib.mla_time_next_decode_launch(16, None) == 1
+    assert lib.mla_time_next_decode_launch(None, 16) == 1
+    assert lib.mla_time_next_decode_launch(None, None) == 0

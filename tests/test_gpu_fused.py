@@ -52,3 +52,59 @@ def test_append_decode_matches_separate_calls(case):
     assert torch.equal(a.out, b.out), "outputs differ"
     assert torch.equal(a.lse, b.lse), "lse differs"
     print(f"  {name}: cache {a.cache.numel()} bytes and {a.out.numel()} outputs identical", flush=True)
+
+
+def test_timing_hook_leaves_outputs_and_times_the_kernel():
+    """Events attached to the decode dispatch by mla_time_next_decode_launch:
+    the outputs are unchanged, the pair is consumed by the decode dispatch (a
+    second launch without re-arming records nothing new) and brackets a time
+    shorter than events recorded around the call on the same stream."""
+    import ctypes
+    import os
+
+    import torch
+
+    from paper_2609_36760_amd import _binding as mb
+    from paper_2609_36760_amd.runner import DecodeRun
+    w = syn.Workload("hook", 150, B=4, H=128, s_q=1, context=None, layers=((4, 4),), split_tokens=256,
+                     ctx_range=(1, 2))
+    lens = np.asarray([300, 1000, 777, 1024], np.int32)
+    a = DecodeRun(w, kind="lowbit", seq_lens=lens)
+    b = DecodeRun(w, kind="lowbit", seq_lens=lens)
+    b.cache.copy_(a.cache)
+    torch.cuda.init()
+    hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD | os.RTLD_GLOBAL)
+    hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+    hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    ev = [ctypes.c_void_p() for _ in range(4)]
+    for e in ev:
+        assert hip.hipEventCreateWithFlags(ctypes.byref(e), 0) == 0
+
+    def elapsed(x, y):
+        f = ctypes.c_float()
+        assert hip.hipEventElapsedTime(ctypes.byref(f), x, y) == 0
+        return f.value
+
+    try:
+        sh = torch.cuda.current_stream().cuda_stream
+        torch.cuda.synchronize()
+        a.fused_step()
+        mb.mla_time_next_decode_launch(ev[0].value, ev[1].value)
+        assert hip.hipEventRecord(ev[2], sh) == 0
+        b.fused_step()
+        assert hip.hipEventRecord(ev[3], sh) == 0
+        torch.cuda.synchronize()
+        kern, window = elapsed(ev[0], ev[1]), elapsed(ev[2], ev[3])
+        assert torch.equal(a.cache, b.cache) and torch.equal(a.out, b.out) and torch.equal(a.lse, b.lse)
+        assert 0.0 < kern < window, (kern, window)
+        # consumed: another launch leaves the pair as it was
+        b.fused_step()
+        torch.cuda.synchronize()
+        assert elapsed(ev[0], ev[1]) == kern
+        print(f"  kernel {kern * 1e3:.1f} us inside a {window * 1e3:.1f} us window", flush=True)
+    finally:
+        mb.mla_time_next_decode_launch(None, None)
+        for e in ev:
+            hip.hipEventDestroy(e)
