@@ -105,7 +105,7 @@ def algorithmic_bytes(run) -> int:
 
 
 def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=None, split_tokens=None,
-                  meta="fp16"):
+                  meta="fp16", layer=0, device_tokens=False):
     import torch
 
     from paper_2609_36760_amd import _binding as mb
@@ -113,7 +113,8 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
     from paper_2609_36760_amd.runner import DecodeRun
     w = syn.WORKLOADS[name]
     t0 = time.perf_counter()
-    run = DecodeRun(w, kind=kind, token_cache=token_cache, protect=protect, split_tokens=split_tokens, meta=meta)
+    run = DecodeRun(w, layer=layer, kind=kind, token_cache=token_cache, protect=protect, split_tokens=split_tokens,
+                    meta=meta, device_tokens=device_tokens)
     caches = [run.cache] + [run.cache.clone() for _ in range(layers - 1)]
     prots = [None] * layers if protect is None else [run.prot] + [run.prot.clone() for _ in range(layers - 1)]
     torch.cuda.synchronize()
@@ -262,6 +263,39 @@ def grid_split(B: int, n_list: int, target: int = 1024) -> int:
     return 32 * per
 
 
+CONFIG_SHAPES = (
+    # (workload, cache layer, label)
+    ("int2_b64_h128_32k_c2r4", 0, "C2R4, 64 x 32K"),
+    ("splitkv_b8_h128_128k_c4r4", 0, "C4R4, 8 x 128K, 64 splits of 2048"),
+    ("ragged_b96_h128_sq2_mixed", 0, "C4R4 layer, 96 ragged 1K-128K, s_q 2, 2 tokens appended"),
+    ("ragged_b96_h128_sq2_mixed", 1, "C2R4 layer, 96 ragged 1K-128K, s_q 2, 2 tokens appended"),
+)
+
+
+def config_report(args):
+    """The full-size correctness configurations timed like the bench workload
+    (append inside the decode launch, then the combine; one resident cache),
+    low-bit and BF16 cache, with the roofline that binds each: a kernel is
+    MFMA-bound when its algorithmic intensity (flop per HBM byte) exceeds the
+    ridge 2500 TFLOP/s / 8 TB/s = 312.5 flop/B, else HBM-bound."""
+    ridge = PEAK_BF16_TFLOPS / (PEAK_HBM_GBS / 1e3)
+    rows = []
+    for name, layer, label in CONFIG_SHAPES:
+        res = {"workload": name, "layer": layer, "label": label}
+        for kind in ("lowbit", "bf16"):
+            r = time_workload(name, kind, args.config_steps, 2, 1, layer=layer, device_tokens=True)
+            inten = r["flops_per_launch"] / r["bytes_per_launch"]
+            bound = "mfma" if inten > ridge else "hbm"
+            r["intensity_flop_per_byte"] = inten
+            r["bound"] = bound
+            r["frac_of_binding_roofline"] = r["mfma_frac"] if bound == "mfma" else r["hbm_frac"]
+            res[kind] = r
+        res["speedup_vs_bf16"] = res["bf16"]["ms_per_step"] / res["lowbit"]["ms_per_step"]
+        rows.append(res)
+    print(json.dumps({"metric": METRIC, "report": "configs", "ridge_flop_per_byte": ridge, "configs": rows}),
+          flush=True)
+
+
 def paper_grid(args):
     """Attention latency over the paper's grid: decode + combine, L2 flushed
     (a 512 MiB write) before every sample, HIP events on the launch stream."""
@@ -333,6 +367,9 @@ def main():
                     help="first copy a 256 MiB buffer once (reference for HBM traffic counters)")
     ap.add_argument("--paper-grid", action="store_true",
                     help="instead of the step benchmark: the paper's 16-head attention latency grid")
+    ap.add_argument("--configs", action="store_true",
+                    help="report the full-size correctness configurations instead (one JSON line)")
+    ap.add_argument("--config-steps", type=int, default=5)
     ap.add_argument("--grid-batches", default="8,32")
     ap.add_argument("--grid-contexts", default="1024,4096,8192,16384,32768,65536,131072,262144,524288,1048576")
     ap.add_argument("--grid-samples", type=int, default=30)
@@ -349,6 +386,9 @@ def main():
 
     if args.paper_grid:
         paper_grid(args)
+        return
+    if args.configs:
+        config_report(args)
         return
     if args.calib_copy:
         src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda")
