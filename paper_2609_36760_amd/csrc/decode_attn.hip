@@ -325,6 +325,7 @@ template <int KIND> struct Dq {
                                     // rmeta = fp32 scale bits, rzero)
     uint32_t rzero;
     f16x2 zz, ss, rz, rs;           // metadata as fp16 (zero + 1024, scale)
+    f16x2 zo[3], rzo;               // -(1024 / 4^(k+1) + zero) for pairs at bit offset 2(k+1) (RoPE: offset 4)
     uint32_t pr[4];                 // pairs in flight (index task & 3)
     uint32_t o[4];                  // finished pairs of the chunk being stored
 };
@@ -372,14 +373,22 @@ __device__ __forceinline__ uint32_t dq_word(const Dq<KIND>& d, int j) {
     }
 }
 
-// Pair p (channels 2p, 2p+1) of chunk j as fp16 bits 0x6400 | q = 1024 + q:
-// in the code layout a channel pair sits at one bit offset of the two 16-bit
-// halves of a word, so one shift and one mask-and-or extract it.
+// Bit offset of pair p of chunk j in its code word: in the code layout a
+// channel pair sits at one bit offset of the two 16-bit halves of a word.
+template <int KIND>
+__device__ __forceinline__ constexpr int dq_shift(int j, int p) {
+    return dq_is4<KIND>(j) ? 4 * p : 8 * (j & 1) + 2 * p;
+}
+
+// Pair p (channels 2p, 2p+1) of chunk j as the fp16 pair with bits
+// 0x6400 | (q << o) = 1024 + 2^o q, o = dq_shift mod 8: the word is shifted
+// only by the multiple of 8 (shared by the pairs of a byte), and the code is
+// masked in place.  1024 + 2^o q is an integer below 2048, exact in fp16.
 template <int KIND>
 __device__ __forceinline__ uint32_t dq_pair(const Dq<KIND>& d, int j, int p) {
-    const bool is4 = dq_is4<KIND>(j);
-    const int sh = is4 ? 4 * p : 8 * (j & 1) + 2 * p;
-    return and_or(dq_word<KIND>(d, j) >> sh, is4 ? 0x000F000Fu : 0x00030003u, 0x64006400u);
+    const int sh = dq_shift<KIND>(j, p);
+    const uint32_t m = (dq_is4<KIND>(j) ? 0x000F000Fu : 0x00030003u) << (sh & 7);
+    return and_or(dq_word<KIND>(d, j) >> (sh & ~7), m, 0x64006400u);
 }
 
 // Dequantization steps 0 .. kDqSteps - 1 (36 pairs through three stages).
@@ -395,6 +404,14 @@ __device__ __forceinline__ void dq_step(Dq<KIND>& d, int s, uint8_t* tile, int t
             meta_to_f16(d.meta, d.zz, d.ss);
             meta_to_f16(d.rmeta, d.rz, d.rs);
         }
+        // -(1024 / 2^o + zero) for the offsets o = 2, 4, 6 (from zero + 1024:
+        // exact, integers and quarters below 1024)
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            const _Float16 c = static_cast<_Float16>(1024.0f - 1024.0f / static_cast<float>(4 << (2 * k)));
+            d.zo[k] = f16x2{c, c} - d.zz;
+        }
+        d.rzo = f16x2{static_cast<_Float16>(960.0f), static_cast<_Float16>(960.0f)} - d.rz;
     }
     if (s >= 2 && s - 2 < 36) {                 // C: scale; store a finished chunk
         const int t = s - 2, j = t >> 2, p = t & 3;
@@ -410,9 +427,19 @@ __device__ __forceinline__ void dq_step(Dq<KIND>& d, int s, uint8_t* tile, int t
             *reinterpret_cast<uint4*>(tile + base + 16 * (j < 8 ? j : 0)) = make_uint4(d.o[0], d.o[1], d.o[2], d.o[3]);
         }
     }
-    if (s >= 1 && s - 1 < 36) {                 // B: (1024 + q) - (1024 + zero) = q - zero, exact
-        const int t = s - 1, j = t >> 2;
-        d.pr[t & 3] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, d.pr[t & 3]) - (j < 8 ? d.zz : d.rz));
+    if (s >= 1 && s - 1 < 36) {                 // B: q - zero, exact
+        const int t = s - 1, j = t >> 2, o = dq_shift<KIND>(j, t & 3) & 7;
+        const f16x2 x = __builtin_bit_cast(f16x2, d.pr[t & 3]);
+        if (o == 0) {
+            // (1024 + q) - (1024 + zero)
+            d.pr[t & 3] = __builtin_bit_cast(uint32_t, x - (j < 8 ? d.zz : d.rz));
+        } else {
+            // (1024 + 2^o q) 2^-o is 1024 / 2^o + q exactly; adding -(1024 / 2^o + zero)
+            // leaves q - zero, so the fused multiply-add rounds nothing
+            const _Float16 w = static_cast<_Float16>(1.0f / static_cast<float>(1 << o));
+            const f16x2 c = j < 8 ? d.zo[o / 2 - 1] : d.rzo;
+            d.pr[t & 3] = __builtin_bit_cast(uint32_t, __builtin_elementwise_fma(x, f16x2{w, w}, c));
+        }
     }
     if (s < 36) {                               // A: extract pair p of chunk j
         const int t = s;
