@@ -14,7 +14,9 @@
  *   - Pointers named as device buffers must be device memory of the current
  *     HIP device; host pointers are marked "host".  The caller owns every
  *     buffer; the library allocates nothing and keeps no state between calls
- *     except a per-thread copy of the last HIP error.
+ *     except, per host thread, a copy of the last HIP error and the event
+ *     pair armed by mla_time_next_decode_launch (two handles, cleared by the
+ *     decode dispatch that consumes them).
  *   - bf16 tensors are passed as uint16_t bit patterns.  All tensors are dense
  *     and row-major in the index order given, unless a stride is an argument.
  *     Query, output and partial tensors must be 16-byte aligned (else

@@ -169,6 +169,26 @@ def read_tokens(cache: np.ndarray, fmt: CacheFormat, slots):
     for i, slot in enumerate(slots):
         for (start, size), dst in zip(_token_byte_ranges(fmt, slot), blocks):
             dst[i] = cache[start:start + size]
+    return decode_blocks(fmt, blocks)
+
+
+def page_blocks(fmt: CacheFormat, pages: np.ndarray, n: int):
+    """The per-token byte blocks of every region (page order) of the first
+    ``n`` tokens stored in consecutive pages ``pages [num, page_bytes]``
+    (token ``t`` at page ``t // P``, offset ``t % P``)."""
+    pages = np.asarray(pages, np.uint8).reshape(-1, fmt.page_bytes)
+    offs = fmt.region_offsets()
+    out = []
+    for o, size in zip(offs[:-1], fmt.region_sizes()):
+        reg = pages[:, o:o + fmt.page_size * size].reshape(-1, size)
+        out.append(np.ascontiguousarray(reg[:n]))
+    return out
+
+
+def decode_blocks(fmt: CacheFormat, blocks):
+    """Reconstruct fp32 ``(c_hat [n, d_c], kr_hat [n, d_r])`` from the per-token
+    region blocks of :func:`encode_tokens` / :func:`page_blocks`."""
+    n = blocks[0].shape[0]
     pc, pr = blocks[0], blocks[1]
     if fmt.meta == "paper":
         rec = blocks[2]

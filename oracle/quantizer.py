@@ -31,9 +31,16 @@ Readings taken where the paper leaves a choice (all listed in the design doc):
     byte (exact: an integer in ``[0, m]``).  Dequantization multiplies by the
     stored scale the same way.
 
-Codes are packed little-endian inside a byte: for 4 bits channel ``2j`` sits in
-bits 0-3 of byte ``j`` and channel ``2j+1`` in bits 4-7; for 2 bits channel
-``4j+k`` sits in bits ``2k..2k+1`` of byte ``j``.
+Codes are packed into little-endian 32-bit words of ``32 / bits`` consecutive
+channels (8 at 4 bits, 16 at 2 bits), stored as the word's four bytes.  Inside
+a word, channel ``2i`` occupies bits ``[bits*i, bits*(i+1))`` and channel
+``2i+1`` the same bits of the upper 16-bit half, i.e. bits
+``[16 + bits*i, 16 + bits*(i+1))``.  For 4 bits the word of channels 0..7
+holds channels 0, 2, 4, 6 in its low half (bytes 0-1) and 1, 3, 5, 7 in its
+high half (bytes 2-3); for 2 bits the low half holds channels 0, 2, ..., 14
+and the high half 1, 3, ..., 15.  The paper fixes only the byte count per
+token; this order lets a decoder take a channel pair with one shift and one
+mask (:func:`pack_codes`, :func:`unpack_codes`).
 
 Pure numpy; shares no code with the GPU library.
 """

@@ -27,13 +27,21 @@ class DecodeRun:
     def __init__(self, w: syn.Workload, layer: int = 0, kind: str = "lowbit", device: str = "cuda",
                  split_tokens: int | None = None, seq_lens=None, threads: int = 16, prefill: bool = True,
                  token_cache: dict | None = None, protect=None, prot_slots=None, meta: str = "fp16",
-                 device_tokens: bool = False):
+                 device_tokens: bool = False, inputs=None):
         """``protect``: an ``mla_protect_policy`` to keep sink/recent tokens in
         bf16 (low-bit caches only); ``prot_slots``: the protection buffer of
         each sequence (default: buffer b for sequence b); ``meta``: "fp16"
         (fp16 scale and zero) or "paper" (the paper's bf16 / fp32 scales);
         ``device_tokens``: draw the tokens on the GPU
-        (:func:`synthetic.device_sequence_tokens`, for long contexts)."""
+        (:func:`synthetic.device_sequence_tokens`, for long contexts);
+        ``inputs``: explicit host inputs ``(tokens, q_lat, q_rope)`` instead of
+        the workload's seeded draws -- ``tokens[b] = (c_kv [L_b, 512],
+        k_rope [L_b, 64])`` bf16 bit patterns of every position of sequence b
+        (the last s_q are the step's new tokens), ``q_lat [B, s_q, H, 512]``,
+        ``q_rope [B, s_q, H, 64]`` bf16 bit patterns."""
+        if inputs is not None and device_tokens:
+            raise ValueError("explicit inputs are host arrays")
+        self.inputs = inputs
         if kind not in ("lowbit", "bf16"):
             raise ValueError(kind)
         if protect is not None and kind != "lowbit":
@@ -48,7 +56,12 @@ class DecodeRun:
                                    meta=mb.MLA_META_PAPER if meta == "paper" else mb.MLA_META_FP16)
         self.B, self.H, self.s_q = w.B, w.H, w.s_q
         self.tau = w.tau
-        lens = syn.seq_lens(w) if seq_lens is None else np.asarray(seq_lens, np.int32)
+        if inputs is not None:
+            lens = np.asarray([len(c) for c, _ in inputs[0]], np.int32)
+            if seq_lens is not None and not np.array_equal(lens, np.asarray(seq_lens, np.int32)):
+                raise ValueError("seq_lens disagree with the explicit tokens")
+        else:
+            lens = syn.seq_lens(w) if seq_lens is None else np.asarray(seq_lens, np.int32)
         self.lens = lens
         bt, num_pages = syn.page_table(w, lens, layer)
         self.block_table_host = bt
@@ -58,7 +71,8 @@ class DecodeRun:
         self.cache = torch.empty(num_pages * self.page_bytes, dtype=torch.uint8, device=device)
         self.block_table = _dev(bt, device)
         self.seq_lens = _dev(lens, device)
-        ql, qr = syn.queries(w, layer)
+        ql, qr = syn.queries(w, layer) if inputs is None else (np.asarray(inputs[1], np.uint16),
+                                                                  np.asarray(inputs[2], np.uint16))
         self.q_lat = _dev(ql.view(np.int16), device)
         self.q_rope = _dev(qr.view(np.int16), device)
         if protect is not None:
@@ -93,8 +107,7 @@ class DecodeRun:
         if not device_tokens:
             new_c, new_k = [], []
             for b in range(self.B):
-                L = int(lens[b])
-                c, k = syn.sequence_tokens(w, layer, b, L, start=L - self.s_q)
+                c, k = self.tokens(b, start=int(lens[b]) - self.s_q)
                 new_c.append(c)
                 new_k.append(k)
             self.new_c = _dev(np.concatenate(new_c).view(np.int16), device)
@@ -110,6 +123,27 @@ class DecodeRun:
             self._device_fill(prefill)
         elif prefill:
             self._prefill(threads)
+
+    def tokens(self, b: int, start: int = 0):
+        """Host bf16 bit patterns of positions ``[start, L_b)`` of sequence b:
+        ``(c_kv, k_rope)`` from the explicit inputs or the workload's draw."""
+        L = int(self.lens[b])
+        if self.inputs is not None:
+            c, k = self.inputs[0][b]
+            return np.asarray(c[start:L], np.uint16), np.asarray(k[start:L], np.uint16)
+        if self.device_tokens:
+            c, k = syn.device_sequence_tokens(self.w, self.layer, b, L, self.device)
+            return (c[start:].view(torch.int16).cpu().numpy().view(np.uint16),
+                    k[start:].view(torch.int16).cpu().numpy().view(np.uint16))
+        return syn.sequence_tokens(self.w, self.layer, b, L, start=start)
+
+    def queries(self, b: int):
+        """Host bf16 bit patterns ``(q_lat [s_q, H, 512], q_rope [s_q, H, 64])``
+        of sequence b."""
+        if self.inputs is not None:
+            return np.asarray(self.inputs[1][b], np.uint16), np.asarray(self.inputs[2][b], np.uint16)
+        ql, qr = syn.queries(self.w, self.layer, batch=[b])
+        return ql[0], qr[0]
 
     def _device_fill(self, prefill: bool):
         """Draw every sequence on the GPU, write its history, keep its last s_q tokens."""
@@ -156,7 +190,10 @@ class DecodeRun:
         hist = np.maximum(self.lens.astype(np.int64) - self.s_q, 0)
         tc = self.token_cache
         key = (self.w.name, self.layer)
-        if tc is not None and key in tc:
+        if self.inputs is not None:
+            source = ((b, c[:int(hist[b])], k[:int(hist[b])]) for b, (c, k) in enumerate(self.inputs[0]))
+            tc = None
+        elif tc is not None and key in tc:
             source = ((b, c, k) for b, (c, k) in enumerate(tc[key]))
         else:
             source = syn.generate_sequences(self.w, self.layer, hist, threads=threads)

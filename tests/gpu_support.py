@@ -1,17 +1,14 @@
-"""Shared helpers of the GPU parity tests: oracle-side reconstruction and the
-tolerance checks.
+"""Shared helpers of the GPU parity tests: the cache bytes the GPU wrote,
+checked byte for byte against the oracle's packing, the oracle's attention
+over the values dequantized from those bytes, and the tolerance checks.
 
-Tolerances (attention, floating point):
-  * output: mean |gpu - oracle| <= 2e-3 * RMS(oracle) over all compared
-    outputs, and for every latent channel c and row r,
-    |gpu - oracle|_rc <= 2e-2 * RMS_c + u_rc, where RMS_c is the RMS over
-    rows of the oracle's channel c and u_rc half a bf16 ulp of the oracle
-    value (the representation error of the bf16 output format).  The max
-    rule is read this way because the synthetic latents carry 10x outlier
-    channels: those channels' outputs sit an order of magnitude above the
-    global RMS, and rounding the exact result to bf16 alone moves them by
-    more than 2e-2 of the global RMS (and of their own channel RMS), for any
-    kernel;
+Parity rule (floating point), over all compared outputs of a test:
+  * max rule: max_rc (|gpu - oracle|_rc - u_rc) <= 2e-2 * RMS(oracle), with
+    u_rc half a bf16 ulp of the oracle value.  The output format is bf16, so
+    rounding even the exact result moves an element by up to u_rc; the rule
+    bounds the error beyond that representation error against the global
+    RMS of the compared outputs;
+  * mean rule: mean |gpu - oracle| <= 2e-3 * RMS(oracle);
   * lse: |gpu - oracle| <= d_r + 1e-5 * |lse| per row, with
     d_r = tau * 2^-8 * max_t sum_c |q_rc| |k_hat_tc|.  The kernels round a
     reconstructed key at most once, to fp16 (low-bit kernels, relative error
@@ -19,16 +16,19 @@ Tolerances (attention, floating point):
     logit moves by at most tau * 2^-11 * sum_c |q_c k_hat_c| plus fp32
     accumulation error -- d_r allows the bf16 unit roundoff 2^-8 -- and the
     log-sum-exp moves by at most the largest logit move;
-  * every output element: |gpu - oracle|_rc <= 1.25 * (2^-8 |out_rc| +
-    (2^-8 + 2.1 d_r) A_rc), A_rc = sum_t w_rt |c_hat_tc| with w the exact
-    attention weights.  Weights move by a factor within e^{+-2 d_r}; the
-    rounding of the probabilities (bf16 at most, unit roundoff 2^-8) and of
-    the reconstructed values (fp16, 2^-11, or none) add at most a relative
+  * every output element, in addition: |gpu - oracle|_rc <= 1.25 * (2^-8
+    |out_rc| + (2^-8 + 2.1 d_r) A_rc), A_rc = sum_t w_rt |c_hat_tc| with w
+    the exact attention weights.  Weights move by a factor within e^{+-2 d_r};
+    the rounding of the probabilities (bf16 at most, unit roundoff 2^-8) and
+    of the reconstructed values (fp16, 2^-11, or none) add at most a relative
     2^-8 + 2^-11 per term (the factor 1.25 covers the 2^-11), and the bf16
     output adds 2^-8 |out|.
-    This bound holds for any row, including rows whose output is a single
-    key with 10x outlier channels, where bf16 output rounding alone exceeds
-    2e-2 of the output RMS.
+
+Cache bytes: before any attention comparison the pages of the compared
+sequence are copied back from the GPU and compared byte for byte with the
+oracle's quantize-and-pack of the same tokens (low-bit caches; BF16 caches:
+the rows bit for bit; protection buffers: every protected row); the oracle
+then dequantizes the GPU's own bytes.
 """
 from __future__ import annotations
 
@@ -37,12 +37,11 @@ import numpy as np
 from oracle import attention as at
 from oracle import paged_cache as pc
 from oracle import protection as pr
-from oracle import quantizer as qz
-from paper_2609_36760_amd import synthetic as syn
 
 MAX_TOL = 2e-2
 MEAN_TOL = 2e-3
 D_C = 512
+PAGE = 64
 
 
 def bf16_bits_to_f64(t) -> np.ndarray:
@@ -50,13 +49,74 @@ def bf16_bits_to_f64(t) -> np.ndarray:
     return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
 
 
-def reconstructed_sequence(w, layer, b, L, kind, meta="fp16"):
-    """Oracle reconstruction of sequence b's cache (fp32 [L, 512], [L, 64])."""
-    c_bits, r_bits = w.layers[layer]
-    c, k = syn.sequence_tokens(w, layer, b, L)
-    if kind == "bf16":
-        return qz.bf16_bits_to_f32(c), qz.bf16_bits_to_f32(k)
-    return pc.encode_sequence_dense(pc.CacheFormat(c_bits=c_bits, r_bits=r_bits, meta=meta), c, k)
+def half_ulp_bf16(y) -> np.ndarray:
+    """Half a bf16 ulp at |y| (the larger ulp for values that round up to a
+    power of two); 0 at y = 0."""
+    ay = np.abs(np.asarray(y, np.float64)) * (1 + 2.0 ** -7)
+    return np.where(ay > 0, np.exp2(np.floor(np.log2(np.maximum(ay, 1e-300))) - 8), 0.0)
+
+
+def oracle_format(run) -> pc.CacheFormat:
+    return pc.CacheFormat(c_bits=run.c_bits, r_bits=run.r_bits, meta=run.meta)
+
+
+def gpu_pages(run, b: int) -> np.ndarray:
+    """The pages of sequence b, in sequence order, copied from the GPU cache
+    (``[n_pages, page_bytes]`` uint8)."""
+    import torch
+    L = int(run.lens[b])
+    ids = run.block_table_host[b][: (L + PAGE - 1) // PAGE].astype(np.int64)
+    pages = run.cache.view(run.num_pages, run.page_bytes)[torch.from_numpy(ids).to(run.cache.device)]
+    return pages.cpu().numpy()
+
+
+def cache_values(run, b: int, c_bits=None, k_bits=None):
+    """Byte-exact check of sequence b's cache against the oracle, then the
+    values attention reads: ``(c [L, 512], k [L, 64])`` fp64 dequantized from
+    the GPU-written bytes (BF16 caches: the stored rows)."""
+    L = int(run.lens[b])
+    if c_bits is None:
+        c_bits, k_bits = run.tokens(b)
+    pages = gpu_pages(run, b)
+    if run.kind == "bf16":
+        rows = pages.view(np.uint16).reshape(-1, 576)[:L]
+        assert np.array_equal(rows[:, :512], c_bits) and np.array_equal(rows[:, 512:], k_bits), \
+            f"BF16 cache rows of sequence {b} differ from the tokens"
+        return bf16_bits_to_f64(rows[:, :512]), bf16_bits_to_f64(rows[:, 512:])
+    fmt = oracle_format(run)
+    got = pc.page_blocks(fmt, pages, L)
+    want = pc.encode_tokens(fmt, c_bits, k_bits)
+    for r, (g, e) in enumerate(zip(got, want)):
+        if not np.array_equal(g, e):
+            bad = np.nonzero((g != e).any(axis=1))[0]
+            raise AssertionError(f"sequence {b}: region {r} of {len(bad)} tokens differs from the oracle's "
+                                 f"packing (first at position {bad[0]})")
+    c_hat, kr_hat = pc.decode_blocks(fmt, got)
+    return c_hat.astype(np.float64), kr_hat.astype(np.float64)
+
+
+def protected_values(run, b: int):
+    """As :func:`cache_values` under BF16 protection: the packed copy of every
+    token byte-exact, every row of P_L in the sequence's protection buffer equal
+    to the token's bf16 bits; the representation attention reads (the bf16 row
+    inside P_L, the dequantized GPU bytes elsewhere)."""
+    L = int(run.lens[b])
+    c_bits, k_bits = run.tokens(b)
+    c_hat, kr_hat = cache_values(run, b, c_bits, k_bits)
+    sink, recent = run.protect.sink, run.protect.recent
+    slot = int(run.prot_slot_host[b])
+    rows = sink + recent
+    buf = run.prot.view(run.num_prot, run.prot_bytes)[slot].cpu().numpy().view(np.uint16).reshape(rows, 576)
+    pos, cb, kb = pr.read_protection(buf, L, 512, sink, recent)
+    assert np.array_equal(cb, c_bits[pos]) and np.array_equal(kb, k_bits[pos]), \
+        f"protection rows of sequence {b} differ from the tokens"
+    keep = pr.protected_mask(L, sink, recent)
+    c = c_hat.copy()
+    k = kr_hat.copy()
+    c[pos] = bf16_bits_to_f64(cb)
+    k[pos] = bf16_bits_to_f64(kb)
+    assert keep.sum() == len(pos)
+    return c, k
 
 
 def lse_bound(q_lat_bits, q_rope_bits, c_hat, kr_hat, tau, L, s_q):
@@ -68,98 +128,6 @@ def lse_bound(q_lat_bits, q_rope_bits, c_hat, kr_hat, tau, L, s_q):
     lim = at.decode_limits(L, s_q, H)
     mag = np.where(np.arange(L)[None, :] < lim[:, None], mag, 0.0)
     return tau * 2.0 ** -8 * mag.max(axis=1)
-
-
-class AttnStats:
-    """Accumulates output and lse errors over many compared rows."""
-
-    def __init__(self):
-        self.abs_sum = 0.0
-        self.abs_max = 0.0
-        self.sq_sum = 0.0
-        self.n = 0
-        self.lse_excess = -np.inf
-        self.lse_max_err = 0.0
-
-    def add(self, got_out, want_out, got_lse=None, want_lse=None, bound=None, elem_tol=None):
-        d = np.abs(np.asarray(got_out, np.float64) - want_out)
-        if elem_tol is not None:
-            ex = d - np.asarray(elem_tol)
-            self.elem_excess = max(getattr(self, "elem_excess", -np.inf), float(ex.max()))
-            self.elem_ratio = max(getattr(self, "elem_ratio", 0.0), float((d / np.asarray(elem_tol)).max()))
-        self.abs_sum += float(d.sum())
-        self.abs_max = max(self.abs_max, float(d.max()))
-        wo = np.asarray(want_out, np.float64)
-        self.sq_sum += float((wo ** 2).sum())
-        self.n += d.size
-        # error beyond the bf16 output's own half-ulp representation error
-        ay = np.abs(wo) * (1 + 2.0 ** -7)
-        half_ulp = np.where(ay > 0, np.exp2(np.floor(np.log2(np.maximum(ay, 1e-300))) - 8), 0.0)
-        d2 = np.maximum(d - half_ulp, 0.0).reshape(-1, D_C)
-        if not hasattr(self, "ch_max"):
-            self.ch_max = np.zeros(D_C)
-            self.ch_sq = np.zeros(D_C)
-            self.ch_n = 0
-        self.ch_max = np.maximum(self.ch_max, d2.max(axis=0))
-        self.ch_sq += (wo.reshape(-1, D_C) ** 2).sum(axis=0)
-        self.ch_n += d2.shape[0]
-        if got_lse is not None:
-            e = np.abs(np.asarray(got_lse, np.float64).reshape(-1) - np.asarray(want_lse).reshape(-1))
-            lim = np.asarray(bound).reshape(-1) + 1e-5 * np.abs(np.asarray(want_lse).reshape(-1))
-            self.lse_excess = max(self.lse_excess, float((e - lim).max()))
-            self.lse_max_err = max(self.lse_max_err, float(e.max()))
-
-    def check(self, label="", rms_max=True):
-        """Assert the bounds.  ``rms_max`` applies the per-channel max-abs rule
-        (small edge-case batches, whose channel RMS is dominated by a few rows,
-        rely on the per-element bound instead)."""
-        rms = np.sqrt(self.sq_sum / self.n)
-        mean = self.abs_sum / self.n
-        ch_rms = np.sqrt(self.ch_sq / self.ch_n)
-        ch_ratio = float((self.ch_max / ch_rms).max())
-        msg = (f"{label}: n={self.n} rms={rms:.4g} max_abs={self.abs_max:.4g} ({self.abs_max / rms:.2e} rms) "
-               f"mean_abs={mean:.4g} ({mean / rms:.2e} rms) max_excess/channel_rms={ch_ratio:.3g} "
-               f"lse_max_err={self.lse_max_err:.3g} "
-               f"elem_err/bound={getattr(self, 'elem_ratio', float('nan')):.3g}")
-        print(msg, flush=True)
-        assert getattr(self, "elem_excess", -1.0) <= 0.0, msg
-        assert mean <= MEAN_TOL * rms, msg
-        assert self.lse_excess <= 0.0, msg
-        if rms_max:
-            assert ch_ratio <= MAX_TOL, msg
-        return msg
-
-
-def check_sequence(stats, run, b, heads=None):
-    """Compare rows of sequence b of a finished DecodeRun with the oracle."""
-    w, L = run.w, int(run.lens[b])
-    c_hat, kr_hat = reconstructed_sequence(w, run.layer, b, L, run.kind, run.meta)
-    ql, qr = syn.queries(w, run.layer, batch=[b])
-    hs = np.arange(w.H) if heads is None else np.asarray(heads)
-    want_out, want_lse = at.decode_sequence(ql[0], qr[0], c_hat, kr_hat, w.tau, heads=hs)
-    got = bf16_bits_to_f64(run.out[b].cpu().numpy())[:, hs]
-    got_lse = run.lse[b].cpu().numpy()[:, hs]
-    bound = lse_bound(ql[0][:, hs], qr[0][:, hs], c_hat, kr_hat, w.tau, L, w.s_q)
-    tol = elem_bound(ql[0][:, hs], qr[0][:, hs], c_hat, kr_hat, w.tau, L, w.s_q, want_out, bound)
-    stats.add(got, want_out, got_lse, want_lse, bound, tol)
-
-
-def check_sequence_protected(stats, run, b, heads=None):
-    """As :func:`check_sequence` for a run under BF16 protection: the oracle
-    attends every token in its single representation (bf16 inside P_L)."""
-    w, L = run.w, int(run.lens[b])
-    c_bits, r_bits = w.layers[run.layer]
-    c, k = syn.sequence_tokens(w, run.layer, b, L)
-    c_rep, k_rep = pr.representation(pc.CacheFormat(c_bits=c_bits, r_bits=r_bits, meta=run.meta), c, k,
-                                     run.protect.sink, run.protect.recent)
-    ql, qr = syn.queries(w, run.layer, batch=[b])
-    hs = np.arange(w.H) if heads is None else np.asarray(heads)
-    want_out, want_lse = at.decode_sequence(ql[0], qr[0], c_rep, k_rep, w.tau, heads=hs)
-    got = bf16_bits_to_f64(run.out[b].cpu().numpy())[:, hs]
-    got_lse = run.lse[b].cpu().numpy()[:, hs]
-    bound = lse_bound(ql[0][:, hs], qr[0][:, hs], c_rep, k_rep, w.tau, L, w.s_q)
-    tol = elem_bound(ql[0][:, hs], qr[0][:, hs], c_rep, k_rep, w.tau, L, w.s_q, want_out, bound)
-    stats.add(got, want_out, got_lse, want_lse, bound, tol)
 
 
 def elem_bound(q_lat_bits, q_rope_bits, c_hat, kr_hat, tau, L, s_q, want_out, dz):
@@ -176,3 +144,105 @@ def elem_bound(q_lat_bits, q_rope_bits, c_hat, kr_hat, tau, L, s_q, want_out, dz
     d = np.asarray(dz).reshape(R, 1)
     tol = 1.25 * (2.0 ** -8 * np.abs(np.asarray(want_out).reshape(R, -1)) + (2.0 ** -8 + 2.1 * d) * A) + 1e-30
     return tol.reshape(np.asarray(want_out).shape)
+
+
+class AttnStats:
+    """Accumulates output and lse errors over many compared rows."""
+
+    def __init__(self):
+        self.abs_sum = 0.0
+        self.abs_max = 0.0
+        self.excess_max = 0.0
+        self.sq_sum = 0.0
+        self.n = 0
+        self.lse_excess = -np.inf
+        self.lse_max_err = 0.0
+        self.elem_excess = -np.inf
+        self.elem_ratio = 0.0
+
+    def add(self, got_out, want_out, got_lse=None, want_lse=None, bound=None, elem_tol=None):
+        want = np.asarray(want_out, np.float64)
+        d = np.abs(np.asarray(got_out, np.float64) - want)
+        if not np.all(np.isfinite(d)):
+            d = np.where(np.isfinite(d), d, np.inf)
+        if elem_tol is not None:
+            tol = np.asarray(elem_tol)
+            self.elem_excess = max(self.elem_excess, float((d - tol).max()))
+            self.elem_ratio = max(self.elem_ratio, float((d / tol).max()))
+        self.abs_sum += float(d.sum())
+        self.abs_max = max(self.abs_max, float(d.max()))
+        # error beyond the bf16 output's own half-ulp representation error
+        self.excess_max = max(self.excess_max, float(np.maximum(d - half_ulp_bf16(want), 0.0).max()))
+        self.sq_sum += float((want ** 2).sum())
+        self.n += d.size
+        if got_lse is not None:
+            wl = np.asarray(want_lse, np.float64).reshape(-1)
+            e = np.abs(np.asarray(got_lse, np.float64).reshape(-1) - wl)
+            e = np.where(np.isfinite(e), e, np.inf)
+            lim = np.asarray(bound).reshape(-1) + 1e-5 * np.abs(wl)
+            self.lse_excess = max(self.lse_excess, float((e - lim).max()))
+            self.lse_max_err = max(self.lse_max_err, float(e.max()))
+
+    @classmethod
+    def merged(cls, parts):
+        """The statistics of several accumulators taken together."""
+        out = cls()
+        for p in parts:
+            out.abs_sum += p.abs_sum
+            out.abs_max = max(out.abs_max, p.abs_max)
+            out.excess_max = max(out.excess_max, p.excess_max)
+            out.sq_sum += p.sq_sum
+            out.n += p.n
+            out.lse_excess = max(out.lse_excess, p.lse_excess)
+            out.lse_max_err = max(out.lse_max_err, p.lse_max_err)
+            out.elem_excess = max(out.elem_excess, p.elem_excess)
+            out.elem_ratio = max(out.elem_ratio, p.elem_ratio)
+        return out
+
+    def check(self, label="", quiet=False):
+        """Assert the max, mean, lse and per-element rules (module docstring)."""
+        rms = np.sqrt(self.sq_sum / self.n)
+        mean = self.abs_sum / self.n
+        msg = (f"{label}: n={self.n} rms={rms:.4g} max_abs={self.abs_max:.4g} "
+               f"max_excess={self.excess_max:.4g} ({self.excess_max / rms:.3e} rms, rule {MAX_TOL}) "
+               f"mean_abs={mean:.4g} ({mean / rms:.2e} rms, rule {MEAN_TOL}) "
+               f"lse_max_err={self.lse_max_err:.3g} elem_err/bound={self.elem_ratio:.3g}")
+        if not quiet:
+            print(msg, flush=True)
+        assert self.excess_max <= MAX_TOL * rms, msg
+        assert mean <= MEAN_TOL * rms, msg
+        assert self.lse_excess <= 0.0, msg
+        assert self.elem_excess <= 0.0, msg
+        return msg
+
+
+def compare_sequence(stats, got_out, got_lse, ql, qr, c, k, tau, s_q, heads=None):
+    """Oracle attention of one sequence over values ``c, k`` (fp64), compared
+    with the GPU's ``got_out [s_q, H, 512]`` (bf16 bits) and ``got_lse``."""
+    H = ql.shape[1]
+    hs = np.arange(H) if heads is None else np.asarray(heads)
+    L = c.shape[0]
+    want_out, want_lse = at.decode_sequence(ql, qr, c, k, tau, heads=hs)
+    got = bf16_bits_to_f64(np.asarray(got_out))[:, hs]
+    gl = np.asarray(got_lse)[:, hs]
+    bound = lse_bound(ql[:, hs], qr[:, hs], c, k, tau, L, s_q)
+    tol = elem_bound(ql[:, hs], qr[:, hs], c, k, tau, L, s_q, want_out, bound)
+    stats.add(got, want_out, gl, want_lse, bound, tol)
+
+
+def check_sequence(stats, run, b, heads=None):
+    """Compare rows of sequence b of a finished DecodeRun with the oracle,
+    which reads the values the GPU wrote (after the byte-exact check)."""
+    c, k = cache_values(run, b)
+    ql, qr = run.queries(b)
+    compare_sequence(stats, run.out[b].cpu().numpy(), run.lse[b].cpu().numpy(), ql, qr, c, k, run.tau, run.s_q,
+                     heads)
+
+
+def check_sequence_protected(stats, run, b, heads=None):
+    """As :func:`check_sequence` for a run under BF16 protection: the oracle
+    attends every token in its single representation (bf16 inside P_L)."""
+    c, k = protected_values(run, b)
+    ql, qr = run.queries(b)
+    compare_sequence(stats, run.out[b].cpu().numpy(), run.lse[b].cpu().numpy(), ql, qr, c, k, run.tau, run.s_q,
+                     heads)

@@ -7,8 +7,6 @@ launches, 4-bit and 2-bit content, the BF16 cache and 16 to 256 query rows.
 The full-size workloads run in the launch configuration the benchmark times
 and are compared on sampled sequences and heads.
 """
-import dataclasses
-
 import numpy as np
 import pytest
 
@@ -58,7 +56,7 @@ def test_decode_small_all_rows(case):
     for b in range(len(lens)):
         check_sequence(stats, run, b)
         print(f"  seq {b} L={lens[b]}: cumulative max_abs={stats.abs_max:.4g}", flush=True)
-    stats.check(name, rms_max=False)
+    stats.check(name)
 
 
 def test_split_partials_match_oracle_chunks():
@@ -78,10 +76,10 @@ def test_split_partials_match_oracle_chunks():
     pm = run.part_m.cpu().numpy().reshape(-1, R)
     ps = run.part_s.cpu().numpy().reshape(-1, R)
     po = run.part_o.float().cpu().numpy().reshape(-1, R, 512)     # normalized by part_s
-    from gpu_support import reconstructed_sequence
+    from gpu_support import cache_values
     for b in range(2):
         L = int(lens[b])
-        c_hat, kr_hat = reconstructed_sequence(w, 0, b, L, "lowbit")
+        c_hat, kr_hat = cache_values(run, b)
         ql, qr = syn.queries(w, 0, batch=[b])
         bounds = [(a, min(a + 64, L)) for a in range(0, L, 64)]
         m, s, o = at.chunk_partials(at.bf16_bits_to_f64(ql[0]).reshape(R, 512),
@@ -150,7 +148,12 @@ def test_large_score_jump_rescale():
                               out=out, lse=lse)
     torch.cuda.synchronize()
     from oracle import paged_cache as pc
-    c_hat, kr_hat = pc.encode_sequence_dense(pc.CacheFormat(c_bits=4), cb, kb)
+    ofmt = pc.CacheFormat(c_bits=4)
+    got_cache = cache.cpu().numpy()
+    want_cache = got_cache.copy()
+    pc.write_tokens(want_cache, ofmt, np.arange(L), cb, kb)
+    assert np.array_equal(got_cache, want_cache)
+    c_hat, kr_hat = pc.read_tokens(got_cache, ofmt, np.arange(L))
     want, want_lse = at.decode_sequence(ql[0], qr[0], c_hat, kr_hat, tau)
     z = at.logits(at.bf16_bits_to_f64(ql[0, 0]), at.bf16_bits_to_f64(qr[0, 0]), c_hat, kr_hat, tau)
     assert (z[:, 64:].max(1) - z[:, :32].max(1)).max() * np.log2(np.e) > 64   # the path is taken
@@ -186,7 +189,12 @@ def test_identical_keys_give_the_key():
                               torch.tensor([L], dtype=torch.int32, device=dev), 1, H, 0.07, out=out, lse=lse)
     torch.cuda.synchronize()
     from oracle import paged_cache as pc
-    c_hat, kr_hat = pc.encode_sequence_dense(pc.CacheFormat(c_bits=4), cb[:1], kb[:1])
+    ofmt = pc.CacheFormat(c_bits=4)
+    got_cache = cache.cpu().numpy()
+    want_cache = got_cache.copy()
+    pc.write_tokens(want_cache, ofmt, np.arange(L), cb, kb)
+    assert np.array_equal(got_cache, want_cache)
+    c_hat, kr_hat = pc.read_tokens(got_cache, ofmt, np.arange(1))
     got = bf16_bits_to_f64(out.cpu().numpy())[0, 0]
     # uniform weights: the output is the (bf16-rounded) reconstructed key row
     want = bf16_bits_to_f64(((c_hat[0].view(np.uint32) + 0x7FFF + ((c_hat[0].view(np.uint32) >> 16) & 1)) >> 16)
@@ -213,26 +221,37 @@ def test_empty_batch_is_noop():
 # ---- full-size workloads, launch configuration of the benchmark ---------------
 
 FULL = [
-    # (workload, layer, kind, sampled sequences, sampled heads)
-    ("tiny_b1_h16_256", 0, "lowbit", None, None),
-    ("dsv3_b32_h128_4k_c4r4", 0, "lowbit", [0, 17, 31], None),
-    ("dsv3_b32_h128_4k_c4r4", 0, "bf16", [3, 30], None),
-    ("int2_b64_h128_32k_c2r4", 0, "lowbit", [0, 63], np.arange(0, 128, 4)),
-    ("splitkv_b8_h128_128k_c4r4", 0, "lowbit", [5], np.arange(0, 128, 8)),
-    ("ragged_b96_h128_sq2_mixed", 0, "lowbit", "ends", np.arange(0, 128, 4)),
-    ("ragged_b96_h128_sq2_mixed", 1, "lowbit", "ends", np.arange(1, 128, 4)),
-    ("c4r4_b64_h128_32k", 0, "lowbit", [1, 62], np.arange(0, 128, 4)),
-    ("c4r4_b64_h128_32k", 0, "bf16", [7], np.arange(0, 128, 8)),
+    # (workload, layer, kind, sampled sequences, sampled heads, path)
+    # path "fused": the benchmark's step (append inside the decode launch, then
+    # the combine); "step": the writer launch, the decode launch, the combine
+    ("tiny_b1_h16_256", 0, "lowbit", None, None, "fused"),
+    ("dsv3_b32_h128_4k_c4r4", 0, "lowbit", [0, 17, 31], None, "fused"),
+    ("dsv3_b32_h128_4k_c4r4", 0, "lowbit", [5, 30], None, "step"),
+    ("dsv3_b32_h128_4k_c4r4", 0, "bf16", [3, 30], None, "fused"),
+    ("int2_b64_h128_32k_c2r4", 0, "lowbit", [0, 63], np.arange(0, 128, 4), "fused"),
+    ("splitkv_b8_h128_128k_c4r4", 0, "lowbit", [5], np.arange(0, 128, 8), "fused"),
+    ("ragged_b96_h128_sq2_mixed", 0, "lowbit", "ends", np.arange(0, 128, 4), "fused"),
+    ("ragged_b96_h128_sq2_mixed", 1, "lowbit", "ends", np.arange(1, 128, 4), "fused"),
+    ("c4r4_b64_h128_32k", 0, "lowbit", [1, 62], np.arange(0, 128, 4), "fused"),
+    ("c4r4_b64_h128_32k", 0, "bf16", [7], np.arange(0, 128, 8), "fused"),
 ]
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("case", FULL, ids=[f"{c[0]}-L{c[1]}-{c[2]}" for c in FULL])
+@pytest.mark.parametrize("case", FULL, ids=[f"{c[0]}-L{c[1]}-{c[2]}-{c[5]}" for c in FULL])
 def test_decode_full_size_sampled(case):
+    """Every token of the sampled sequences: the GPU-written pages byte for
+    byte against the oracle's packing, then the outputs of the sampled heads
+    against the oracle's attention over the values dequantized from those
+    bytes."""
     import torch
-    name, layer, kind, seqs, heads = case
+
+    from paper_2609_36760_amd.runner import DecodeRun
+    name, layer, kind, seqs, heads, path = case
     w = syn.WORKLOADS[name]
-    run = _run(w, layer=layer, kind=kind)
+    run = DecodeRun(w, layer=layer, kind=kind)
+    (run.fused_step if path == "fused" else run.step)()
+    torch.cuda.synchronize()
     out = run.out.cpu().numpy()
     assert np.all(np.isfinite(bf16_bits_to_f64(out)))
     if seqs is None:
@@ -243,7 +262,9 @@ def test_decode_full_size_sampled(case):
     stats = AttnStats()
     for b in seqs:
         check_sequence(stats, run, b, heads)
-    stats.check(f"{name} layer {layer} {kind}")
+        print(f"  seq {b} L={int(run.lens[b])}: cache bytes exact, cumulative max_excess={stats.excess_max:.4g}",
+              flush=True)
+    stats.check(f"{name} layer {layer} {kind} {path}")
     del run
     torch.cuda.empty_cache()
 
@@ -294,4 +315,4 @@ def test_decode_narrow_all_rows(case):
     for b in range(len(lens)):
         check_sequence(stats, run, b)
         print(f"  seq {b} L={lens[b]}: cumulative max_abs={stats.abs_max:.4g}", flush=True)
-    stats.check(name, rms_max=False)
+    stats.check(name)

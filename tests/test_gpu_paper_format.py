@@ -51,7 +51,7 @@ def test_paper_format_decode_small_all_rows(case):
     for b in range(len(lens)):
         (check_sequence if prot is None else check_sequence_protected)(stats, run, b)
         print(f"  seq {b} L={lens[b]}: cumulative max_abs={stats.abs_max:.4g}", flush=True)
-    stats.check(name, rms_max=False)
+    stats.check(name)
 
 
 @pytest.mark.slow
