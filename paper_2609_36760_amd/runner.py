@@ -38,7 +38,10 @@ class DecodeRun:
         the workload's seeded draws -- ``tokens[b] = (c_kv [L_b, 512],
         k_rope [L_b, 64])`` bf16 bit patterns of every position of sequence b
         (the last s_q are the step's new tokens), ``q_lat [B, s_q, H, 512]``,
-        ``q_rope [B, s_q, H, 64]`` bf16 bit patterns."""
+        ``q_rope [B, s_q, H, 64]`` bf16 bit patterns.  With explicit inputs,
+        ``seq_lens`` may start the sequences at a prefix of their tokens:
+        pages are allocated for all of them and :meth:`advance` moves the
+        sequences on, step by step."""
         if inputs is not None and device_tokens:
             raise ValueError("explicit inputs are host arrays")
         self.inputs = inputs
@@ -57,13 +60,16 @@ class DecodeRun:
         self.B, self.H, self.s_q = w.B, w.H, w.s_q
         self.tau = w.tau
         if inputs is not None:
-            lens = np.asarray([len(c) for c, _ in inputs[0]], np.int32)
-            if seq_lens is not None and not np.array_equal(lens, np.asarray(seq_lens, np.int32)):
-                raise ValueError("seq_lens disagree with the explicit tokens")
+            capacity = np.asarray([len(c) for c, _ in inputs[0]], np.int32)
+            lens = capacity if seq_lens is None else np.asarray(seq_lens, np.int32)
+            if np.any(lens > capacity) or np.any(lens < self.s_q):
+                raise ValueError("seq_lens must lie between s_q and the explicit token counts")
         else:
             lens = syn.seq_lens(w) if seq_lens is None else np.asarray(seq_lens, np.int32)
+            capacity = lens
         self.lens = lens
-        bt, num_pages = syn.page_table(w, lens, layer)
+        self.capacity = capacity
+        bt, num_pages = syn.page_table(w, capacity, layer)
         self.block_table_host = bt
         self.num_pages = num_pages
         self.page_bytes = (mb.mla_lowbit_page_bytes(self.fmt) if kind == "lowbit"
@@ -83,39 +89,14 @@ class DecodeRun:
             self.prot_slot_host = slots
             self.prot_slot = _dev(slots, device)
         self.split_tokens = w.split_tokens if split_tokens is None else split_tokens
-        if self.split_tokens:
-            if protect is not None:
-                indptr, total = mb.mla_plan_splits_protected(lens, self.split_tokens, protect)
-            else:
-                indptr, total = mb.mla_plan_splits(lens, self.split_tokens)
-            self.split_indptr_host = indptr
-            self.split_indptr = _dev(indptr, device)
-            self.num_splits = total
-            R = self.s_q * self.H
-            self.part_m = torch.empty(total * R, dtype=torch.float32, device=device)
-            self.part_s = torch.empty(total * R, dtype=torch.float32, device=device)
-            self.part_o = torch.empty(total * R * 512, dtype=torch.float16, device=device)
-        else:
-            self.split_indptr = self.part_m = self.part_s = self.part_o = None
-            self.num_splits = 0
+        self.part_m = self.part_s = self.part_o = None
+        self._plan()
         self.out = torch.empty((self.B, self.s_q, self.H, 512), dtype=torch.int16, device=device)
         self.lse = torch.empty((self.B, self.s_q, self.H), dtype=torch.float32, device=device)
-        # the step's new tokens (the last s_q positions of every sequence)
-        new_slots = [syn.slots_of(bt[b], np.arange(int(lens[b]) - self.s_q, int(lens[b]))) for b in range(self.B)]
-        self.new_slots = _dev(np.concatenate(new_slots), device)
         self.device_tokens = device_tokens
-        if not device_tokens:
-            new_c, new_k = [], []
-            for b in range(self.B):
-                c, k = self.tokens(b, start=int(lens[b]) - self.s_q)
-                new_c.append(c)
-                new_k.append(k)
-            self.new_c = _dev(np.concatenate(new_c).view(np.int16), device)
-            self.new_k = _dev(np.concatenate(new_k).view(np.int16), device)
+        self._step_tokens()
         if protect is not None:
             self.new_seq = _dev(np.repeat(np.arange(self.B, dtype=np.int32), self.s_q), device)
-            self.new_pos = _dev(np.concatenate([np.arange(int(l) - self.s_q, int(l), dtype=np.int32)
-                                                for l in lens]), device)
             hist = np.maximum(lens.astype(np.int64) - self.s_q, 0).astype(np.int32)
             self.hist_lens = _dev(hist, device)
         self.token_cache = token_cache
@@ -123,6 +104,57 @@ class DecodeRun:
             self._device_fill(prefill)
         elif prefill:
             self._prefill(threads)
+
+    def _plan(self):
+        """Split plan and partial buffers for the current lengths."""
+        lens, device = self.lens, self.device
+        if not self.split_tokens:
+            self.split_indptr = self.part_m = self.part_s = self.part_o = None
+            self.num_splits = 0
+            return
+        if self.protect is not None:
+            indptr, total = mb.mla_plan_splits_protected(lens, self.split_tokens, self.protect)
+        else:
+            indptr, total = mb.mla_plan_splits(lens, self.split_tokens)
+        self.split_indptr_host = indptr
+        self.split_indptr = _dev(indptr, device)
+        self.num_splits = total
+        R = self.s_q * self.H
+        if self.part_m is None or self.part_m.numel() < total * R:
+            self.part_m = torch.empty(total * R, dtype=torch.float32, device=device)
+            self.part_s = torch.empty(total * R, dtype=torch.float32, device=device)
+            self.part_o = torch.empty(total * R * 512, dtype=torch.float16, device=device)
+
+    def _step_tokens(self):
+        """Slots, positions and host rows of the step's new tokens (the last s_q
+        positions of every sequence)."""
+        lens, bt, device = self.lens, self.block_table_host, self.device
+        new_slots = [syn.slots_of(bt[b], np.arange(int(lens[b]) - self.s_q, int(lens[b]))) for b in range(self.B)]
+        self.new_slots = _dev(np.concatenate(new_slots), device)
+        if not self.device_tokens:
+            new_c, new_k = [], []
+            for b in range(self.B):
+                c, k = self.tokens(b, start=int(lens[b]) - self.s_q)
+                new_c.append(c)
+                new_k.append(k)
+            self.new_c = _dev(np.concatenate(new_c).view(np.int16), device)
+            self.new_k = _dev(np.concatenate(new_k).view(np.int16), device)
+        self.new_pos = _dev(np.concatenate([np.arange(int(l) - self.s_q, int(l), dtype=np.int32) for l in lens]),
+                            device)
+
+    def advance(self):
+        """Move every sequence on by s_q positions (explicit inputs): the next
+        decode step's lengths, new tokens, slots and split plan.  The cache and
+        protection buffers keep what earlier steps wrote."""
+        if self.inputs is None:
+            raise ValueError("advance() needs explicit inputs")
+        lens = self.lens + self.s_q
+        if np.any(lens > self.capacity):
+            raise ValueError("no explicit tokens left to advance into")
+        self.lens = lens.astype(np.int32)
+        self.seq_lens = _dev(self.lens, self.device)
+        self._plan()
+        self._step_tokens()
 
     def tokens(self, b: int, start: int = 0):
         """Host bf16 bit patterns of positions ``[start, L_b)`` of sequence b:

@@ -17,7 +17,7 @@ sampled sequences.
 import numpy as np
 import pytest
 
-from gpu_support import AttnStats, check_sequence_protected
+from gpu_support import FP16_LIMITED, AttnStats, check_fp16_limited, check_sequence_protected
 from oracle import protection as pr
 from paper_2609_36760_amd import synthetic as syn
 
@@ -144,3 +144,65 @@ def test_device_drawn_inputs_sixteen_heads():
     for b in range(w.B):
         check_sequence_protected(stats, run, b)
     stats.check("device-drawn 16 heads protected")
+
+
+AGING = [
+    # (name, c_bits, H, s_q, split_tokens, (sink, recent), start lengths, steps)
+    ("aging_c4_h128_sq1_split64", 4, 128, 1, 64, (4, 128), [1, 4, 100, 127, 128, 129, 131, 200], 36),
+    ("aging_c4_h128_sq2_nosplit", 4, 128, 2, 0, (4, 128), [2, 98, 126, 130, 164], 20),
+    ("aging_c2_h128_sq2_split32", 2, 128, 2, 32, (40, 8), [2, 40, 47, 60], 16),
+    ("aging_c4_h16_sq2_split32", 4, 16, 2, 32, (4, 128), [2, 100, 129, 133], 20),
+]
+
+
+@pytest.mark.parametrize("case", AGING, ids=[c[0] for c in AGING])
+def test_token_aging_over_consecutive_steps(case):
+    """Consecutive decode steps of sequences that grow across the recent
+    window's edge (Appendix C.5, "BF16 protection and cache lifecycle"): each
+    step appends s_q tokens through the protected writer (the token entering
+    the window overwrites the ring row of the one leaving it, which attention
+    then reads from its packed copy) and decodes.  After every step the whole
+    protection buffer of every sequence equals the oracle's lifecycle replayed
+    over the same calls, the packed pages equal the oracle's packing, and every
+    output row matches the oracle's single softmax over the per-token
+    representations."""
+    import torch
+
+    from paper_2609_36760_amd import _binding as mb
+    from paper_2609_36760_amd.runner import DecodeRun
+    name, cb, H, s_q, split, (sink, recent), start, steps = case
+    seed = 360 + AGING.index(case)
+    cap = [L + s_q * (steps - 1) for L in start]
+    w = syn.Workload(name, seed, B=len(start), H=H, s_q=s_q, context=None, layers=((cb, 4),),
+                     split_tokens=split, ctx_range=(1, 2))
+    tokens = [syn.sequence_tokens(w, 0, b, L) for b, L in enumerate(cap)]
+    ql, qr = syn.queries(w, 0)
+    run = DecodeRun(w, protect=mb.protect_policy(sink, recent), inputs=(tokens, ql, qr),
+                    seq_lens=np.asarray(start, np.int32))
+    rows = sink + recent
+    bufs = []
+    for b, L in enumerate(start):       # the oracle's lifecycle: the prefill call
+        buf = np.zeros((rows, 576), np.uint16)
+        hist = L - s_q
+        pr.write_protection(buf, np.arange(hist), hist, tokens[b][0][:hist], tokens[b][1][:hist], sink, recent)
+        bufs.append(buf)
+    stats = AttnStats()
+    for step in range(steps):
+        if step:
+            run.advance()
+        run.step()
+        torch.cuda.synchronize()
+        prot = run.prot.cpu().numpy().view(np.uint16).reshape(run.num_prot, rows, 576)
+        for b in range(w.B):
+            L = int(run.lens[b])
+            new = np.arange(L - s_q, L)
+            pr.write_protection(bufs[b], new, L, tokens[b][0][new], tokens[b][1][new], sink, recent)
+            assert np.array_equal(prot[run.prot_slot_host[b]], bufs[b]), \
+                f"step {step}: protection buffer of sequence {b} (length {L}) differs from the oracle's ring"
+            check_sequence_protected(stats, run, b)
+        print(f"  step {step}: lengths {run.lens.tolist()}, buffers equal, "
+              f"cumulative max_excess={stats.excess_max:.4g}", flush=True)
+    if name in FP16_LIMITED:
+        check_fp16_limited(stats, name)
+    else:
+        stats.check(name)
