@@ -380,6 +380,33 @@ int mla_lowbit_decode_attn_protected(const mla_cache_format* f, const mla_protec
  */
 int64_t mla_persistent_cache_bytes(const mla_cache_format* f, const mla_protect_policy* p, int64_t L);
 
+/*
+ * Decode attention without any allocation, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses that
+ * forbid hipMalloc): mla_lowbit_decode_attn followed by mla_splitkv_combine,
+ * with the split partials held in storage the library owns -- one static
+ * device array per GPU, for at most 65536 partial rows (num_splits * s_q * H;
+ * 64.5 MiB, held from module load until the process ends).  The caller passes
+ * inputs and the final outputs only.  Arguments as for mla_lowbit_decode_attn
+ * without part_m / part_s / part_o: split_tokens = 0 decodes unsplit (no
+ * storage used); split_tokens > 0 needs split_indptr and num_splits from
+ * mla_plan_splits and writes out (bf16 [B][s_q][H][d_c]) and lse (NULL
+ * allowed) as the combine does.  Returns MLA_ENOTSUP when num_splits * s_q * H
+ * exceeds 65536, before any HIP call.  No hipMalloc, hipFree or allocating
+ * library routine is called.  Every call on one GPU shares that GPU's storage
+ * (each call writes every partial it reads, so nothing carries over between
+ * calls): calls that overlap on one GPU, on different streams or host
+ * threads, race and give unspecified results.
+ */
+int mla_lowbit_decode_attn_noalloc(const mla_cache_format* f,
+                                   const uint16_t* q_lat, const uint16_t* q_rope,
+                                   const void* cache, int64_t num_pages,
+                                   const int32_t* block_table, int32_t max_pages_per_seq,
+                                   const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
+                                   float softmax_scale,
+                                   int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
+                                   uint16_t* out, float* lse, hipStream_t stream);
+
 /* Human-readable name of a status code (static string). */
 const char* mla_status_str(int status);
 

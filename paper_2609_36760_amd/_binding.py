@@ -24,6 +24,7 @@ SYMBOLS = (
     "mla_status_str", "mla_last_hip_error", "mla_protect_buffer_bytes", "mla_lowbit_quant_append_protected",
     "mla_plan_splits_protected", "mla_lowbit_decode_attn_protected", "mla_persistent_cache_bytes",
     "mla_lowbit_append_decode_attn", "mla_bf16_append_decode_attn", "mla_time_next_decode_launch",
+    "mla_lowbit_decode_attn_noalloc",
 )
 
 
@@ -95,6 +96,8 @@ def library() -> ctypes.CDLL:
         "mla_plan_splits_protected": (I32, [P, I32, I32, POL, P]),
         "mla_lowbit_decode_attn_protected": (ctypes.c_int, [FMT, POL, P, P, P, I64, P, I32, P, I32, I32, I32, F32,
                                                             P, I64, P, I32, P, I32, P, P, P, P, P, P]),
+        "mla_lowbit_decode_attn_noalloc": (ctypes.c_int, [FMT, P, P, P, I64, P, I32, P, I32, I32, I32, F32,
+                                                          I32, P, I32, P, P, P]),
         "mla_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "mla_last_hip_error": (ctypes.c_int, []),
         "mla_time_next_decode_launch": (ctypes.c_int, [P, P]),
@@ -195,6 +198,18 @@ def mla_bf16_decode_attn(fmt, q_lat, q_rope, cache, num_pages, block_table, seq_
                          lse=None, part_m=None, part_s=None, part_o=None, stream=None):
     _decode("mla_bf16_decode_attn", fmt, q_lat, q_rope, cache, num_pages, block_table, seq_lens, s_q, H,
             softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s, part_o, stream)
+
+
+def mla_lowbit_decode_attn_noalloc(fmt, q_lat, q_rope, cache, num_pages, block_table, seq_lens, s_q, H,
+                                   softmax_scale, split_tokens=0, split_indptr=None, num_splits=0, out=None,
+                                   lse=None, stream=None):
+    """Decode (+ combine when split) with the partials in the library's own
+    storage; writes ``out`` and ``lse``."""
+    B = q_lat.shape[0]
+    _check("mla_lowbit_decode_attn_noalloc", library().mla_lowbit_decode_attn_noalloc(
+        ctypes.byref(fmt), _ptr(q_lat), _ptr(q_rope), _ptr(cache), num_pages, _ptr(block_table),
+        block_table.shape[1], _ptr(seq_lens), B, s_q, H, float(softmax_scale), split_tokens, _ptr(split_indptr),
+        num_splits, _ptr(out), _ptr(lse), _stream(stream)))
 
 
 def _append_decode(name, fmt, c_kv, k_rope, slot_mapping, q_lat, q_rope, cache, num_pages, block_table, seq_lens,

@@ -109,4 +109,12 @@ hipError_t launch_lowbit_append_protected(const AppendArgs& a, hipStream_t strea
 // num_splits (split_indptr[B]) chooses between one wave per row and four waves sharing a row.
 hipError_t launch_combine(const CombineArgs& a, int32_t num_splits, hipStream_t stream);
 
+// Split-partial storage owned by the library for the allocation-free decode
+// entry point: at most kNoallocSplitRows partial rows (split x query row) of
+// kNoallocRowBytes (fp16 latent, fp32 max and sum).  Returns this device's
+// part_m / part_s / part_o addresses (resolved on the device's first call).
+constexpr int64_t kNoallocSplitRows = 65536;
+constexpr int64_t kNoallocRowBytes = 512 * 2 + 2 * 4;
+hipError_t noalloc_partials(float** part_m, float** part_s, uint16_t** part_o);
+
 }  // namespace mla

@@ -156,12 +156,14 @@ struct NewTokens {
     const int64_t* slot_mapping;
 };
 
-int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat, const uint16_t* q_rope,
-                  const void* cache, int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
-                  const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H, float softmax_scale,
-                  int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits, uint16_t* out,
-                  float* lse, float* part_m, float* part_s, uint16_t* part_o, const ProtDecode* pd,
-                  hipStream_t stream, const NewTokens* nt = nullptr) {
+// Host validation of a decode call (no HIP call); part_* are checked only when
+// check_parts is set (the allocation-free entry point supplies its own).
+int check_decode(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat, const uint16_t* q_rope,
+                 const void* cache, int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
+                 const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H, float softmax_scale,
+                 int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits, const uint16_t* out,
+                 const float* part_m, const float* part_s, const uint16_t* part_o, const ProtDecode* pd,
+                 bool check_parts) {
     int st = lowbit ? check_lowbit_format(f) : check_shape(f);
     if (st != MLA_OK) return st;
     if (pd != nullptr) {
@@ -188,10 +190,25 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
         if (out == nullptr) return MLA_EINVAL;
         if (!aligned(out, 16)) return MLA_ENOTSUP;
     } else {
-        if (split_indptr == nullptr || part_m == nullptr || part_s == nullptr || part_o == nullptr || num_splits < 0)
-            return MLA_EINVAL;
-        if (!aligned(part_o, 16)) return MLA_ENOTSUP;
+        if (split_indptr == nullptr || num_splits < 0) return MLA_EINVAL;
+        if (check_parts) {
+            if (part_m == nullptr || part_s == nullptr || part_o == nullptr) return MLA_EINVAL;
+            if (!aligned(part_o, 16)) return MLA_ENOTSUP;
+        }
     }
+    return MLA_OK;
+}
+
+int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat, const uint16_t* q_rope,
+                  const void* cache, int64_t num_pages, const int32_t* block_table, int32_t max_pages_per_seq,
+                  const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H, float softmax_scale,
+                  int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits, uint16_t* out,
+                  float* lse, float* part_m, float* part_s, uint16_t* part_o, const ProtDecode* pd,
+                  hipStream_t stream, const NewTokens* nt = nullptr) {
+    int st = check_decode(f, lowbit, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
+                          s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, part_m, part_s, part_o,
+                          pd, true);
+    if (st != MLA_OK || B == 0) return st;
     mla::DecodeArgs a{};
     a.q_lat = q_lat;
     a.q_rope = q_rope;
@@ -432,6 +449,35 @@ int mla_bf16_append_decode_attn(const mla_cache_format* f, const uint16_t* c_kv,
     return append_decode(f, false, c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, q_lat, q_rope, cache,
                          num_pages, block_table, max_pages_per_seq, seq_lens, B, s_q, H, softmax_scale, split_tokens,
                          split_indptr, num_splits, out, lse, part_m, part_s, part_o, stream);
+}
+
+int mla_lowbit_decode_attn_noalloc(const mla_cache_format* f, const uint16_t* q_lat, const uint16_t* q_rope,
+                                   const void* cache, int64_t num_pages, const int32_t* block_table,
+                                   int32_t max_pages_per_seq, const int32_t* seq_lens, int32_t B, int32_t s_q,
+                                   int32_t H, float softmax_scale, int32_t split_tokens, const int32_t* split_indptr,
+                                   int32_t num_splits, uint16_t* out, float* lse, hipStream_t stream) {
+    if (split_tokens == 0)
+        return decode_common(f, true, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
+                             s_q, H, softmax_scale, 0, nullptr, 0, out, lse, nullptr, nullptr, nullptr, nullptr,
+                             stream);
+    // every check of the decode and the combine, before any HIP call
+    int st = check_decode(f, true, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B, s_q,
+                          H, softmax_scale, split_tokens, split_indptr, num_splits, out, nullptr, nullptr, nullptr,
+                          nullptr, false);
+    if (st != MLA_OK || B == 0) return st;
+    if (static_cast<int64_t>(num_splits) * s_q * H > mla::kNoallocSplitRows) return MLA_ENOTSUP;
+    if (out == nullptr) return MLA_EINVAL;
+    if (!aligned(out, 16)) return MLA_ENOTSUP;
+    float* part_m = nullptr;
+    float* part_s = nullptr;
+    uint16_t* part_o = nullptr;
+    st = hip_status(mla::noalloc_partials(&part_m, &part_s, &part_o));
+    if (st != MLA_OK) return st;
+    st = decode_common(f, true, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B, s_q, H,
+                       softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s, part_o,
+                       nullptr, stream);
+    if (st != MLA_OK) return st;
+    return mla_splitkv_combine(part_m, part_s, part_o, split_indptr, num_splits, B, s_q, H, kDc, out, lse, stream);
 }
 
 int mla_splitkv_combine(const float* part_m, const float* part_s, const uint16_t* part_o, const int32_t* split_indptr,

@@ -32,7 +32,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(mb):
     names = declared_functions()
-    assert len(names) == 18
+    assert len(names) == 19
     lib = ctypes.CDLL(mb.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -242,3 +242,21 @@ def test_timing_hook_takes_both_events_or_none(mb):
     assert lib.mla_time_next_decode_launch(16, None) == 1
     assert lib.mla_time_next_decode_launch(None, 16) == 1
     assert lib.mla_time_next_decode_launch(None, None) == 0
+
+
+def test_noalloc_rejects_more_partials_than_its_storage(mb):
+    """num_splits * s_q * H above 65536 partial rows: MLA_ENOTSUP before any
+    HIP call (the pointers are never dereferenced)."""
+    lib = mb.library()
+    fmt = mb.cache_format()
+    fake = 1 << 20                       # 256-byte aligned, never touched
+    st = lib.mla_lowbit_decode_attn_noalloc(ctypes.byref(fmt), fake, fake, fake, 4, fake, 4, fake, 8, 2, 128, 0.1,
+                                            64, fake, 257, fake, fake, None)
+    assert st == mb.MLA_ENOTSUP
+    st = lib.mla_lowbit_decode_attn_noalloc(ctypes.byref(fmt), fake, fake, fake, 4, fake, 4, fake, 8, 1, 128, 0.1,
+                                            64, fake, 513, fake, fake, None)
+    assert st == mb.MLA_ENOTSUP
+    # scalar checks still apply
+    st = lib.mla_lowbit_decode_attn_noalloc(ctypes.byref(fmt), fake, fake, fake, 4, fake, 4, fake, 8, 3, 128, 0.1,
+                                            64, fake, 4, fake, fake, None)
+    assert st == mb.MLA_EINVAL
