@@ -376,7 +376,8 @@ int mla_lowbit_decode_attn_protected(const mla_cache_format* f, const mla_protec
  * protection).  With MLA_META_PAPER, c_bits = 4 and the paper's policy this is
  * the paper's M_C4R4(L); for a BF16 format (c_bits = 16) it returns the
  * equation's M_BF16(L) = ceil(L / page_size) * mla_bf16_page_bytes.
- * Returns -1 for an invalid format, policy or L < 0.
+ * Returns -1 for an invalid format, policy, L < 0, or a byte count beyond
+ * INT64_MAX.
  */
 int64_t mla_persistent_cache_bytes(const mla_cache_format* f, const mla_protect_policy* p, int64_t L);
 

@@ -316,15 +316,20 @@ int mla_bf16_append(const mla_cache_format* f, const uint16_t* c_kv, int64_t c_k
 
 int64_t mla_persistent_cache_bytes(const mla_cache_format* f, const mla_protect_policy* p, int64_t L) {
     if (f == nullptr || L < 0) return -1;
+    constexpr int64_t kMax = INT64_MAX;
     if (f->c_bits == 16) {
         if (check_shape(f) != MLA_OK || p != nullptr) return -1;
-        return (L + f->page_size - 1) / f->page_size * bf16_geom(f).page_bytes;
+        const int64_t pages = L / f->page_size + (L % f->page_size != 0);
+        const int64_t per = bf16_geom(f).page_bytes;
+        return pages > kMax / per ? -1 : pages * per;
     }
     if (check_lowbit_format(f) != MLA_OK) return -1;
     if (p != nullptr && check_policy(p) != MLA_OK) return -1;
-    const int64_t pages = (L + f->page_size - 1) / f->page_size;
+    const int64_t pages = L / f->page_size + (L % f->page_size != 0);
     const int64_t prot = p == nullptr ? 0 : (static_cast<int64_t>(p->sink) + p->recent) * kProtRowBytes;
-    return pages * (lowbit_geom(f).page_bytes + kReverseMapBytes) + prot;
+    const int64_t per = lowbit_geom(f).page_bytes + kReverseMapBytes;
+    if (pages > (kMax - prot) / per) return -1;     // the result does not fit int64
+    return pages * per + prot;
 }
 
 int64_t mla_protect_buffer_bytes(const mla_cache_format* f, const mla_protect_policy* p) {
