@@ -1,17 +1,20 @@
 """Benchmark of the low-bit MLA decode step on one MI355X.
 
-A step is one pass of the decode hot path for one cache layer: quantize-append
-the step's new tokens, fused low-bit decode attention over the paged cache,
-and the split-KV combine.  The workload is the 128-head DeepSeek-V3-shaped
-decode batch (32 sequences x 4096 tokens, INT4 content + INT4 RoPE key).
-Successive steps cycle through 8 resident layer caches (8 x 42.5 MB), more
-than the 256 MB last-level cache holds, as a model's layer loop would.
+A step is one pass of the decode hot path for one cache layer: the step's new
+tokens quantized and appended inside the fused low-bit decode launch, decode
+attention over the paged cache, and the split-KV combine.  The headline
+workload is the 128-head INT4/INT4 decode batch of 64 sequences x 32768 tokens
+(the target shape; 680 MB of packed cache per layer).  Successive steps
+alternate between two resident layer caches, so no step finds the previous
+one's bytes in the 256 MB last-level cache.
 
-Printed: one JSON line (stdout) with whole-step decode tokens/s, the decode
-kernel's roofline (live HIP-event timing of the kernel on its stream), the
-same step over a BF16 cache (the unquantized comparison), the
-batch-64 x 32K-token target shape for both caches, and the CPU oracle timed on
-a bounded sample of the workload.
+Printed: one JSON line (stdout) with whole-step decode tokens/s at that shape,
+the decode kernel's roofline (live HIP-event timing of every timed launch on
+its own dispatch: mean, median, p10, p90), the GPU clock sampled during the
+timed steps, the same step over a BF16 cache (the unquantized comparison), the
+32 x 4096 workload, the paper's sampling protocol (graph replay, caches
+flushed before every sample, 2 runs x 2 rounds x 30 samples in alternating
+order), and the CPU oracle timed on a bounded sample of the headline workload.
 """
 from __future__ import annotations
 
@@ -28,11 +31,12 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "decode attn tokens/s + HBM GB/s & MFMA util vs peak, 128 heads, INT4/INT4 vs BF16"
-MAIN = "dsv3_b32_h128_4k_c4r4"
-TARGET = "c4r4_b64_h128_32k"
+MAIN = "c4r4_b64_h128_32k"            # the headline: 64 x 32768, INT4/INT4, 128 heads
+SMALL = "dsv3_b32_h128_4k_c4r4"       # 32 x 4096
+TARGET = MAIN
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
-LAYERS = 8
+LAYERS = {MAIN: 2, SMALL: 8}       # resident layer caches cycled by the timed steps
 
 
 def log(*a):
@@ -104,21 +108,75 @@ def algorithmic_bytes(run) -> int:
     return keys + q + rows * 512 * 2
 
 
+class ClockSampler:
+    """Samples the GPU's graphics clock (torch.cuda.clock_rate, MHz) from a
+    host thread while the timed steps run; None when the platform does not
+    report it."""
+
+    def __init__(self, period_s: float = 0.002):
+        import threading
+        self.samples, self._stop, self.period = [], threading.Event(), period_s
+        self._t = threading.Thread(target=self._run, daemon=True)
+
+    def _run(self):
+        import torch
+        while not self._stop.is_set():
+            try:
+                self.samples.append(float(torch.cuda.clock_rate()))
+            except Exception:
+                return
+            time.sleep(self.period)
+
+    def __enter__(self):
+        self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._t.join()
+
+    def summary(self):
+        if not self.samples:
+            return None
+        a = np.asarray(self.samples)
+        return {"median_mhz": float(np.median(a)), "min_mhz": float(a.min()), "max_mhz": float(a.max()),
+                "samples": int(a.size)}
+
+
+def stats_of(a):
+    a = np.asarray(a, np.float64)
+    return {"mean": float(a.mean()), "median": float(np.median(a)), "p10": float(np.percentile(a, 10)),
+            "p90": float(np.percentile(a, 90)), "n": int(a.size)}
+
+
+def make_run(name, kind, token_cache=None, protect=None, split_tokens=None, meta="fp16", layer=0,
+             device_tokens=False):
+    import torch
+
+    from paper_2609_36760_amd import synthetic as syn
+    from paper_2609_36760_amd.runner import DecodeRun
+    t0 = time.perf_counter()
+    run = DecodeRun(syn.WORKLOADS[name], layer=layer, kind=kind, token_cache=token_cache, protect=protect,
+                    split_tokens=split_tokens, meta=meta, device_tokens=device_tokens)
+    torch.cuda.synchronize()
+    log(f"[{name} {kind}] setup {time.perf_counter() - t0:.1f}s, cache {run.cache.numel() / 1e6:.1f} MB")
+    return run
+
+
 def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=None, split_tokens=None,
-                  meta="fp16", layer=0, device_tokens=False):
+                  meta="fp16", layer=0, device_tokens=False, run=None, clock=False):
+    """Time ``steps`` steps after ``warmup`` untimed ones, cycling ``layers``
+    resident caches; returns the step and per-launch kernel figures."""
     import torch
 
     from paper_2609_36760_amd import _binding as mb
-    from paper_2609_36760_amd import synthetic as syn
-    from paper_2609_36760_amd.runner import DecodeRun
-    w = syn.WORKLOADS[name]
-    t0 = time.perf_counter()
-    run = DecodeRun(w, layer=layer, kind=kind, token_cache=token_cache, protect=protect, split_tokens=split_tokens,
-                    meta=meta, device_tokens=device_tokens)
+    own = run is None
+    if own:
+        run = make_run(name, kind, token_cache, protect, split_tokens, meta, layer, device_tokens)
+    protect = run.protect
     caches = [run.cache] + [run.cache.clone() for _ in range(layers - 1)]
     prots = [None] * layers if protect is None else [run.prot] + [run.prot.clone() for _ in range(layers - 1)]
     torch.cuda.synchronize()
-    log(f"[{name} {kind}] setup {time.perf_counter() - t0:.1f}s, cache {run.cache.numel() / 1e6:.1f} MB x {layers}")
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
 
@@ -148,19 +206,24 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
                 part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
         if run.split_tokens:
             mb.mla_splitkv_combine(run.part_m, run.part_s, run.part_o, run.split_indptr, run.num_splits, run.B,
-                                   run.s_q, run.H,
-                                   run.out, run.lse, stream=sh)
+                                   run.s_q, run.H, run.out, run.lse, stream=sh)
 
     for i in range(warmup):
         one_step(i)
     evs = TimingEvents(steps)
     torch.cuda.synchronize()
+    sampler = ClockSampler() if clock else None
+    if sampler is not None:
+        sampler.__enter__()
     t0 = time.perf_counter()
     for i in range(warmup, warmup + steps):
         one_step(i, evs)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    kern_ms = float(np.mean([evs.elapsed_ms(k) for k in range(steps)]))
+    if sampler is not None:
+        sampler.__exit__(None, None, None)
+    kern = [evs.elapsed_ms(k) for k in range(steps)]
+    kern_ms = float(np.mean(kern))
     ms_step = wall * 1e3 / steps
     flops = run.flops()
     nbytes = algorithmic_bytes(run)
@@ -169,33 +232,105 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
         "decode_tokens_per_s": run.B * run.s_q / (ms_step * 1e-3),
         "kv_tokens_per_s": float(run.lens.sum()) / (ms_step * 1e-3),
         "decode_kernel_ms": kern_ms,
+        "decode_kernel_ms_stats": stats_of(kern),
         "decode_kernel_tflops": flops / (kern_ms * 1e-3) / 1e12,
         "decode_kernel_gbs": nbytes / (kern_ms * 1e-3) / 1e9,
         "flops_per_launch": flops, "bytes_per_launch": nbytes,
-        "splits": run.num_splits,
+        "splits": run.num_splits, "split_tokens": run.split_tokens, "layers_cycled": layers,
     }
     res["mfma_frac"] = res["decode_kernel_tflops"] / PEAK_BF16_TFLOPS
     res["hbm_frac"] = res["decode_kernel_gbs"] / PEAK_HBM_GBS
+    if sampler is not None:
+        res["gpu_clock"] = sampler.summary()
     if protect is not None:
         res["protect"] = {"sink": protect.sink, "recent": protect.recent}
     tag = ("" if protect is None else " protected") + ("" if meta == "fp16" else f" {meta} metadata")
-    log(f"[{name} {kind}{tag}] {ms_step * 1e3:.1f} us/step, decode kernel {kern_ms * 1e3:.1f} us = "
+    log(f"[{name} {kind}{tag}] {ms_step * 1e3:.1f} us/step, decode kernel {kern_ms * 1e3:.1f} us "
+        f"(median {res['decode_kernel_ms_stats']['median'] * 1e3:.1f}) = "
         f"{res['decode_kernel_tflops']:.1f} TFLOP/s ({100 * res['mfma_frac']:.1f}% MFMA), "
-        f"{res['decode_kernel_gbs']:.0f} GB/s ({100 * res['hbm_frac']:.1f}% HBM)")
-    del run, caches, prots
-    torch.cuda.empty_cache()
+        f"{res['decode_kernel_gbs']:.0f} GB/s ({100 * res['hbm_frac']:.1f}% HBM)"
+        + (f", clock {res['gpu_clock']}" if sampler is not None else ""))
+    del caches, prots
+    if own:
+        del run
+        torch.cuda.empty_cache()
     return res
 
 
-def cpu_baseline(budget_s: float = 12.0):
-    """The oracle, as it stands, on whole sequences of the main workload."""
+def latency_protocol(runs, runs_per=2, rounds=2, samples=30, flush_bytes=1 << 30):
+    """The paper's kernel-latency protocol (Appendix F.1): attention + combine
+    replayed from a captured HIP graph, the L2 and last-level caches flushed
+    (a 1 GiB write) before every sample, HIP events around the replay,
+    ``runs_per`` runs x ``rounds`` rounds x ``samples`` samples with the
+    kinds' order alternating between rounds.  ``runs``: {label: DecodeRun}."""
+    import torch
+    flush = torch.empty(flush_bytes, dtype=torch.uint8, device="cuda")
+    graphs, mode = {}, "graph"
+    for label, run in runs.items():
+        run.attend()                                 # warm, outside the capture
+        torch.cuda.synchronize()
+        try:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                run.attend()
+            graphs[label] = g.replay
+        except Exception as e:                       # the capture failed: time eager launches
+            log(f"graph capture of {label} failed ({e}); timing eager launches")
+            graphs[label] = run.attend
+            mode = "eager"
+    torch.cuda.synchronize()
+    lat = {label: [] for label in runs}
+    labels = list(runs)
+    stream = torch.cuda.current_stream()
+    for r in range(runs_per):
+        for rd in range(rounds):
+            order = labels if (r + rd) % 2 == 0 else labels[::-1]
+            for label in order:
+                for i in range(samples):
+                    flush.fill_((r * 7 + rd * 3 + i) & 0xFF)
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    graphs[label]()
+                    e1.record(stream)
+                    torch.cuda.synchronize()
+                    lat[label].append(e0.elapsed_time(e1) * 1e3)
+    del flush
+    torch.cuda.empty_cache()
+    out = {"replay": mode, "runs": runs_per, "rounds": rounds, "samples_per_round": samples,
+           "flush_bytes": flush_bytes, "unit": "us"}
+    for label, v in lat.items():
+        out[label] = stats_of(v)
+        log(f"[protocol {label}] {mode}: mean {out[label]['mean']:.1f} us, median {out[label]['median']:.1f}, "
+            f"p10 {out[label]['p10']:.1f}, p90 {out[label]['p90']:.1f}")
+    return out
+
+
+def environment():
+    import platform
+
+    import torch
+    rocm = None
+    try:
+        rocm = open("/opt/rocm/.info/version").read().strip()
+    except OSError:
+        pass
+    props = torch.cuda.get_device_properties(0)
+    return {"device": props.name, "gcn_arch": getattr(props, "gcnArchName", None),
+            "compute_units": props.multi_processor_count, "rocm": rocm, "torch_hip": torch.version.hip,
+            "host_cpus": os.cpu_count(), "python": platform.python_version()}
+
+
+def cpu_baseline(budget_s: float = 15.0):
+    """The oracle, as it stands, on whole sequences of the headline workload
+    (quantize and pack of every cached token, then fp64 attention of all
+    heads), for about ``budget_s`` seconds."""
     from oracle import attention as at
     from oracle import paged_cache as pc
     from paper_2609_36760_amd import synthetic as syn
     w = syn.WORKLOADS[MAIN]
     fmt = pc.CacheFormat(c_bits=w.layers[0][0], r_bits=w.layers[0][1])
     lens = syn.seq_lens(w)
-    done, spent, first = 0, 0.0, None
+    done, spent = 0, 0.0
     while done < w.B and spent < budget_s:
         b = done
         c, k = syn.sequence_tokens(w, 0, b, int(lens[b]))
@@ -203,42 +338,47 @@ def cpu_baseline(budget_s: float = 12.0):
         ts = time.perf_counter()
         c_hat, kr_hat = pc.encode_sequence_dense(fmt, c, k)
         at.decode_sequence(ql[0], qr[0], c_hat, kr_hat, w.tau)
-        dt = time.perf_counter() - ts
-        first = dt if first is None else first
-        spent += dt
+        spent += time.perf_counter() - ts
         done += 1
-    el = spent
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
-        cores = 1
-    return {"value": done * w.s_q / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{done} of {w.B} sequences of {MAIN} (4096 tokens, 128 heads each): fp32 quantize + "
-                      f"dequant of every cached token and fp64 attention of all heads; oracle time {el:.1f}s "
-                      f"(input generation excluded)"}
+        blas = 1
+    return {"value": done * w.s_q / spent, "unit": "tokens/s", "cores": blas, "host_cpus": os.cpu_count(),
+            "kind": "oracle",
+            "sample": f"{done} of {w.B} sequences of {MAIN} (32768 tokens, 128 heads each): fp32 quantize and "
+                      f"pack of every cached token and fp64 attention of all heads; oracle time {spent:.1f}s on "
+                      f"{blas} BLAS threads of {os.cpu_count()} host CPUs (input generation excluded)"}
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per launch of the low-bit decode kernel from the recorded
-    FETCH_SIZE / WRITE_SIZE counter runs, each scaled by what the same counter
-    read for a plain 256 MiB copy; None when the kernel sources changed since
-    (or the record is for another workload)."""
+    """HBM bytes per launch of the low-bit decode kernel on ``workload`` from
+    the recorded FETCH_SIZE / WRITE_SIZE counter runs, each scaled by what the
+    same counter read for a plain 256 MiB copy; None when there is no record
+    for the workload or the kernel sources changed since it was taken."""
     import hashlib
     pkg = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2609_36760_amd")
     try:
-        rec = json.load(open(os.path.join(pkg, "measured_traffic.json")))
-        h = hashlib.sha256()
-        for f in rec["kernel_sources"]:
-            h.update(open(os.path.join(pkg, f), "rb").read())
+        recs = json.load(open(os.path.join(pkg, "measured_traffic.json")))["records"]
     except (OSError, KeyError, ValueError):
         return None
-    if h.hexdigest() != rec["kernel_sources_sha256"] or rec["workload"] != workload:
-        return None
-    kib = rec["copy_bytes"] / 1024.0
-    fetch = rec["fetch_kib_per_dispatch"] * kib / rec["copy_fetch_kib"] * 1024.0
-    write = rec["write_kib_per_dispatch"] * kib / rec["copy_write_kib"] * 1024.0
-    return fetch + write
+    for rec in recs:
+        if rec.get("workload") != workload:
+            continue
+        try:
+            h = hashlib.sha256()
+            for f in rec["kernel_sources"]:
+                h.update(open(os.path.join(pkg, f), "rb").read())
+        except (OSError, KeyError):
+            return None
+        if h.hexdigest() != rec["kernel_sources_sha256"]:
+            return None
+        kib = rec["copy_bytes"] / 1024.0
+        fetch = rec["fetch_kib_per_dispatch"] * kib / rec["copy_fetch_kib"] * 1024.0
+        write = rec["write_kib_per_dispatch"] * kib / rec["copy_write_kib"] * 1024.0
+        return fetch + write
+    return None
 
 
 # The paper's attention latency table (Appendix F.1): 16 heads, one query token,
@@ -353,14 +493,15 @@ def paper_grid(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--no-target", action="store_true", help="skip the batch-64 x 32K target shape")
+    ap.add_argument("--steps", type=int, default=30, help="timed steps of the headline workload")
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--small-steps", type=int, default=50, help="timed steps of the 32 x 4096 workload")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--kinds", default="lowbit,bf16,protected,paper",
-                    help="steps to time on the main workload: lowbit, bf16, protected (the low-bit cache with "
-                         "the 4 sink / 128 recent bf16 protection), paper (the paper's metadata storage: bf16 "
-                         "content scales, fp32 RoPE scales, 320 B/token)")
+    ap.add_argument("--no-protocol", action="store_true", help="skip the paper's sampling protocol")
+    ap.add_argument("--kinds", default="lowbit,bf16,small,protected,paper",
+                    help="what to time besides the headline: bf16 (the BF16 cache at both shapes), small (the 32 x "
+                         "4096 workload), protected (4 sink / 128 recent bf16 protection at 32 x 4096), paper (the "
+                         "paper's metadata storage at 32 x 4096); 'lowbit' alone times only the headline")
     ap.add_argument("--protect-split", type=int, default=0,
                     help="key split of the protected step (0: as many splits per sequence as the unprotected plan)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -398,47 +539,52 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     kinds = args.kinds.split(",")
-    main_lb = time_workload(MAIN, "lowbit", args.steps, args.warmup, LAYERS)
-    if "bf16" not in kinds:
-        print(json.dumps({"metric": METRIC, "value": main_lb["decode_tokens_per_s"], "unit": "tokens/s",
-                          "partial_run": True, "lowbit": main_lb}), flush=True)
-        return
-    main_bf = time_workload(MAIN, "bf16", args.steps, args.warmup, LAYERS)
+    env = environment()
+    tc = {}
+    run_lb = make_run(MAIN, "lowbit", token_cache=tc)
+    main_lb = time_workload(MAIN, "lowbit", args.steps, args.warmup, LAYERS[MAIN], run=run_lb, clock=True)
     extra = {}
+    main_bf = None
+    run_bf = None
+    if "bf16" in kinds:
+        run_bf = make_run(MAIN, "bf16", token_cache=tc)
+        main_bf = time_workload(MAIN, "bf16", args.steps, args.warmup, LAYERS[MAIN], run=run_bf, clock=True)
+    del tc
+    if not args.no_protocol:
+        runs = {"c4r4": run_lb} if run_bf is None else {"c4r4": run_lb, "bf16": run_bf}
+        extra["latency_protocol"] = latency_protocol(runs)
+        if "bf16" in runs:
+            extra["latency_protocol"]["speedup_vs_bf16_median"] = (extra["latency_protocol"]["bf16"]["median"] /
+                                                                  extra["latency_protocol"]["c4r4"]["median"])
+    del run_lb, run_bf
+    torch.cuda.empty_cache()
+
+    if "small" in kinds:
+        sm = time_workload(SMALL, "lowbit", args.small_steps, 10, LAYERS[SMALL])
+        entry = {"c4r4": sm}
+        if "bf16" in kinds:
+            sb = time_workload(SMALL, "bf16", args.small_steps, 10, LAYERS[SMALL])
+            entry["bf16"] = sb
+            entry["speedup_vs_bf16"] = sb["ms_per_step"] / sm["ms_per_step"]
+        entry["traffic"] = measured_traffic(SMALL)
+        extra[SMALL] = entry
     if "protected" in kinds:
         from paper_2609_36760_amd import _binding as mb
         from paper_2609_36760_amd import synthetic as syn
         # as many key splits per sequence as the unprotected plan: the tile list
         # (packed tiles + protected rows) is one tile longer than the sequence
-        w = syn.WORKLOADS[MAIN]
+        w = syn.WORKLOADS[SMALL]
         L, pol = w.context, mb.protect_policy(4, 128)
         n_list = -(-(L - pol.recent) // 32) - pol.sink // 32 + -(-(pol.sink + pol.recent) // 32)
         split = args.protect_split or 32 * -(-n_list // -(-L // w.split_tokens))
-        pr = time_workload(MAIN, "lowbit", args.steps, args.warmup, LAYERS, protect=pol, split_tokens=split)
-        extra["protected_sink4_recent128"] = {
-            "value": pr["decode_tokens_per_s"], "ms_per_step": pr["ms_per_step"],
-            "decode_kernel_ms": pr["decode_kernel_ms"], "decode_kernel_tflops": pr["decode_kernel_tflops"],
-            "mfma_frac": pr["mfma_frac"], "hbm_gbs": pr["decode_kernel_gbs"], "splits": pr["splits"],
-            "split_tokens": split,
-            "bytes_per_launch": pr["bytes_per_launch"],
-            "step_vs_unprotected": main_lb["ms_per_step"] / pr["ms_per_step"],
-            "speedup_vs_bf16": main_bf["ms_per_step"] / pr["ms_per_step"]}
-    if not args.no_target:
-        tc = {}
-        t_lb = time_workload(TARGET, "lowbit", max(args.steps // 5, 5), 3, 1, token_cache=tc)
-        t_bf = time_workload(TARGET, "bf16", max(args.steps // 5, 5), 3, 1, token_cache=tc)
-        del tc
-        extra[TARGET] = {"c4r4": t_lb, "bf16": t_bf,
-                         "speedup_vs_bf16": t_bf["ms_per_step"] / t_lb["ms_per_step"]}
+        pr = time_workload(SMALL, "lowbit", args.small_steps, 10, LAYERS[SMALL], protect=pol, split_tokens=split)
+        pr["step_vs_unprotected"] = (extra[SMALL]["c4r4"]["ms_per_step"] / pr["ms_per_step"]
+                                     if SMALL in extra else None)
+        extra["protected_sink4_recent128_" + SMALL] = pr
     if "paper" in kinds:
-        pp = time_workload(MAIN, "lowbit", args.steps, args.warmup, LAYERS, meta="paper")
-        extra["paper_storage_c4r4"] = {
-            "value": pp["decode_tokens_per_s"], "ms_per_step": pp["ms_per_step"],
-            "decode_kernel_ms": pp["decode_kernel_ms"], "decode_kernel_tflops": pp["decode_kernel_tflops"],
-            "mfma_frac": pp["mfma_frac"], "hbm_gbs": pp["decode_kernel_gbs"],
-            "bytes_per_launch": pp["bytes_per_launch"], "cache_bytes_per_token": 320,
-            "step_vs_fp16_metadata": main_lb["ms_per_step"] / pp["ms_per_step"],
-            "speedup_vs_bf16": main_bf["ms_per_step"] / pp["ms_per_step"]}
+        pp = time_workload(SMALL, "lowbit", args.small_steps, 10, LAYERS[SMALL], meta="paper")
+        pp["cache_bytes_per_token"] = 320
+        extra["paper_storage_c4r4_" + SMALL] = pp
     cpu = None if args.no_cpu else cpu_baseline()
 
     line = {
@@ -448,19 +594,27 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": main_lb["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": MAIN, "batch": 32, "heads": 128, "context": 4096, "s_q": 1,
+        "dtype": "fp16",
+        "dtype_detail": "INT4 codes dequantized to fp16 MFMA operands, fp32 accumulation; bf16 queries and outputs",
+        "data": "synthetic",
+        "config": {"workload": MAIN, "batch": 64, "heads": 128, "context": 32768, "s_q": 1,
                    "cache": "INT4 content + INT4 RoPE key, group 64, fp16 scale/zero",
-                   "split_tokens": 512, "layers_cycled": LAYERS},
+                   "split_tokens": main_lb["split_tokens"], "layers_cycled": LAYERS[MAIN]},
         "roofline": {"bound": "mfma", "achieved": main_lb["decode_kernel_tflops"], "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": main_lb["mfma_frac"], "traffic": measured_traffic(MAIN),
-                     "algorithmic_bytes": main_lb["bytes_per_launch"]},
+                     "algorithmic_bytes": main_lb["bytes_per_launch"],
+                     "algorithmic_flops": main_lb["flops_per_launch"],
+                     "kernel_ms": main_lb["decode_kernel_ms_stats"]},
+        "gpu_clock": main_lb.get("gpu_clock"),
         "hbm_gbs": main_lb["decode_kernel_gbs"], "hbm_frac": main_lb["hbm_frac"],
-        "bf16_cache": {"value": main_bf["decode_tokens_per_s"], "ms_per_step": main_bf["ms_per_step"],
-                       "decode_kernel_ms": main_bf["decode_kernel_ms"], "hbm_gbs": main_bf["decode_kernel_gbs"],
-                       "hbm_frac": main_bf["hbm_frac"], "mfma_frac": main_bf["mfma_frac"]},
-        "speedup_vs_bf16": main_bf["ms_per_step"] / main_lb["ms_per_step"],
+        "bf16_cache": None if main_bf is None else {
+            "value": main_bf["decode_tokens_per_s"], "ms_per_step": main_bf["ms_per_step"],
+            "decode_kernel_ms": main_bf["decode_kernel_ms"], "kernel_ms": main_bf["decode_kernel_ms_stats"],
+            "hbm_gbs": main_bf["decode_kernel_gbs"], "hbm_frac": main_bf["hbm_frac"],
+            "mfma_frac": main_bf["mfma_frac"], "bound": "hbm", "gpu_clock": main_bf.get("gpu_clock")},
+        "speedup_vs_bf16": None if main_bf is None else main_bf["ms_per_step"] / main_lb["ms_per_step"],
         "cpu_baseline": cpu,
+        "environment": env,
         "context": {"paper_kv_compression_128k": 3.59, "paper_serving_speedup_vs_bf16": 5.168,
                     "paper_hardware": "unnamed NVIDIA GPUs (one for kernels, eight for serving)"},
     }

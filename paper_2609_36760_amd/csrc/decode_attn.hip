@@ -801,10 +801,12 @@ void decode_kernel(DecodeArgs a) {
         const int tr_col = 16 * (tr_g & 1) + 4 * (tr_i & 3);  // + 32 * m
 
         OpT pb_prev[2] = {OpT{}, OpT{}};   // weights of the previous tile (P^T operands)
-        // BF16 pipeline: the weights' residuals w - bf16(w), rounded to bf16, as
-        // a second P^T operand, so that the aggregation sees each weight to 16
-        // significant bits (bf16 alone keeps 8)
-        OpT pl_prev[C::lowbit ? 1 : 2] = {};
+        // BF16 pipeline over protected rows: the weights' residuals w - bf16(w),
+        // rounded to bf16, as a second P^T operand, so that the aggregation sees
+        // each weight to 16 significant bits (bf16 alone keeps 8).  Over the BF16
+        // cache one bf16 operand, the normalizer summing the rounded weights.
+        constexpr bool kPairW = !C::lowbit && kRing;
+        OpT pl_prev[kPairW ? 2 : 1] = {};
         bool move_pending = false;         // the previous tile moved the reference:
         float alpha_pending = 1.0f;        // accumulators *= alpha before its aggregation
 
@@ -908,7 +910,7 @@ void decode_kernel(DecodeArgs a) {
             bool move = false;
             float alpha = 1.0f;
             uint32_t pw[8];
-            uint32_t pwl[C::lowbit ? 1 : 8];
+            uint32_t pwl[kPairW ? 8 : 1];
             // (The empty statements pin each piece's results where it is computed:
             // the compiler would otherwise sink the work next to its first use,
             // after the aggregation.)
@@ -943,14 +945,21 @@ void decode_kernel(DecodeArgs a) {
                         pw[v2] = pack_f16x2(p0, p1);
                         l_run = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, pw[v2]), f16x2{1.0f16, 1.0f16}, l_run,
                                                        false);
-                    } else {
+                    } else if constexpr (kPairW) {
                         l_run += p0 + p1;
                         pw[v2] = pack_bf16x2(p0, p1);
                         // w - bf16(w) is exact in fp32 (|r| <= 2^-9 |w|); its bf16 rounding
                         // leaves each weight to a relative 2^-17
                         const float h0 = __uint_as_float(pw[v2] << 16), h1 = __uint_as_float(pw[v2] & 0xFFFF0000u);
-                        pwl[v2 % (C::lowbit ? 1 : 8)] = pack_bf16x2(p0 - h0, p1 - h1);
-                        asm volatile("" : "+v"(pwl[v2 % (C::lowbit ? 1 : 8)]));
+                        pwl[v2 % (kPairW ? 8 : 1)] = pack_bf16x2(p0 - h0, p1 - h1);
+                        asm volatile("" : "+v"(pwl[v2 % (kPairW ? 8 : 1)]));
+                    } else {
+                        // the sum of the bf16 weights the aggregation uses, one dot2 per pair
+                        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+                        pw[v2] = pack_bf16x2(p0, p1);
+                        l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw[v2]),
+                                                                bf16x2{static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)},
+                                                                l_run, false);
                     }
                     asm volatile("" : "+v"(pw[v2]), "+v"(l_run));
                 }
@@ -985,7 +994,7 @@ void decode_kernel(DecodeArgs a) {
                     const int so = stp ^ 1;
                     const int m = so & 15;
                     acc[m] = mfma(vb[so % kVAhead], pb_prev[so >> 4], acc[m]);
-                    if constexpr (!C::lowbit) acc[m] = mfma(vb[so % kVAhead], pl_prev[(so >> 4) % 2], acc[m]);
+                    if constexpr (kPairW) acc[m] = mfma(vb[so % kVAhead], pl_prev[(so >> 4) % 2], acc[m]);
                     if (stp & 1) {
 #pragma unroll
                         for (int j = stp - 1; j <= stp; ++j)
@@ -1009,10 +1018,10 @@ void decode_kernel(DecodeArgs a) {
             if constexpr (kQK) {
                 pb_prev[0] = __builtin_bit_cast(OpT, make_uint4(pw[0], pw[1], pw[2], pw[3]));
                 pb_prev[1] = __builtin_bit_cast(OpT, make_uint4(pw[4], pw[5], pw[6], pw[7]));
-                if constexpr (!C::lowbit) {
-                    constexpr int n = C::lowbit ? 1 : 8;
+                if constexpr (kPairW) {
+                    constexpr int n = kPairW ? 8 : 1;
                     pl_prev[0] = __builtin_bit_cast(OpT, make_uint4(pwl[0 % n], pwl[1 % n], pwl[2 % n], pwl[3 % n]));
-                    pl_prev[1 % (C::lowbit ? 1 : 2)] =
+                    pl_prev[1 % (kPairW ? 2 : 1)] =
                         __builtin_bit_cast(OpT, make_uint4(pwl[4 % n], pwl[5 % n], pwl[6 % n], pwl[7 % n]));
                 }
                 move_pending = move;

@@ -315,8 +315,10 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
             for (int v = 0; v < 4; ++v) {
                 p[v] = __builtin_amdgcn_exp2f(fmaf(s[v], a.scale_log2, nref));
                 // the normalizer sums the weights the aggregation uses: fp16-rounded
-                // (low-bit), or to 16 significant bits (BF16 rows, a bf16 pair)
+                // (low-bit), bf16-rounded (the BF16 cache), or to 16 significant bits
+                // (protected rows, a bf16 pair)
                 if constexpr (C::lowbit) p[v] = static_cast<float>(static_cast<_Float16>(p[v]));
+                else if constexpr (!kRing) p[v] = static_cast<float>(static_cast<__bf16>(p[v]));
                 l_run += p[v];
             }
         };
@@ -445,8 +447,9 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
                 s16x4 vb[kVAhead];
 #pragma unroll
                 for (int m = 0; m < kVAhead; ++m) vb[m] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + 32 * m));
-                // the weights to 16 significant bits: bf16(w) and the bf16 rounding of
-                // the exact residual w - bf16(w), two products per block
+                // protected rows: the weights to 16 significant bits, bf16(w) and the
+                // bf16 rounding of the exact residual w - bf16(w), two products per
+                // block; the BF16 cache: the bf16 weights alone (already rounded)
                 const uint32_t h01 = pack_bf16x2(p[0], p[1]), h23 = pack_bf16x2(p[2], p[3]);
                 const s16x4 pbb = __builtin_bit_cast(s16x4, make_uint2(h01, h23));
                 const s16x4 pbl = __builtin_bit_cast(
@@ -455,7 +458,8 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
 #pragma unroll
                 for (int m = 0; m < 32; ++m) {
                     acc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vb[m % kVAhead], pbb, acc[m], 0, 0, 0);
-                    acc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vb[m % kVAhead], pbl, acc[m], 0, 0, 0);
+                    if constexpr (kRing)
+                        acc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vb[m % kVAhead], pbl, acc[m], 0, 0, 0);
                     if (m + kVAhead < 32)
                         vb[m % kVAhead] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + 32 * (m + kVAhead)));
                 }

@@ -11,9 +11,10 @@ It records:
   * why the low-bit kernels use fp16 rather than bf16 matrix products: with
     bf16 tiles and weights the rule fails on the 32 x 4K workload, with fp16
     it holds;
-  * why the BF16-cache pipeline carries each weight as a bf16 pair (the weight
-    and its rounded residual, 16 significant bits): with the weight rounded
-    once to bf16 the rule fails, with the pair it holds;
+  * why the BF16-cache kernel normalizes by the sum of its bf16-rounded
+    weights (with the exact sum the rule fails, with the rounded one it holds)
+    and why protected rows carry each weight as a bf16 pair (the weight and its
+    rounded residual, 16 significant bits);
   * that rounding the exact result to bf16 already costs more than 2e-2 of the
     global RMS, so the rule is read beyond the output's own rounding;
   * the two small batches of the GPU tests where the fp16 datapath itself
@@ -162,11 +163,18 @@ def bf16_sample():
     return w, _rows(w, [(3, None), (30, None)], np.arange(128), exact_bf16=True)
 
 
-def test_bf16_cache_weights_need_sixteen_bits(bf16_sample):
+def test_bf16_weights_need_a_normalizer_of_the_rounded_weights(bf16_sample):
+    """bf16 weights normalized by the sum of the unrounded weights fail the
+    rule (the lazy reference puts the dominant weight anywhere in [1, 2^10],
+    where its rounding moves the whole row); normalized by the sum of the
+    rounded weights they hold it (the BF16-cache kernel), and so does the bf16
+    pair (protected rows)."""
     w, rows = bf16_sample
     _, _, once = _ratio(w, rows, _ident, _rnd_bf16, split=512, part_round=_rnd_f16, sum_rounded=False)
+    _, _, rounded = _ratio(w, rows, _ident, _rnd_bf16, split=512, part_round=_rnd_f16, sum_rounded=True)
     _, _, pair = _ratio(w, rows, _ident, _bf16_pair, split=512, part_round=_rnd_f16, sum_rounded=False)
     assert once > 0.02, once
+    assert rounded <= 0.02, rounded
     assert pair <= 0.02, pair
 
 
