@@ -130,13 +130,13 @@ __device__ __forceinline__ void stage_narrow_lowbit(int k, const uint8_t* page, 
     const int last = nvalid - 1;
     if (k < C::u_rc / 64) {
         const int u = 64 * k + lane;
-        dma16(page, (po + min(u & 15, last)) * C::cc + 16 * (u >> 4), lds + 64 * 16 * k);
+        dma16_m0(page, (po + min(u & 15, last)) * C::cc + 16 * (u >> 4), lds + 64 * 16 * k);
     } else if (k == C::u_rc / 64) {
         const int v = lane & 31;
         const int base = lane < 32 ? g.off_cr : g.off_mc;
-        dma16(page, base + (po + min(v & 15, last)) * 32 + 16 * (v >> 4), lds + 64 * 16 * k);
+        dma16_m0(page, base + (po + min(v & 15, last)) * 32 + 16 * (v >> 4), lds + 64 * 16 * k);
     } else if (lane < 4) {
-        dma16(page, g.off_mr + po * 4 + 16 * lane, lds + 64 * 16 * k);
+        dma16_m0(page, g.off_mr + po * 4 + 16 * lane, lds + 64 * 16 * k);
     }
 }
 
@@ -150,23 +150,50 @@ __device__ __forceinline__ void stage_narrow_bf16(int k, const uint8_t* src, Row
     int r = min(u / 74, 15);
     if (u < bf_row(r)) --r;
     const int col = min(u - bf_row(r), 71);
-    dma16(src, row_start(min(r, nvalid - 1)) + 16 * col, lds + 64 * 16 * k);
+    dma16_m0(src, row_start(min(r, nvalid - 1)) + 16 * col, lds + 64 * 16 * k);
 }
 
 // Dequantize 8 channels into fp16 pairs (2p, 2p+1).  In the code layout a
 // channel pair sits at one bit offset of the two 16-bit halves of a word: the
 // 8 channels are the word's pairs at bit offsets sh0 + CBITS p (a 4-bit word
-// holds exactly 8 channels, sh0 = 0; a 2-bit word 16, sh0 = 0 or 8).
+// holds exactly 8 channels, sh0 = 0; a 2-bit word 16, sh0 = 0 or 8).  A pair
+// is extracted in place at its offset o within a byte: masked and or'ed with
+// 0x6400 it is the fp16 value 1024 + 2^o q.  For o = 0, subtracting
+// zz = 1024 + zero leaves q - zero; otherwise one fused multiply-add by 2^-o
+// adds zo = -(1024 / 2^o + zero) (zo[o / 2 - 1]).  Both are exact, so the
+// word is shifted only by whole bytes, and the one rounding is the multiply
+// by the scale.
 template <int CBITS>
-__device__ __forceinline__ f16x8 dequant8(uint32_t w, int sh0, f16x2 zz, f16x2 ss) {
-    constexpr uint32_t kMask = CBITS == 4 ? 0x000F000Fu : 0x00030003u;
+__device__ __forceinline__ f16x8 dequant8(uint32_t w, int sh0, f16x2 zz, const f16x2* zo, f16x2 ss) {
     uint32_t o[4];
+    if constexpr (CBITS == 4) {
+        const uint32_t w8 = w >> 8;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        const uint32_t b = and_or(w >> (sh0 + CBITS * p), kMask, 0x64006400u);   // 1024 + q
-        o[p] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, b) - zz) * ss);
+        for (int p = 0; p < 4; ++p) {
+            const uint32_t src = p < 2 ? w : w8;
+            const f16x2 x = __builtin_bit_cast(f16x2, and_or(src, (p & 1) ? 0x00F000F0u : 0x000F000Fu, 0x64006400u));
+            const f16x2 d = (p & 1) ? __builtin_elementwise_fma(x, f16x2{0.0625f16, 0.0625f16}, zo[1]) : x - zz;
+            o[p] = __builtin_bit_cast(uint32_t, d * ss);
+        }
+    } else {
+        const uint32_t ws = w >> sh0;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            const f16x2 x = __builtin_bit_cast(f16x2, and_or(ws, 0x00030003u << (2 * p), 0x64006400u));
+            constexpr _Float16 kInv[4] = {1.0f16, 0.25f16, 0.0625f16, 0.015625f16};
+            const f16x2 d = p == 0 ? x - zz : __builtin_elementwise_fma(x, f16x2{kInv[p], kInv[p]}, zo[p - 1]);
+            o[p] = __builtin_bit_cast(uint32_t, d * ss);
+        }
     }
     return __builtin_bit_cast(f16x8, make_uint4(o[0], o[1], o[2], o[3]));
+}
+
+// zo[k] = -(1024 / 2^o + zero) for o = 2 (k + 1), from zz = 1024 + zero
+// (exact: integers and quarters below 1024).
+__device__ __forceinline__ void zero_offsets(f16x2 zz, f16x2* zo) {
+    zo[0] = f16x2{768.0f16, 768.0f16} - zz;
+    zo[1] = f16x2{960.0f16, 960.0f16} - zz;
+    zo[2] = f16x2{1008.0f16, 1008.0f16} - zz;
 }
 
 // ---------------------------------------------------------------------------
@@ -245,6 +272,9 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
                                                                   bf16x2_to_f16x2(v.z), bf16x2_to_f16x2(v.w)));
                 else
                     qf[kk] = __builtin_bit_cast(bf16x8, v);
+                // kept in accumulation registers, which the score products read
+                // directly as their B operand
+                asm volatile("" : "+a"(qf[kk]));
             }
         }
 
@@ -252,6 +282,7 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
             if constexpr (C::lowbit) return smem + slot_offset(j, C::NS, C::stage_bytes);
             else return smem + slot_offset(j, C::NS, kBfTileBytes);
         };
+        int st_pg = t_begin / P, st_po = t_begin % P, pid_pg = -1, pid = 0;   // next tile to stage
         auto issue_tile = [&](int j) __attribute__((always_inline)) {
             const int t0 = t_begin + min(j, n_tiles - 1) * kTok;   // past the end: the last tile again
             const int nvalid = min(t_end - t0, kTok);
@@ -266,10 +297,23 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
 #pragma unroll
                 for (int k = 0; k < C::loads; ++k) stage_narrow_bf16(k, ring_base, row_start, nvalid, lds, lane);
             } else {
-                int pid = load_page_id(bt, t0 / P);
-                pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
+                // tiles are issued in order; a 16-token tile never crosses a page
+                // (t_begin and the page size are multiples of 32), and the page
+                // id is fetched once per page
+                if (st_pg != pid_pg) {
+                    pid = load_page_id(bt, st_pg);
+                    pid = min(max(pid, 0), static_cast<int>(a.num_pages - 1));
+                    pid_pg = st_pg;
+                }
                 const uint8_t* page = a.cache + static_cast<int64_t>(pid) * a.g.page_bytes;
-                const int po = t0 % P;
+                const int po = st_po;
+                if (j < n_tiles - 1) {
+                    st_po += kTok;
+                    if (st_po == P) {
+                        st_po = 0;
+                        ++st_pg;
+                    }
+                }
                 if constexpr (C::lowbit) {
 #pragma unroll
                     for (int k = 0; k < C::loads; ++k) stage_narrow_lowbit<PK>(k, page, po, nvalid, a.g, lds, lane);
@@ -349,27 +393,34 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
                 mc1 = *reinterpret_cast<const uint4*>(st + 16 * (C::u_mc + 16 + li));
                 if constexpr (!C::pmeta) rmw = *reinterpret_cast<const uint32_t*>(st + 16 * C::u_mr + 4 * li);
             };
-            auto dq = [&](int kk) __attribute__((always_inline)) {
-                f16x2 zz, ss;
+            // dequantization constants of the group holding k-step kk (its
+            // scale, 1024 + zero, and the zero offsets of the in-place extraction)
+            struct Gm { f16x2 zz, ss, zo[3]; };
+            auto group_meta = [&](int kk) __attribute__((always_inline)) {
+                Gm m;
                 if (kk >= 16) {
-                    if constexpr (C::pmeta) pmeta_to_f16(__uint_as_float(mc1.z), mc1.w & 0xFFu, zz, ss);
-                    else meta_to_f16(rmw, zz, ss);
-                    return dequant8<4>(words[kk], 0, zz, ss);
-                }
-                const int grp = kk >> 1;
-                if constexpr (C::pmeta) {
-                    const uint32_t sw = grp < 4 ? (grp < 2 ? mc0.x : mc0.y) : (grp < 6 ? mc0.z : mc0.w);
-                    const uint32_t sbits = (sw >> (16 * (grp & 1))) & 0xFFFFu;
-                    const uint32_t zw = grp < 4 ? mc1.x : mc1.y;
-                    pmeta_to_f16(__uint_as_float(sbits << 16), (zw >> (8 * (grp & 3))) & 0xFFu, zz, ss);
+                    if constexpr (C::pmeta) pmeta_to_f16(__uint_as_float(mc1.z), mc1.w & 0xFFu, m.zz, m.ss);
+                    else meta_to_f16(rmw, m.zz, m.ss);
                 } else {
-                    const uint32_t mw = grp < 4 ? (grp < 2 ? (grp == 0 ? mc0.x : mc0.y) : (grp == 2 ? mc0.z : mc0.w))
-                                                : (grp < 6 ? (grp == 4 ? mc1.x : mc1.y) : (grp == 6 ? mc1.z : mc1.w));
-                    meta_to_f16(mw, zz, ss);
+                    const int grp = kk >> 1;
+                    if constexpr (C::pmeta) {
+                        const uint32_t sw = grp < 4 ? (grp < 2 ? mc0.x : mc0.y) : (grp < 6 ? mc0.z : mc0.w);
+                        const uint32_t sbits = (sw >> (16 * (grp & 1))) & 0xFFFFu;
+                        const uint32_t zw = grp < 4 ? mc1.x : mc1.y;
+                        pmeta_to_f16(__uint_as_float(sbits << 16), (zw >> (8 * (grp & 3))) & 0xFFu, m.zz, m.ss);
+                    } else {
+                        const uint32_t mw = grp < 4 ? (grp < 2 ? (grp == 0 ? mc0.x : mc0.y) : (grp == 2 ? mc0.z : mc0.w))
+                                                    : (grp < 6 ? (grp == 4 ? mc1.x : mc1.y) : (grp == 6 ? mc1.z : mc1.w));
+                        meta_to_f16(mw, m.zz, m.ss);
+                    }
                 }
-                return dequant8<C::cbits>(words[kk], C::cbits == 4 ? 0 : 8 * (g & 1), zz, ss);
+                zero_offsets(m.zz, m.zo);
+                return m;
             };
-            f16x8 kv[kQSteps];
+            auto dq = [&](int kk, const Gm& m) __attribute__((always_inline)) {
+                if (kk >= 16) return dequant8<4>(words[kk], 0, m.zz, m.zo, m.ss);
+                return dequant8<C::cbits>(words[kk], C::cbits == 4 ? 0 : 8 * (g & 1), m.zz, m.zo, m.ss);
+            };
             float p[4] = {0.0f, 0.0f, 0.0f, 0.0f};
             constexpr int kVAhead = 8;
             s16x4 vb[kVAhead];
@@ -381,45 +432,80 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
                                                                0, 0, 0);
                 if (m + kVAhead < 32) vb[m % kVAhead] = vread(m + kVAhead);
             };
-            // one step: scores of tile it (QK) and aggregation of tile it-1 (PV)
+            // one step: scores of tile it (QK) and aggregation of tile it-1 (PV).
+            // Tile it's content channels 32 kk + 8 g .. +8 (channel blocks 2 kk and
+            // 2 kk + 1) replace tile it-1's as soon as they are dequantized: the
+            // transposing reads of those blocks were issued before (in the previous
+            // k-steps, or before the loop), and LDS serves one wave's accesses in
+            // the order they are issued.
             auto step = [&](int it, auto QK, auto PV) __attribute__((always_inline)) {
                 constexpr bool kQK = decltype(QK)::value, kPV = decltype(PV)::value;
                 const f16x4 pbh = {static_cast<_Float16>(p[0]), static_cast<_Float16>(p[1]),
                                    static_cast<_Float16>(p[2]), static_cast<_Float16>(p[3])};
                 f32x4 s = f32x4{};
-                if constexpr (kQK) {
-                    // tile it has landed; every LDS access before this point is done
-                    wait_loads<(C::D - 1) * C::loads>();
-                    read_stage(slot_base(it));
-                    issue_tile(it + C::D);
-                }
+                // tile it's code words were read at the end of the previous step;
+                // its staging slot is free (the slot of tile it + D held tile it - 1)
+                if constexpr (kQK) issue_tile(it + C::D);
                 if constexpr (kPV) {
 #pragma unroll
                     for (int m = 0; m < kVAhead; ++m) vb[m] = vread(m);
                 }
                 __builtin_amdgcn_sched_barrier(0);
+                // the dequantization runs one k-step ahead of the score product,
+                // so that vector work separates the products (each 16 cycles on the
+                // matrix unit) instead of issuing them back to back
+                Gm gm;
+                f16x8 kv_next;
+                if constexpr (kQK) {
+                    gm = group_meta(0);
+                    kv_next = dq(0, gm);
+                }
 #pragma unroll
                 for (int kk = 0; kk < kQSteps; ++kk) {
+                    f16x8 kv;
                     if constexpr (kQK) {
-                        kv[kk] = dq(kk);
-                        s = __builtin_amdgcn_mfma_f32_16x16x32_f16(kv[kk], qf[kk], s, 0, 0, 0);
+                        kv = kv_next;
+                        s = __builtin_amdgcn_mfma_f32_16x16x32_f16(kv, qf[kk], s, 0, 0, 0);
                     }
                     if constexpr (kPV) {
+                        if (kk < 16) pv(2 * kk, pbh);
+                    }
+                    if constexpr (kQK) {
+                        if (kk + 1 < kQSteps) {
+                            if (((kk + 1) & 1) == 0) gm = group_meta(kk + 1);
+                            kv_next = dq(kk + 1, gm);
+                        }
+                    }
+                    if constexpr (kPV) {
+                        if (kk < 16) pv(2 * kk + 1, pbh);
+                    }
+                    if constexpr (kQK) {
+                        if (kk < 16) *reinterpret_cast<f16x8*>(tile + 16 * (f16_row(li) + 4 * kk + g)) = kv;
+                    }
+                    if constexpr (kQK && kPV) {
                         if (kk < 16) {
-                            pv(2 * kk, pbh);
-                            pv(2 * kk + 1, pbh);
+                            // product, 5 vector, product, 5 vector, product, the rest
+                            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+                            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+                            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                         }
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }
                 if constexpr (kQK) {
-                    // tile it-1's transposing reads are all consumed: overwrite it
-#pragma unroll
-                    for (int kk = 0; kk < 16; ++kk)
-                        *reinterpret_cast<f16x8*>(tile + 16 * (f16_row(li) + 4 * kk + g)) = kv[kk];
+                    if (it + 1 < n_tiles) {
+                        // tile it+1 has landed: its code words are read while the
+                        // softmax runs
+                        wait_loads<(C::D - 1) * C::loads>();
+                        read_stage(slot_base(it + 1));
+                    }
                     softmax(it, s, p);
                 }
             };
+            wait_loads<(C::D - 1) * C::loads>();
+            read_stage(slot_base(0));
             step(0, std::true_type{}, std::false_type{});
             for (int it = 1; it < n_tiles; ++it) step(it, std::true_type{}, std::true_type{});
             step(n_tiles, std::false_type{}, std::true_type{});
