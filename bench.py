@@ -109,13 +109,16 @@ def algorithmic_bytes(run) -> int:
 
 
 class ClockSampler:
-    """Samples the GPU's graphics clock (torch.cuda.clock_rate, MHz) from a
-    host thread while the timed steps run; None when the platform does not
-    report it."""
+    """Samples the GPU's graphics clock (torch.cuda.clock_rate, MHz) and its
+    average socket power (torch.cuda.power_draw, amdsmi's
+    average_socket_power, W) from a host thread.  amdsmi refreshes these
+    about once a second, so the figures mean something only over a run of
+    seconds: ``sustained`` runs the step back to back for that long and keeps
+    the samples after the first third (the clock's ramp from idle)."""
 
-    def __init__(self, period_s: float = 0.002):
+    def __init__(self, period_s: float = 0.02):
         import threading
-        self.samples, self._stop, self.period = [], threading.Event(), period_s
+        self.samples, self.power, self._stop, self.period = [], [], threading.Event(), period_s
         self._t = threading.Thread(target=self._run, daemon=True)
 
     def _run(self):
@@ -125,6 +128,10 @@ class ClockSampler:
                 self.samples.append(float(torch.cuda.clock_rate()))
             except Exception:
                 return
+            try:
+                self.power.append(float(torch.cuda.power_draw()))
+            except Exception:
+                pass
             time.sleep(self.period)
 
     def __enter__(self):
@@ -135,12 +142,35 @@ class ClockSampler:
         self._stop.set()
         self._t.join()
 
-    def summary(self):
+    def summary(self, seconds):
         if not self.samples:
             return None
-        a = np.asarray(self.samples)
-        return {"median_mhz": float(np.median(a)), "min_mhz": float(a.min()), "max_mhz": float(a.max()),
-                "samples": int(a.size)}
+        a = np.asarray(self.samples[len(self.samples) // 3:])
+        out = {"median_mhz": float(np.median(a)), "min_mhz": float(a.min()), "max_mhz": float(a.max()),
+               "samples": int(a.size), "seconds": seconds,
+               "source": "amdsmi, sampled every 20 ms while the step runs back to back; first third dropped"}
+        p = np.asarray(self.power[len(self.power) // 3:])
+        if p.size and p.max() > 0:
+            out["socket_power_w"] = {"median": float(np.median(p)), "max": float(p.max())}
+        return out
+
+
+def sustained(one_step, seconds=1.5, burst=50):
+    """Clock and socket power while ``one_step`` runs back to back for
+    ``seconds`` (bursts of ``burst`` steps, synchronized between bursts)."""
+    import torch
+    with ClockSampler() as smp:
+        t0, i = time.perf_counter(), 0
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(burst):
+                one_step(i)
+                i += 1
+            torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    res = smp.summary(round(wall, 2))
+    if res is not None:
+        res["ms_per_step"] = wall * 1e3 / i
+    return res
 
 
 def stats_of(a):
@@ -212,16 +242,11 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
         one_step(i)
     evs = TimingEvents(steps)
     torch.cuda.synchronize()
-    sampler = ClockSampler() if clock else None
-    if sampler is not None:
-        sampler.__enter__()
     t0 = time.perf_counter()
     for i in range(warmup, warmup + steps):
         one_step(i, evs)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    if sampler is not None:
-        sampler.__exit__(None, None, None)
     kern = [evs.elapsed_ms(k) for k in range(steps)]
     kern_ms = float(np.mean(kern))
     ms_step = wall * 1e3 / steps
@@ -240,8 +265,8 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
     }
     res["mfma_frac"] = res["decode_kernel_tflops"] / PEAK_BF16_TFLOPS
     res["hbm_frac"] = res["decode_kernel_gbs"] / PEAK_HBM_GBS
-    if sampler is not None:
-        res["gpu_clock"] = sampler.summary()
+    if clock:
+        res["gpu_clock"] = sustained(lambda i: one_step(warmup + steps + i))
     if protect is not None:
         res["protect"] = {"sink": protect.sink, "recent": protect.recent}
     tag = ("" if protect is None else " protected") + ("" if meta == "fp16" else f" {meta} metadata")
@@ -249,7 +274,7 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
         f"(median {res['decode_kernel_ms_stats']['median'] * 1e3:.1f}) = "
         f"{res['decode_kernel_tflops']:.1f} TFLOP/s ({100 * res['mfma_frac']:.1f}% MFMA), "
         f"{res['decode_kernel_gbs']:.0f} GB/s ({100 * res['hbm_frac']:.1f}% HBM)"
-        + (f", clock {res['gpu_clock']}" if sampler is not None else ""))
+        + (f", sustained clock {res['gpu_clock']}" if clock else ""))
     del caches, prots
     if own:
         del run
@@ -493,9 +518,13 @@ def paper_grid(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30, help="timed steps of the headline workload")
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--small-steps", type=int, default=50, help="timed steps of the 32 x 4096 workload")
+    ap.add_argument("--steps", type=int, default=300, help="timed steps of the headline workload")
+    ap.add_argument("--warmup", type=int, default=300,
+                    help="untimed steps first: the clock ramps up from idle over the first tens of milliseconds")
+    ap.add_argument("--small-steps", type=int, default=300, help="timed steps of the 32 x 4096 workload")
+    ap.add_argument("--small-warmup", type=int, default=300)
+    ap.add_argument("--no-sustain", action="store_true",
+                    help="skip the 1.5 s back-to-back runs that measure the sustained clock and power")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-protocol", action="store_true", help="skip the paper's sampling protocol")
     ap.add_argument("--kinds", default="lowbit,bf16,small,protected,paper",
@@ -542,13 +571,15 @@ def main():
     env = environment()
     tc = {}
     run_lb = make_run(MAIN, "lowbit", token_cache=tc)
-    main_lb = time_workload(MAIN, "lowbit", args.steps, args.warmup, LAYERS[MAIN], run=run_lb, clock=True)
+    main_lb = time_workload(MAIN, "lowbit", args.steps, args.warmup, LAYERS[MAIN], run=run_lb,
+                            clock=not args.no_sustain)
     extra = {}
     main_bf = None
     run_bf = None
     if "bf16" in kinds:
         run_bf = make_run(MAIN, "bf16", token_cache=tc)
-        main_bf = time_workload(MAIN, "bf16", args.steps, args.warmup, LAYERS[MAIN], run=run_bf, clock=True)
+        main_bf = time_workload(MAIN, "bf16", args.steps, args.warmup, LAYERS[MAIN], run=run_bf,
+                                clock=not args.no_sustain)
     del tc
     if not args.no_protocol:
         runs = {"c4r4": run_lb} if run_bf is None else {"c4r4": run_lb, "bf16": run_bf}
@@ -560,10 +591,10 @@ def main():
     torch.cuda.empty_cache()
 
     if "small" in kinds:
-        sm = time_workload(SMALL, "lowbit", args.small_steps, 10, LAYERS[SMALL])
+        sm = time_workload(SMALL, "lowbit", args.small_steps, args.small_warmup, LAYERS[SMALL])
         entry = {"c4r4": sm}
         if "bf16" in kinds:
-            sb = time_workload(SMALL, "bf16", args.small_steps, 10, LAYERS[SMALL])
+            sb = time_workload(SMALL, "bf16", args.small_steps, args.small_warmup, LAYERS[SMALL])
             entry["bf16"] = sb
             entry["speedup_vs_bf16"] = sb["ms_per_step"] / sm["ms_per_step"]
         entry["traffic"] = measured_traffic(SMALL)
@@ -577,12 +608,13 @@ def main():
         L, pol = w.context, mb.protect_policy(4, 128)
         n_list = -(-(L - pol.recent) // 32) - pol.sink // 32 + -(-(pol.sink + pol.recent) // 32)
         split = args.protect_split or 32 * -(-n_list // -(-L // w.split_tokens))
-        pr = time_workload(SMALL, "lowbit", args.small_steps, 10, LAYERS[SMALL], protect=pol, split_tokens=split)
+        pr = time_workload(SMALL, "lowbit", args.small_steps, args.small_warmup, LAYERS[SMALL], protect=pol,
+                           split_tokens=split)
         pr["step_vs_unprotected"] = (extra[SMALL]["c4r4"]["ms_per_step"] / pr["ms_per_step"]
                                      if SMALL in extra else None)
         extra["protected_sink4_recent128_" + SMALL] = pr
     if "paper" in kinds:
-        pp = time_workload(SMALL, "lowbit", args.small_steps, 10, LAYERS[SMALL], meta="paper")
+        pp = time_workload(SMALL, "lowbit", args.small_steps, args.small_warmup, LAYERS[SMALL], meta="paper")
         pp["cache_bytes_per_token"] = 320
         extra["paper_storage_c4r4_" + SMALL] = pp
     cpu = None if args.no_cpu else cpu_baseline()

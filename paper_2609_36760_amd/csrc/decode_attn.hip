@@ -167,7 +167,8 @@ static_assert(lds_bytes<KIND_BF16>() <= 160 * 1024, "LDS budget of a gfx950 CU")
 // chain's first product writes the tile without reading it, the following
 // ones accumulate back to back (no wait needed between products of one shape),
 // and score_ready() supplies the wait before vector instructions read the
-// result.
+// result (12 wait states, what the compiler's hazard model places after a
+// 32 x 32 x 16 product whose result a vector instruction reads).
 __device__ __forceinline__ void mfma_v(f32x16& c, f16x8 a, f16x8 b, bool first) {
     if (first)
         asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, %2, 0" : "=&v"(c) : "v"(a), "v"(b));
@@ -181,7 +182,7 @@ __device__ __forceinline__ void mfma_v(f32x16& c, bf16x8 a, bf16x8 b, bool first
         asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
 }
 __device__ __forceinline__ void score_ready(f32x16& c) {
-    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" : "+v"(c));
+    asm volatile("s_nop 7\n\ts_nop 3" : "+v"(c));
 }
 __device__ __forceinline__ float max_halves(float v) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
@@ -228,6 +229,19 @@ __device__ __forceinline__ int step_barrier(const int32_t* table, int index) {
                  : "=&s"(v)
                  : "s"(table), "s"(__builtin_amdgcn_readfirstlane(index * 4)), "n"(N)
                  : "memory");
+    return v;
+}
+
+// A page-table entry fetched through the scalar cache without waiting
+// (issue_page_id), and the step's wait and barrier that deliver it
+// (wait_barrier names the result, so that no use is placed before the wait).
+__device__ __forceinline__ void issue_page_id(const int32_t* table, int index, int& v) {
+    asm volatile("s_load_dword %0, %1, %2" : "=&s"(v) : "s"(table), "s"(__builtin_amdgcn_readfirstlane(index * 4)));
+}
+template <int N>
+__device__ __forceinline__ int wait_barrier(int& v) {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%1) lgkmcnt(0)\n\ts_barrier" : "+s"(v) : "n"(N) : "memory");
     return v;
 }
 
@@ -807,6 +821,7 @@ void decode_kernel(DecodeArgs a) {
         // cache one bf16 operand, the normalizer summing the rounded weights.
         constexpr bool kPairW = !C::lowbit && kRing;
         OpT pl_prev[kPairW ? 2 : 1] = {};
+        int pid_next = 0;                  // page id of the tile the next step stages
         bool move_pending = false;         // the previous tile moved the reference:
         float alpha_pending = 1.0f;        // accumulators *= alpha before its aggregation
 
@@ -822,8 +837,9 @@ void decode_kernel(DecodeArgs a) {
                 if (it == 0) plain_barrier<0>();
                 else plain_barrier<C::loads>();
             } else {
-                if (it == 0) pid = step_barrier<0>(bt, cur_page);
-                else pid = step_barrier<C::loads>(bt, cur_page);
+                // the page of tile it + D, fetched at the end of the previous step
+                if (it == 0) pid = wait_barrier<0>(pid_next);
+                else pid = wait_barrier<C::loads>(pid_next);
             }
             const int stage_j = it + C::D;
             constexpr int kStageQ = C::D % (C::lowbit ? C::NS : C::NT);    // slot of tile it + D
@@ -1035,6 +1051,7 @@ void decode_kernel(DecodeArgs a) {
                         ++cur_page;
                     }
                 }
+                if constexpr (!kRing) issue_page_id(bt, cur_page, pid_next);
             }
             // the buffer slots move on by one tile
             {
@@ -1054,8 +1071,10 @@ void decode_kernel(DecodeArgs a) {
         if (n_tiles > 0) {
             // prologue part 2: tile 0 decoded (low-bit) before the first step
             if constexpr (C::lowbit) {
-                (void)step_barrier<0>(bt, cur_page);
+                pid_next = step_barrier<0>(bt, cur_page);
                 dequant_tile<kDqKind>(stages, tiles, tid);
+            } else if constexpr (!kRing) {
+                issue_page_id(bt, cur_page, pid_next);
             }
             step(0, std::true_type{}, std::false_type{});
             for (int it = 1; it < n_tiles; ++it) step(it, std::true_type{}, std::true_type{});
