@@ -448,7 +448,7 @@ def config_report(args):
     for name, layer, label in CONFIG_SHAPES:
         res = {"workload": name, "layer": layer, "label": label}
         for kind in ("lowbit", "bf16"):
-            r = time_workload(name, kind, args.config_steps, 2, 1, layer=layer, device_tokens=True)
+            r = time_workload(name, kind, args.config_steps, args.config_warmup, 1, layer=layer, device_tokens=True)
             inten = r["flops_per_launch"] / r["bytes_per_launch"]
             bound = "mfma" if inten > ridge else "hbm"
             r["intensity_flop_per_byte"] = inten
@@ -539,7 +539,8 @@ def main():
                     help="instead of the step benchmark: the paper's 16-head attention latency grid")
     ap.add_argument("--configs", action="store_true",
                     help="report the full-size correctness configurations instead (one JSON line)")
-    ap.add_argument("--config-steps", type=int, default=5)
+    ap.add_argument("--config-steps", type=int, default=100)
+    ap.add_argument("--config-warmup", type=int, default=100)
     ap.add_argument("--grid-batches", default="8,32")
     ap.add_argument("--grid-contexts", default="1024,4096,8192,16384,32768,65536,131072,262144,524288,1048576")
     ap.add_argument("--grid-samples", type=int, default=30)
