@@ -181,7 +181,11 @@ int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens
  * Scores and latent aggregation run as fp16 matrix products with fp32
  * accumulation: the dequantized cache (x_hat, one fp16 rounding) and the
  * softmax weights are fp16 operands, so queries and x_hat must lie within the
- * fp16 range.  Under MLA_META_PAPER the RoPE scale enters as fp16(scale) (a
+ * fp16 range.  Past it the result is not finite, never a plausible value: a
+ * row that sees a key with |x_hat| >= 65520 in some channel comes out NaN or
+ * inf (output and lse), and a row of the same launch work item that does not
+ * see the key is non-finite in that key's overflowing channels.  Under
+ * MLA_META_PAPER the RoPE scale enters as fp16(scale) (a
  * second rounding of the RoPE key, relative 2^-11).  The output is rounded to
  * bf16 once.
  */
