@@ -10,11 +10,13 @@ one's bytes in the 256 MB last-level cache.
 
 Printed: one JSON line (stdout) with whole-step decode tokens/s at that shape,
 the decode kernel's roofline (live HIP-event timing of every timed launch on
-its own dispatch: mean, median, p10, p90), the GPU clock sampled during the
-timed steps, the same step over a BF16 cache (the unquantized comparison), the
-32 x 4096 workload, the paper's sampling protocol (graph replay, caches
-flushed before every sample, 2 runs x 2 rounds x 30 samples in alternating
-order), and the CPU oracle timed on a bounded sample of the headline workload.
+its own dispatch: mean, median, p10, p90), the sustained clock and socket
+power (the step run back to back for 1.5 s after the timed steps), the same
+step over a BF16 cache (the unquantized comparison), the 32 x 4096 workload,
+the paper's sink/recent BF16 protection at both shapes, the paper's sampling
+protocol (graph replay, caches flushed before every sample, 2 runs x 2 rounds
+x 30 samples in alternating order), and the CPU oracle timed on a bounded
+sample of the headline workload.
 """
 from __future__ import annotations
 
@@ -603,17 +605,26 @@ def main():
     if "protected" in kinds:
         from paper_2609_36760_amd import _binding as mb
         from paper_2609_36760_amd import synthetic as syn
-        # as many key splits per sequence as the unprotected plan: the tile list
-        # (packed tiles + protected rows) is one tile longer than the sequence
-        w = syn.WORKLOADS[SMALL]
-        L, pol = w.context, mb.protect_policy(4, 128)
-        n_list = -(-(L - pol.recent) // 32) - pol.sink // 32 + -(-(pol.sink + pol.recent) // 32)
-        split = args.protect_split or 32 * -(-n_list // -(-L // w.split_tokens))
+        pol = mb.protect_policy(4, 128)
+
+        def protect_split(name):
+            # as many key splits per sequence as the unprotected plan: the tile list
+            # (packed tiles + protected rows) is one tile longer than the sequence
+            w = syn.WORKLOADS[name]
+            L = w.context
+            n_list = -(-(L - pol.recent) // 32) - pol.sink // 32 + -(-(pol.sink + pol.recent) // 32)
+            return 32 * -(-n_list // -(-L // w.split_tokens))
+
         pr = time_workload(SMALL, "lowbit", args.small_steps, args.small_warmup, LAYERS[SMALL], protect=pol,
-                           split_tokens=split)
+                           split_tokens=args.protect_split or protect_split(SMALL))
         pr["step_vs_unprotected"] = (extra[SMALL]["c4r4"]["ms_per_step"] / pr["ms_per_step"]
                                      if SMALL in extra else None)
         extra["protected_sink4_recent128_" + SMALL] = pr
+        # the paper's policy at the headline shape (its efficiency runs all use it)
+        pm = time_workload(MAIN, "lowbit", args.steps, args.warmup, LAYERS[MAIN], protect=pol,
+                           split_tokens=protect_split(MAIN), device_tokens=True)
+        pm["step_vs_unprotected"] = main_lb["ms_per_step"] / pm["ms_per_step"]
+        extra["protected_sink4_recent128_" + MAIN] = pm
     if "paper" in kinds:
         pp = time_workload(SMALL, "lowbit", args.small_steps, args.small_warmup, LAYERS[SMALL], meta="paper")
         pp["cache_bytes_per_token"] = 320
