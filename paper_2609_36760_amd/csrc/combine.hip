@@ -29,7 +29,8 @@ namespace {
 constexpr int kDc = 512;
 constexpr int kWaves = 4;         // waves (and rows) per workgroup
 constexpr int kShare = 16;        // splits per sequence from which the waves share a row
-constexpr int kBatch = 8;       // splits whose loads are in flight together
+// kBatch: splits whose loads are in flight together (4 when sequences have
+// at most 4 splits on average, so that no load re-reads a split, else 8)
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -43,6 +44,7 @@ struct RowState {
     float mx, s, o[8];
 };
 
+template <int kBatch>
 __device__ __forceinline__ RowState combine_splits(const CombineArgs& a, int r, int rows_per_seq, int j0, int j1,
                                                    int first, int step, int lane) {
     RowState st{-INFINITY, 0.0f, {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}};
@@ -95,7 +97,7 @@ __device__ __forceinline__ void store_row(const CombineArgs& a, int64_t row, con
 
 // kShared: one row per workgroup, its splits shared by the four waves (many
 // splits per sequence); else four rows per workgroup, one per wave.
-template <bool kShared>
+template <bool kShared, int kBatch>
 __global__ __launch_bounds__(64 * kWaves) void combine_kernel(CombineArgs a) {
     // rows (b * s_q + i) * H + h in 8 contiguous ranges of blocks, range x on
     // XCD x (block id mod 8), the XCD whose decode workgroups wrote most of them
@@ -115,12 +117,12 @@ __global__ __launch_bounds__(64 * kWaves) void combine_kernel(CombineArgs a) {
     const int j1 = a.split_indptr[b + 1];
 
     if constexpr (!kShared) {
-        const RowState st = combine_splits(a, r, rows_per_seq, j0, j1, 0, 1, lane);
+        const RowState st = combine_splits<kBatch>(a, r, rows_per_seq, j0, j1, 0, 1, lane);
         store_row(a, row, st.o, st.mx, st.s, lane);
     } else {
         __shared__ float sh_o[kWaves][8][64];
         __shared__ float sh_ms[kWaves][2];
-        const RowState st = combine_splits(a, r, rows_per_seq, j0, j1, wave, kWaves, lane);
+        const RowState st = combine_splits<kBatch>(a, r, rows_per_seq, j0, j1, wave, kWaves, lane);
 #pragma unroll
         for (int q = 0; q < 8; ++q) sh_o[wave][q][lane] = st.o[q];
         if (lane == 0) {
@@ -153,12 +155,15 @@ hipError_t launch_combine(const CombineArgs& a, int32_t num_splits, hipStream_t 
     const int64_t rows = static_cast<int64_t>(a.B) * a.s_q * a.H;
     if (rows == 0) return hipSuccess;
     if (num_splits >= static_cast<int64_t>(kShare) * a.B) {
-        hipLaunchKernelGGL(combine_kernel<true>, dim3(static_cast<unsigned>((rows + 7) / 8 * 8)), dim3(64 * kWaves),
-                           0, stream, a);
+        hipLaunchKernelGGL((combine_kernel<true, 8>), dim3(static_cast<unsigned>((rows + 7) / 8 * 8)),
+                           dim3(64 * kWaves), 0, stream, a);
     } else {
         const int64_t blocks = (rows + kWaves - 1) / kWaves;
-        hipLaunchKernelGGL(combine_kernel<false>, dim3(static_cast<unsigned>((blocks + 7) / 8 * 8)),
-                           dim3(64 * kWaves), 0, stream, a);
+        const dim3 grid(static_cast<unsigned>((blocks + 7) / 8 * 8)), block(64 * kWaves);
+        if (num_splits <= 4 * static_cast<int64_t>(a.B))
+            hipLaunchKernelGGL((combine_kernel<false, 4>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((combine_kernel<false, 8>), grid, block, 0, stream, a);
     }
     return hipGetLastError();
 }

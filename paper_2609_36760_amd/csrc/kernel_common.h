@@ -43,7 +43,8 @@ __device__ __forceinline__ int slot_offset(int j, int n, int bytes) {
     return off;
 }
 
-// Direct-to-LDS load of 16 bytes per lane: lane l copies base + voff into LDS
+// Direct-to-LDS load of 16 bytes per lane, marked non-temporal (the cache
+// bytes are read once per step): lane l copies base + voff into LDS
 // bytes [lds + 16 l, lds + 16 l + 16) (base and lds wave-uniform).  Written as
 // inline assembly so that the compiler does not track it: it would otherwise
 // wait for every such load in flight before any LDS read of the same array.
@@ -54,7 +55,7 @@ __device__ __forceinline__ void dma16(const uint8_t* base, uint32_t voff, uint32
     uint32_t saved;
     asm volatile(
         "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\t"
-        "global_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
+        "global_load_lds_dwordx4 %1, %2 nt\n\ts_mov_b32 m0, %0"
         : "=&s"(saved)
         : "v"(voff), "s"(base), "s"(lds)
         : "memory");
@@ -64,7 +65,7 @@ __device__ __forceinline__ void dma16(const uint8_t* base, uint32_t voff, uint32
 // the compiler then sets and knows to be in use; the leading wait state covers
 // the M0 write before the load reads it).
 __device__ __forceinline__ void dma16_m0(const uint8_t* base, uint32_t voff, uint32_t lds) {
-    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(base), "{m0}"(lds) : "memory");
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 nt" : : "v"(voff), "s"(base), "{m0}"(lds) : "memory");
 }
 
 // (x & m) | o in one v_and_or_b32 (the compiler otherwise splits it in two
