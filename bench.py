@@ -35,7 +35,6 @@ if ROOT not in sys.path:
 METRIC = "decode attn tokens/s + HBM GB/s & MFMA util vs peak, 128 heads, INT4/INT4 vs BF16"
 MAIN = "c4r4_b64_h128_32k"            # the headline: 64 x 32768, INT4/INT4, 128 heads
 SMALL = "dsv3_b32_h128_4k_c4r4"       # 32 x 4096
-TARGET = MAIN
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 LAYERS = {MAIN: 2, SMALL: 8}       # resident layer caches cycled by the timed steps
