@@ -548,7 +548,7 @@ def main():
     ap.add_argument("--grid-warmup", type=int, default=5)
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no multi-GPU path; "
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no multi-GPU path; "
               "the per-GPU kernel is the whole workload.", file=sys.stderr)
         sys.exit(2)
     import torch

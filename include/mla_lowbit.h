@@ -26,7 +26,7 @@
  *   - Arguments are validated on the host before any HIP call.  Return codes:
  *       MLA_OK      success (work enqueued)
  *       MLA_EINVAL  a null pointer, a negative size or an ill-formed format
- *       MLA_ENOTSUP well-formed, but a shape this build does not implement
+ *       MLA_ENOTSUP well-formed, but a shape the library does not implement
  *       MLA_EHIP    a HIP launch failed; mla_last_hip_error() gives the code
  *   - Device-resident values (page ids, sequence lengths, split offsets) are
  *     not readable by the host without a synchronization and are preconditions:
