@@ -244,7 +244,8 @@ class AttnStats:
 
 def compare_sequence(stats, got_out, got_lse, ql, qr, c, k, tau, s_q, heads=None):
     """Oracle attention of one sequence over values ``c, k`` (fp64), compared
-    with the GPU's ``got_out [s_q, H, 512]`` (bf16 bits) and ``got_lse``."""
+    with the GPU's ``got_out [s_q, H, 512]`` (bf16 bits) and ``got_lse``;
+    returns the oracle's outputs."""
     H = ql.shape[1]
     hs = np.arange(H) if heads is None else np.asarray(heads)
     L = c.shape[0]
@@ -254,6 +255,7 @@ def compare_sequence(stats, got_out, got_lse, ql, qr, c, k, tau, s_q, heads=None
     bound = lse_bound(ql[:, hs], qr[:, hs], c, k, tau, L, s_q)
     tol = elem_bound(ql[:, hs], qr[:, hs], c, k, tau, L, s_q, want_out, bound)
     stats.add(got, want_out, gl, want_lse, bound, tol)
+    return want_out
 
 
 def check_sequence(stats, run, b, heads=None):

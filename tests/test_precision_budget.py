@@ -55,49 +55,88 @@ def _bf16_pair(x):
 
 
 def _emulate(ql, qr, c_hat, kr_hat, tau, s_q, kv_round, p_round, split=0, part_round=_ident,
-             score_round=None, sum_rounded=True):
+             score_round=None, sum_rounded=True, raw=False, groups=None, lim=None, partials=False,
+             p_format=None):
     """Output of a kernel that rounds the reconstructed values with kv_round
     (scores: score_round, default the same), the weights with p_round and the
     normalized split partials with part_round.  As in the kernels, the weights
     are 2^(x - ref) with a lazy reference per row and key range: the first
     32-key tile's maximum, moved only when a later tile's maximum exceeds it by
     more than 10 (log2 units); the normalizer sums the rounded weights
-    (sum_rounded) or the exact ones."""
+    (sum_rounded) or the exact ones.  The output is rounded to bf16 unless
+    ``raw``.
+
+    ``groups`` (a group id per row) makes the move wave-uniform as in the
+    kernels: when any row of a group moves, every row of the group whose tile
+    maximum is above its reference takes that maximum.  ``lim`` overrides the
+    rows' visible-key counts (default: the rows are every query token of some
+    heads, token-major).  ``partials`` returns, per key range, the unrounded
+    partial (true maximum in natural-log units, sum of the weights relative to
+    it, normalized weighted sum) instead of the output, and with ``p_format``
+    ("f16" or "bf16", the format p_round rounds to) how far each of the last
+    two may move if every weight lying within a relative 2^-16 of a rounding
+    tie of that format rounds the other way (fp32 scores differ from these
+    fp64 ones by less than that)."""
     R, L = ql.shape[0], c_hat.shape[0]
     K = np.concatenate([kv_round(c_hat), kv_round(kr_hat)], 1).astype(np.float64)
     Ks = K if score_round is None else np.concatenate([score_round(c_hat), kv_round(kr_hat)], 1).astype(np.float64)
     S = (np.concatenate([ql, qr], 1) @ Ks.T).astype(np.float32)
-    lim = at.decode_limits(L, s_q, R // s_q)
-    x = np.where(np.arange(L)[None] < lim[:, None], S * np.float32(tau * np.log2(np.e)), -np.inf)
+    lim = at.decode_limits(L, s_q, R // s_q) if lim is None else np.asarray(lim)
+    x = np.where(np.arange(L)[None] < lim[:, None], S * np.float32(tau * np.log2(np.e)), -np.inf).astype(np.float64)
     bounds = [(a, min(a + split, L)) for a in range(0, L, split)] if split else [(0, L)]
-    ms, ss, os_ = [], [], []
+    ms, ss, os_, parts = [], [], [], []
+    mant, ulp_min = {"f16": (11, 2.0 ** -24), "bf16": (8, 2.0 ** -133), None: (0, 0.0)}[p_format]
+    absK = np.abs(K[:, :512])
     for a, b in bounds:
         ref = np.full(R, -np.inf)
         o = np.zeros((R, 512))
         s = np.zeros(R)
+        tie_o = np.zeros((R, 512))
+        tie_s = np.zeros(R)
         for t0 in range(a, b, 32):
             xx = x[:, t0:min(t0 + 32, b)]
             mt = xx.max(1)
             first = ~np.isfinite(ref)
             ref = np.where(first, mt, ref)
             move = np.isfinite(mt) & (mt > ref + 10)
+            if groups is not None:
+                wave = np.zeros(int(groups.max()) + 1, bool)
+                np.logical_or.at(wave, groups, move)
+                move = wave[groups] & np.isfinite(mt) & (mt > ref)
             new_ref = np.where(move, mt, ref)
-            alpha = np.where(move, np.exp2(ref - new_ref), 1.0)
+            alpha = np.where(move, np.exp2(np.where(move, ref - new_ref, 0.0)), 1.0)
             o *= alpha[:, None]
             s *= alpha
+            tie_o *= alpha[:, None]
+            tie_s *= alpha
             ref = new_ref
             p = np.exp2(xx - np.where(np.isfinite(ref), ref, 0.0)[:, None]).astype(np.float32)
             pr = p_round(p).astype(np.float64)
             o += pr @ K[t0:t0 + xx.shape[1], :512]
             s += (pr if sum_rounded else p.astype(np.float64)).sum(1)
+            if partials and p_format is not None:
+                p64 = p.astype(np.float64)
+                ulp = np.maximum(np.exp2(np.floor(np.log2(np.maximum(p64, 1e-300))) - (mant - 1)), ulp_min)
+                near = (p64 > 0) & (np.abs(np.abs(p64 - pr) - ulp / 2) <= 2.0 ** -16 * p64)
+                dp = np.where(near, ulp, 0.0)
+                tie_o += dp @ absK[t0:t0 + xx.shape[1]]
+                tie_s += dp.sum(1)
         on = np.divide(o, s[:, None], out=np.zeros((R, 512)), where=s[:, None] > 0)
+        if partials:
+            top = x[:, a:b].max(1)
+            f = np.where(np.isfinite(top), np.exp2(np.where(np.isfinite(top), ref - top, 0.0)), 0.0)
+            tol = np.divide(tie_o + np.abs(on) * tie_s[:, None], s[:, None], out=np.zeros((R, 512)),
+                            where=s[:, None] > 0)
+            parts.append((top * np.log(2.0), s * f, on, tol, tie_s * f))
         ms.append(np.where(s > 0, np.where(np.isfinite(ref), ref, 0.0), -np.inf))
         ss.append(s)
         os_.append(part_round(on).astype(np.float64) if split else on)
+    if partials:
+        return parts
     M = np.max(ms, 0)
     W = [np.exp2(mm - M) * s for mm, s in zip(ms, ss)]
     O = sum(w[:, None] * o for w, o in zip(W, os_)) / sum(W)[:, None]
-    return _rnd_bf16(O.astype(np.float32)).astype(np.float64)
+    return O if raw else _rnd_bf16(O.astype(np.float32)).astype(np.float64)
 
 
 def _excess_ratio(got, want):
@@ -230,3 +269,32 @@ def test_fp16_limited_batches_are_the_rounding_models():
     a_exact = _aging_excess(score_round=_ident)
     assert abs(a - FP16_LIMITED["aging_c2_h128_sq2_split32"]) < 1e-4, a
     assert a_exact < 0.0125, a_exact
+
+
+def test_model_partials_combine_to_its_output():
+    """The model's partials (the full-output GPU test compares the kernels'
+    split partials with them) combine, exactly, to the model's unrounded
+    output; a wave-uniform move changes only the references, so without
+    weight rounding (the fp32 weights aside) it leaves the result as it is;
+    and the tie allowance is zero without a weight format and small
+    otherwise."""
+    w, rows = _c4_h64_batch_rows()
+    ql, qr, c, k, _ = rows[1]                                 # 400 keys, 64 rows
+    kw = dict(split=128, part_round=lambda v: v)          # partials left unrounded
+    out = _emulate(ql, qr, c, k, w.tau, w.s_q, _rnd_f16, _rnd_f16, raw=True, **kw)
+    parts = _emulate(ql, qr, c, k, w.tau, w.s_q, _rnd_f16, _rnd_f16, partials=True, p_format="f16", **kw)
+    assert len(parts) == 4
+    m = np.stack([p[0] for p in parts])
+    s = np.stack([p[1] for p in parts])
+    u = np.stack([p[2] for p in parts])
+    W = np.exp(m - m.max(0)) * s
+    np.testing.assert_allclose((W[..., None] * u).sum(0) / W.sum(0)[:, None], out, rtol=1e-12, atol=1e-12)
+    tol = np.stack([p[3] for p in parts])
+    assert np.all(tol >= 0) and np.all(np.isfinite(tol))
+    assert 0 < np.median(tol / np.abs(u).max(-1, keepdims=True)) < 2.0 ** -15
+    none = _emulate(ql, qr, c, k, w.tau, w.s_q, _rnd_f16, _rnd_f16, partials=True, **kw)
+    assert all(np.all(p[3] == 0) and np.all(p[4] == 0) for p in none)
+    groups = np.repeat(np.arange(2), 32)
+    exact = _emulate(ql, qr, c, k, w.tau, w.s_q, _ident, _ident, raw=True, **kw)
+    waved = _emulate(ql, qr, c, k, w.tau, w.s_q, _ident, _ident, raw=True, groups=groups, **kw)
+    np.testing.assert_allclose(waved, exact, rtol=0, atol=1e-6)
