@@ -10,8 +10,10 @@ then the combine), against the oracle's attention (Sec. 2.1, eq. mla_compact)
 over the values the stored bytes hold, with the global rule and bounds of
 ``gpu_support`` applied per configuration.  The oracle runs per sequence in
 16 worker processes (started fresh, no GPU use); each packs the sequence's
-tokens, checks them against a digest of the GPU's pages, decodes them and
-returns its sequence's statistics.
+tokens (Appendix C.4, "Affine group quantization"), checks the packing
+against a digest of the GPU's pages (the BF16 cache: its rows) -- every
+byte of every cache, 10.8M low-bit tokens in all -- decodes it and returns
+its sequence's statistics.
 
 Over all outputs, some configurations break the max rule in a few rows:
 outlier channels (10x) whose output is tens of times the RMS, in rows whose
