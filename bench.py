@@ -225,16 +225,15 @@ def time_workload(name, kind, steps, warmup, layers, token_cache=None, protect=N
                   split_indptr=run.split_indptr, num_splits=run.num_splits, out=run.out, lse=run.lse,
                   part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
         else:
-            mb.mla_lowbit_quant_append_protected(run.fmt, protect, run.new_c, run.new_k, run.new_slots, cache,
-                                                 run.num_pages, run.new_seq, run.new_pos, run.seq_lens,
-                                                 run.prot_slot, prot, run.num_prot, stream=sh)
+            # under protection too: the new tokens' packed bytes and bf16 rows are
+            # written inside the decode launch
             if ev is not None:
                 ev.arm(i - warmup)
-            mb.mla_lowbit_decode_attn_protected(
-                run.fmt, protect, run.q_lat, run.q_rope, cache, run.num_pages, run.block_table, run.seq_lens,
-                run.s_q, run.H, run.tau, prot, run.num_prot, run.prot_slot, split_tokens=run.split_tokens,
-                split_indptr=run.split_indptr, num_splits=run.num_splits, out=run.out, lse=run.lse,
-                part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
+            mb.mla_lowbit_append_decode_attn_protected(
+                run.fmt, protect, run.new_c, run.new_k, run.new_slots, run.q_lat, run.q_rope, cache, run.num_pages,
+                run.block_table, run.seq_lens, run.s_q, run.H, run.tau, prot, run.num_prot, run.prot_slot,
+                split_tokens=run.split_tokens, split_indptr=run.split_indptr, num_splits=run.num_splits,
+                out=run.out, lse=run.lse, part_m=run.part_m, part_s=run.part_s, part_o=run.part_o, stream=sh)
         if run.split_tokens:
             mb.mla_splitkv_combine(run.part_m, run.part_s, run.part_o, run.split_indptr, run.num_splits, run.B,
                                    run.s_q, run.H, run.out, run.lse, stream=sh)

@@ -371,6 +371,39 @@ int mla_lowbit_decode_attn_protected(const mla_cache_format* f, const mla_protec
                                      hipStream_t stream);
 
 /*
+ * The step's append and decode under protection in one call (Appendix C.5,
+ * "BF16 protection and cache lifecycle", "Cache update and tile reuse"):
+ * equivalent to mla_lowbit_quant_append_protected of the n = B * s_q new
+ * tokens -- token (b, i), row b * s_q + i of c_kv / k_rope, at position
+ * seq_lens[b] - s_q + i of sequence b and slot slot_mapping[b * s_q + i] --
+ * followed by mla_lowbit_decode_attn_protected, with identical cache bytes,
+ * protection buffer rows and outputs.  A buffer index outside [0, num_prot)
+ * skips the token's protection row (as the writer does) and is clamped for
+ * the decode (as the decode does).  For s_q * H > 32 the writer runs inside
+ * the decode launch: the workgroups that read a new token quantize and store
+ * it first (its protection row too, for a token protected after the step).
+ * Otherwise the protected writer is launched separately first.  Arguments
+ * and errors as for the two calls; prot is written (device, 16-byte aligned).
+ * Precondition: the sequences' protection buffers are distinct (a sequence
+ * whose index is clamped onto another's buffer may read that buffer's new
+ * rows before or after they are written).
+ */
+int mla_lowbit_append_decode_attn_protected(const mla_cache_format* f, const mla_protect_policy* p,
+                                            const uint16_t* c_kv, int64_t c_kv_stride,
+                                            const uint16_t* k_rope, int64_t k_rope_stride,
+                                            const int64_t* slot_mapping,
+                                            const uint16_t* q_lat, const uint16_t* q_rope,
+                                            void* cache, int64_t num_pages,
+                                            const int32_t* block_table, int32_t max_pages_per_seq,
+                                            const int32_t* seq_lens, int32_t B, int32_t s_q, int32_t H,
+                                            float softmax_scale,
+                                            void* prot, int64_t num_prot, const int32_t* prot_slot,
+                                            int32_t split_tokens, const int32_t* split_indptr, int32_t num_splits,
+                                            uint16_t* out, float* lse,
+                                            float* part_m, float* part_s, uint16_t* part_o,
+                                            hipStream_t stream);
+
+/*
  * Per-layer persistent cache bytes of one request of L tokens
  * (Appendix C.5, eq. physical_cache_storage):
  *   ceil(L / page_size) * (page bytes + 8) + protection buffer bytes

@@ -24,7 +24,7 @@ SYMBOLS = (
     "mla_status_str", "mla_last_hip_error", "mla_protect_buffer_bytes", "mla_lowbit_quant_append_protected",
     "mla_plan_splits_protected", "mla_lowbit_decode_attn_protected", "mla_persistent_cache_bytes",
     "mla_lowbit_append_decode_attn", "mla_bf16_append_decode_attn", "mla_time_next_decode_launch",
-    "mla_lowbit_decode_attn_noalloc",
+    "mla_lowbit_decode_attn_noalloc", "mla_lowbit_append_decode_attn_protected",
 )
 
 
@@ -96,6 +96,9 @@ def library() -> ctypes.CDLL:
         "mla_plan_splits_protected": (I32, [P, I32, I32, POL, P]),
         "mla_lowbit_decode_attn_protected": (ctypes.c_int, [FMT, POL, P, P, P, I64, P, I32, P, I32, I32, I32, F32,
                                                             P, I64, P, I32, P, I32, P, P, P, P, P, P]),
+        "mla_lowbit_append_decode_attn_protected": (ctypes.c_int, [FMT, POL, P, I64, P, I64, P, P, P, P, I64, P, I32,
+                                                                   P, I32, I32, I32, F32, P, I64, P, I32, P, I32,
+                                                                   P, P, P, P, P, P]),
         "mla_lowbit_decode_attn_noalloc": (ctypes.c_int, [FMT, P, P, P, I64, P, I32, P, I32, I32, I32, F32,
                                                           I32, P, I32, P, P, P]),
         "mla_status_str": (ctypes.c_char_p, [ctypes.c_int]),
@@ -283,6 +286,20 @@ def mla_lowbit_decode_attn_protected(fmt, policy, q_lat, q_rope, cache, num_page
         _ptr(block_table), block_table.shape[1], _ptr(seq_lens), B, s_q, H, float(softmax_scale),
         _ptr(prot), num_prot, _ptr(prot_slot), split_tokens, _ptr(split_indptr), num_splits,
         _ptr(out), _ptr(lse), _ptr(part_m), _ptr(part_s), _ptr(part_o), _stream(stream)))
+
+
+def mla_lowbit_append_decode_attn_protected(fmt, policy, c_kv, k_rope, slot_mapping, q_lat, q_rope, cache,
+                                            num_pages, block_table, seq_lens, s_q, H, softmax_scale, prot,
+                                            num_prot, prot_slot, split_tokens=0, split_indptr=None, num_splits=0,
+                                            out=None, lse=None, part_m=None, part_s=None, part_o=None, stream=None):
+    """The step's new tokens appended under protection, then decode."""
+    B = q_lat.shape[0]
+    _check("mla_lowbit_append_decode_attn_protected", library().mla_lowbit_append_decode_attn_protected(
+        ctypes.byref(fmt), ctypes.byref(policy), _ptr(c_kv), c_kv.stride(0), _ptr(k_rope), k_rope.stride(0),
+        _ptr(slot_mapping), _ptr(q_lat), _ptr(q_rope), _ptr(cache), num_pages, _ptr(block_table),
+        block_table.shape[1], _ptr(seq_lens), B, s_q, H, float(softmax_scale), _ptr(prot), num_prot,
+        _ptr(prot_slot), split_tokens, _ptr(split_indptr), num_splits, _ptr(out), _ptr(lse), _ptr(part_m),
+        _ptr(part_s), _ptr(part_o), _stream(stream)))
 
 
 def mla_persistent_cache_bytes(fmt: mla_cache_format, policy, L: int) -> int:

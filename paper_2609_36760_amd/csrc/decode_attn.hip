@@ -515,6 +515,64 @@ __device__ __forceinline__ void append_in_launch(const DecodeArgs& a, int b, int
     }
 }
 
+// The same under BF16 protection: the key list of a work item (packed tiles,
+// then the protected rows in position order; see below) decides which work
+// item reads a new token, and that work item writes it: the packed copy, as
+// the plain writer does for every token, and for a token that is protected
+// after the step (position p < sink, or p >= L - recent) its bf16 row in the
+// sequence's protection buffer, row p or sink + (p - sink) mod recent -- the
+// ring row of the token leaving the window, which this launch reads from its
+// packed copy.  A protection buffer index outside [0, num_prot) skips the row
+// (as the protected writer does; the decode clamps it).  When a written token
+// lies in the first tiles the work item stages, the stores land first.
+template <int KIND>
+__device__ __forceinline__ void append_in_launch_protected(const DecodeArgs& a, int b, int L, int u0, int u1,
+                                                           int n_pk, int pk0, int tid) {
+    using C = Cfg<KIND>;
+    constexpr int kDpro = C::D > Cfg<KIND_BF16>::D ? C::D : Cfg<KIND_BF16>::D;
+    const int sink = a.sink, recent = a.recent;
+    const int nsink = min(sink, L), r0 = max(sink, L - recent);
+    auto is_prot = [&](int p) { return p < sink || p >= L - recent; };
+    // list tile of position p: a packed position by its tile (from the tile
+    // holding token `sink`), a protected one by its index among the protected rows
+    auto list_tile = [&](int p) {
+        return is_prot(p) ? n_pk + (min(p, nsink) + max(0, p - r0)) / kTile : p / kTile - pk0;
+    };
+    bool early = false;
+    for (int i = 0; i < a.s_q; ++i) {
+        const int pos = L - a.s_q + i;
+        const int u = list_tile(pos);
+        if (pos >= 0 && u >= u0 && u < u1 && u - u0 < kDpro) early = true;
+    }
+    const int i = tid / 72, r = tid % 72;
+    const int pos = L - a.s_q + i;
+    if (i < a.s_q && pos >= 0 && list_tile(pos) >= u0 && list_tile(pos) < u1) {
+        const int64_t tok = static_cast<int64_t>(b) * a.s_q + i;
+        const int64_t slot = a.new_slots[tok];
+        const int64_t num_slots = a.num_pages * a.g.page_size;
+        if (slot >= 0 && slot < num_slots) {
+            uint8_t* base = const_cast<uint8_t*>(a.cache) + slot / a.g.page_size * a.g.page_bytes;
+            const int64_t off = slot % a.g.page_size;
+            const bool rope = r >= 64;
+            const uint16_t* src = rope ? a.new_k + tok * a.new_k_stride + (r - 64) * 8
+                                       : a.new_c + tok * a.new_c_stride + r * 8;
+            const uint4 raw = *reinterpret_cast<const uint4*>(src);
+            wc::quantize_store<C::cc == 256 ? 4 : 2, C::pmeta>(raw, rope, r >> 3, r & 7, base, off, a.g);
+            const int64_t ps = a.prot_slot[b];
+            if (is_prot(pos) && ps >= 0 && ps < a.num_prot) {
+                const int prow = pos < sink ? pos : sink + (pos - sink) % recent;
+                // [c_kv | k_rope] row: piece r at byte 16 r (the RoPE key from byte 1024)
+                uint8_t* dst = const_cast<uint8_t*>(a.prot) + (ps * (sink + recent) + prow) * 1152 + 16 * r;
+                *reinterpret_cast<uint4*>(dst) = raw;
+            }
+        }
+    }
+    if (early) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    }
+}
+
 // ---------------------------------------------------------------------------
 // 3. The kernel.
 //
@@ -1106,6 +1164,9 @@ void decode_kernel(DecodeArgs a) {
         if (a.split_tokens != 0) {
             u0 = split * (a.split_tokens / kTile);
             u1 = min(u0 + a.split_tokens / kTile, n_list);
+        }
+        if constexpr (Cfg<KIND>::lowbit) {
+            if (a.new_c != nullptr) append_in_launch_protected<KIND>(a, b, L, u0, u1, n_pk, pk0, tid);
         }
         if (u0 < n_pk) {
             const int tb = kTile * (pk0 + u0);

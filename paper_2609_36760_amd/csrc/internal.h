@@ -34,8 +34,11 @@ struct AppendArgs {
     // BF16 protection writes (lowbit_append_kernel<CBITS, true> only)
     uint8_t* prot;
     int64_t num_prot;
-    const int32_t* token_seq;   // [n] sequence of each token
-    const int32_t* positions;   // [n] position of each token in its sequence
+    const int32_t* token_seq;   // [n] sequence of each token (nullptr: token t is query
+                                //     token t % s_q of sequence t / s_q, the step's append)
+    const int32_t* positions;   // [n] position of each token in its sequence (nullptr with
+                                //     token_seq: seq_lens[b] - s_q + t % s_q)
+    int32_t s_q;
     const int32_t* seq_lens;    // [B] lengths after the append
     const int32_t* prot_slot;   // [B] buffer of each sequence
     int32_t B;
@@ -69,10 +72,10 @@ struct DecodeArgs {
     int64_t num_prot;
     const int32_t* prot_slot;   // [B] buffer of each sequence
     int32_t sink, recent;
-    // In-launch append (decode_kernel<KIND, false> only; new_c == nullptr: none):
-    // token (b, i) of [B][s_q], position seq_lens[b] - s_q + i of sequence b,
-    // quantized (or copied, BF16) into slot new_slots[b * s_q + i] before it is
-    // read.
+    // In-launch append (decode_kernel only; new_c == nullptr: none): token (b, i)
+    // of [B][s_q], position seq_lens[b] - s_q + i of sequence b, quantized (or
+    // copied, BF16) into slot new_slots[b * s_q + i] before it is read; under
+    // protection also its bf16 row into the protection buffer.
     const uint16_t* new_c;
     int64_t new_c_stride;
     const uint16_t* new_k;

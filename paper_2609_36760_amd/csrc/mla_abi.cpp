@@ -237,9 +237,21 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
     const bool narrow = s_q * H <= mla::kNarrowRows;
     if (nt != nullptr && B > 0) {
         if (narrow) {
-            // few query rows: the writer runs as its own launch first
+            // few query rows: the writer runs as its own launch first (under
+            // protection the protected writer, the step's tokens implied)
+            mla::AppendArgs w{};
+            if (pd != nullptr) {
+                w.prot = static_cast<uint8_t*>(const_cast<void*>(pd->prot));
+                w.num_prot = pd->num_prot;
+                w.seq_lens = seq_lens;
+                w.prot_slot = pd->prot_slot;
+                w.B = B;
+                w.s_q = s_q;
+                w.sink = pd->policy->sink;
+                w.recent = pd->policy->recent;
+            }
             st = append_common(f, lowbit, nt->c_kv, nt->c_kv_stride, nt->k_rope, nt->k_rope_stride,
-                               nt->slot_mapping, B * s_q, const_cast<void*>(cache), num_pages, stream);
+                               nt->slot_mapping, B * s_q, const_cast<void*>(cache), num_pages, stream, w);
             if (st != MLA_OK) return st;
         } else {
             a.new_c = nt->c_kv;
@@ -395,6 +407,31 @@ int mla_lowbit_decode_attn_protected(const mla_cache_format* f, const mla_protec
     return decode_common(f, true, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
                          s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
                          part_o, &pd, stream);
+}
+
+int mla_lowbit_append_decode_attn_protected(const mla_cache_format* f, const mla_protect_policy* p,
+                                            const uint16_t* c_kv, int64_t c_kv_stride, const uint16_t* k_rope,
+                                            int64_t k_rope_stride, const int64_t* slot_mapping,
+                                            const uint16_t* q_lat, const uint16_t* q_rope, void* cache,
+                                            int64_t num_pages, const int32_t* block_table,
+                                            int32_t max_pages_per_seq, const int32_t* seq_lens, int32_t B,
+                                            int32_t s_q, int32_t H, float softmax_scale, void* prot,
+                                            int64_t num_prot, const int32_t* prot_slot, int32_t split_tokens,
+                                            const int32_t* split_indptr, int32_t num_splits, uint16_t* out,
+                                            float* lse, float* part_m, float* part_s, uint16_t* part_o,
+                                            hipStream_t stream) {
+    int st = check_lowbit_format(f);
+    if (st != MLA_OK) return st;
+    st = check_policy(p);
+    if (st != MLA_OK) return st;
+    if (B < 0 || s_q < 0) return MLA_EINVAL;
+    st = check_append(c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, B * s_q, cache, num_pages);
+    if (st != MLA_OK) return st;
+    const NewTokens nt{c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping};
+    const ProtDecode pd{p, prot, num_prot, prot_slot};
+    return decode_common(f, true, q_lat, q_rope, cache, num_pages, block_table, max_pages_per_seq, seq_lens, B,
+                         s_q, H, softmax_scale, split_tokens, split_indptr, num_splits, out, lse, part_m, part_s,
+                         part_o, &pd, stream, &nt);
 }
 
 int32_t mla_plan_splits(const int32_t* seq_lens, int32_t B, int32_t split_tokens, int32_t* split_indptr) {

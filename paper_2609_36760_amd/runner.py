@@ -282,13 +282,21 @@ class DecodeRun:
         self.attend(stream)
 
     def fused_step(self, stream=None):
-        """The same step with the append inside the decode call (unprotected caches)."""
-        assert self.protect is None
-        fn = mb.mla_lowbit_append_decode_attn if self.kind == "lowbit" else mb.mla_bf16_append_decode_attn
-        fn(self.fmt, self.new_c, self.new_k, self.new_slots, self.q_lat, self.q_rope, self.cache, self.num_pages,
-           self.block_table, self.seq_lens, self.s_q, self.H, self.tau, split_tokens=self.split_tokens,
-           split_indptr=self.split_indptr, num_splits=self.num_splits, out=self.out, lse=self.lse,
-           part_m=self.part_m, part_s=self.part_s, part_o=self.part_o, stream=stream)
+        """The same step with the append inside the decode call."""
+        if self.protect is not None:
+            mb.mla_lowbit_append_decode_attn_protected(
+                self.fmt, self.protect, self.new_c, self.new_k, self.new_slots, self.q_lat, self.q_rope, self.cache,
+                self.num_pages, self.block_table, self.seq_lens, self.s_q, self.H, self.tau, self.prot,
+                self.num_prot, self.prot_slot, split_tokens=self.split_tokens, split_indptr=self.split_indptr,
+                num_splits=self.num_splits, out=self.out, lse=self.lse, part_m=self.part_m, part_s=self.part_s,
+                part_o=self.part_o, stream=stream)
+        else:
+            fn = mb.mla_lowbit_append_decode_attn if self.kind == "lowbit" else mb.mla_bf16_append_decode_attn
+            fn(self.fmt, self.new_c, self.new_k, self.new_slots, self.q_lat, self.q_rope, self.cache,
+               self.num_pages, self.block_table, self.seq_lens, self.s_q, self.H, self.tau,
+               split_tokens=self.split_tokens, split_indptr=self.split_indptr, num_splits=self.num_splits,
+               out=self.out, lse=self.lse, part_m=self.part_m, part_s=self.part_s, part_o=self.part_o,
+               stream=stream)
         if self.split_tokens:
             mb.mla_splitkv_combine(self.part_m, self.part_s, self.part_o, self.split_indptr, self.num_splits, self.B,
                                    self.s_q,

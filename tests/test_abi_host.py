@@ -32,7 +32,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(mb):
     names = declared_functions()
-    assert len(names) == 19
+    assert len(names) == 20
     lib = ctypes.CDLL(mb.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -234,6 +234,41 @@ def _append_decode_status(mb, **over):
 def test_append_decode_rejects_before_any_hip_call(mb, over, status):
     """The append-and-decode call validates the writer's and the decode's arguments on the host."""
     assert _append_decode_status(mb, **over) == status
+
+
+def _prot_append_decode_status(mb, pol=None, fmt=None, **over):
+    lib = mb.library()
+    fmt = mb.cache_format() if fmt is None else fmt
+    pol = mb.protect_policy() if pol is None else pol
+    a = dict(c_kv=16, c_stride=512, k_rope=16, k_stride=64, slots=16, q_lat=16, q_rope=16, cache=256,
+             num_pages=4, block_table=16, max_pages=2, seq_lens=16, B=1, s_q=1, H=128, scale=0.07, prot=256,
+             num_prot=1, prot_slot=16, split_tokens=0, split_indptr=None, num_splits=0, out=16, lse=None,
+             part_m=None, part_s=None, part_o=None)
+    a.update(over)
+    return lib.mla_lowbit_append_decode_attn_protected(
+        ctypes.byref(fmt), ctypes.byref(pol), a["c_kv"], a["c_stride"], a["k_rope"], a["k_stride"], a["slots"],
+        a["q_lat"], a["q_rope"], a["cache"], a["num_pages"], a["block_table"], a["max_pages"], a["seq_lens"],
+        a["B"], a["s_q"], a["H"], a["scale"], a["prot"], a["num_prot"], a["prot_slot"], a["split_tokens"],
+        a["split_indptr"], a["num_splits"], a["out"], a["lse"], a["part_m"], a["part_s"], a["part_o"], None)
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(c_kv=None), 1), (dict(slots=None), 1), (dict(c_stride=500), 1), (dict(c_kv=8), 2),
+    (dict(q_lat=None), 1), (dict(out=8), 2), (dict(s_q=3), 1), (dict(H=24), 1),
+    (dict(prot=None), 1), (dict(prot_slot=None), 1), (dict(num_prot=0), 1), (dict(prot=264), 2),
+    (dict(B=0), 0),
+])
+def test_protected_append_decode_rejects_before_any_hip_call(mb, over, status):
+    """The protected append-and-decode call validates the writer's, the
+    protection's and the decode's arguments on the host."""
+    assert _prot_append_decode_status(mb, **over) == status
+
+
+def test_protected_append_decode_rejects_bad_policy_and_format(mb):
+    assert _prot_append_decode_status(mb, pol=mb.protect_policy(-1, 4)) == 1
+    assert _prot_append_decode_status(mb, pol=mb.protect_policy(0, 0)) == 1
+    assert _prot_append_decode_status(mb, fmt=mb.cache_format(c_bits=16)) != 0
+    assert mb.library().mla_last_hip_error() == 0
 
 
 def test_timing_hook_takes_both_events_or_none(mb):

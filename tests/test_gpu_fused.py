@@ -54,6 +54,61 @@ def test_append_decode_matches_separate_calls(case):
     print(f"  {name}: cache {a.cache.numel()} bytes and {a.out.numel()} outputs identical", flush=True)
 
 
+PROTECTED = [
+    # (name, c_bits, meta, H, s_q, split_tokens, (sink, recent), start lengths, steps)
+    ("prot_c4_h128_sq1_split64", 4, "fp16", 128, 1, 64, (4, 128), [1, 4, 100, 127, 128, 129, 131, 200], 6),
+    ("prot_c4_h128_sq2_nosplit", 4, "fp16", 128, 2, 0, (4, 128), [2, 98, 126, 130, 164], 4),
+    ("prot_c2_h128_sq2_split32", 2, "fp16", 128, 2, 32, (40, 8), [2, 40, 47, 60], 8),
+    ("prot_c4_paper_h128_sq1_split32", 4, "paper", 128, 1, 32, (4, 16), [3, 20, 21, 90], 6),
+    ("prot_c4_h128_sq2_recent1_split32", 4, "fp16", 128, 2, 32, (4, 1), [2, 6, 40, 70], 4),
+    ("prot_c4_h128_sq1_sinkonly_split32", 4, "fp16", 128, 1, 32, (4, 0), [1, 3, 5, 70], 4),
+    ("prot_c4_h16_sq2_split32", 4, "fp16", 16, 2, 32, (4, 128), [2, 100, 129, 133], 4),
+]
+
+
+@pytest.mark.parametrize("case", PROTECTED, ids=[c[0] for c in PROTECTED])
+def test_protected_append_decode_matches_separate_calls(case):
+    """mla_lowbit_append_decode_attn_protected against the protected writer
+    followed by the protected decode, over consecutive steps across the
+    window's edge: identical packed pages, protection buffers, outputs and
+    lse after every step.  Cases: new tokens in a work item's first staged
+    tiles and later, sequences still entirely protected, a protected phase
+    that starts a work item, two row blocks (s_q = 2 at 128 heads), a one-row
+    window (the older new token read packed), sink rows only, INT2, the
+    paper's metadata, and 16 heads (the protected writer then runs as its own
+    launch)."""
+    import torch
+
+    from paper_2609_36760_amd import _binding as mb
+    from paper_2609_36760_amd.runner import DecodeRun
+    name, cb, meta, H, s_q, split, (sink, recent), start, steps = case
+    cap = [L + s_q * (steps - 1) for L in start]
+    w = syn.Workload(name, 170 + PROTECTED.index(case), B=len(start), H=H, s_q=s_q, context=None,
+                     layers=((cb, 4),), split_tokens=split, ctx_range=(1, 2))
+    tokens = [syn.sequence_tokens(w, 0, b, L) for b, L in enumerate(cap)]
+    ql, qr = syn.queries(w, 0)
+    lens = np.asarray(start, np.int32)
+    pol = mb.protect_policy(sink, recent)
+    a = DecodeRun(w, protect=pol, inputs=(tokens, ql, qr), seq_lens=lens, meta=meta)
+    b = DecodeRun(w, protect=pol, inputs=(tokens, ql, qr), seq_lens=lens, meta=meta)
+    b.cache.copy_(a.cache)
+    b.prot.copy_(a.prot)
+    torch.cuda.synchronize()
+    for step in range(steps):
+        if step:
+            a.advance()
+            b.advance()
+        a.step()
+        b.fused_step()
+        torch.cuda.synchronize()
+        assert torch.equal(a.cache, b.cache), f"step {step}: cache bytes differ"
+        assert torch.equal(a.prot, b.prot), f"step {step}: protection buffers differ"
+        assert torch.equal(a.out, b.out), f"step {step}: outputs differ"
+        assert torch.equal(a.lse, b.lse), f"step {step}: lse differs"
+    print(f"  {name}: {steps} steps, lengths {a.lens.tolist()}: cache, protection buffers and outputs identical",
+          flush=True)
+
+
 def test_timing_hook_leaves_outputs_and_times_the_kernel():
     """Events attached to the decode dispatch by mla_time_next_decode_launch:
     the outputs are unchanged, the pair is consumed by the decode dispatch (a
