@@ -127,7 +127,7 @@ template <> struct Cfg<KIND_C2R4P> : Cfg<KIND_C2R4> {
 };
 template <> struct Cfg<KIND_BF16> {
     static constexpr bool lowbit = false;
-    static constexpr int cc = 0, code_rounds = 0;
+    static constexpr int cc = 0;
     static constexpr int stage_bytes = 0;
     static constexpr int NT = 4, NS = 0, D = 2, loads = 10;   // 2432 chunks: 9 rounds of 256 + 128
     static constexpr int SC = 76;
