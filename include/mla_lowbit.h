@@ -228,10 +228,9 @@ int mla_bf16_decode_attn(const mla_cache_format* f,
  * is position seq_lens[b] - s_q + i of sequence b and is written at slot
  * slot_mapping[b * s_q + i] (device, int64; < 0 skips the token), which must
  * be that position's slot under block_table (a device-resident precondition).
- * For s_q * H > 32 the writer runs inside the decode launch: the workgroups
- * that read a new token's tile quantize and store it first.  Otherwise the
- * writer is launched separately first.  Arguments and errors as for the two
- * calls.
+ * The writer runs inside the decode launch: the workgroups that read a new
+ * token's tile quantize and store it first.  Arguments and errors as for the
+ * two calls.
  */
 int mla_lowbit_append_decode_attn(const mla_cache_format* f,
                                   const uint16_t* c_kv, int64_t c_kv_stride,
@@ -379,10 +378,9 @@ int mla_lowbit_decode_attn_protected(const mla_cache_format* f, const mla_protec
  * followed by mla_lowbit_decode_attn_protected, with identical cache bytes,
  * protection buffer rows and outputs.  A buffer index outside [0, num_prot)
  * skips the token's protection row (as the writer does) and is clamped for
- * the decode (as the decode does).  For s_q * H > 32 the writer runs inside
- * the decode launch: the workgroups that read a new token quantize and store
- * it first (its protection row too, for a token protected after the step).
- * Otherwise the protected writer is launched separately first.  Arguments
+ * the decode (as the decode does).  The writer runs inside the decode
+ * launch: the workgroups that read a new token quantize and store it first
+ * (its protection row too, for a token protected after the step).  Arguments
  * and errors as for the two calls; prot is written (device, 16-byte aligned).
  * Precondition: the sequences' protection buffers are distinct (a sequence
  * whose index is clamped onto another's buffer may read that buffer's new

@@ -39,6 +39,7 @@
 
 #include "internal.h"
 #include "kernel_common.h"
+#include "writer_common.h"
 
 namespace mla {
 namespace {
@@ -194,6 +195,57 @@ __device__ __forceinline__ void zero_offsets(f16x2 zz, f16x2* zo) {
     zo[0] = f16x2{768.0f16, 768.0f16} - zz;
     zo[1] = f16x2{960.0f16, 960.0f16} - zz;
     zo[2] = f16x2{1008.0f16, 1008.0f16} - zz;
+}
+
+// In-launch append (the writer of mla_lowbit_quant_append / mla_bf16_append,
+// and under protection of mla_lowbit_quant_append_protected, for the step's
+// new tokens), as in decode_attn.hip: the work item that reads a new token
+// (`reads(p)`: its key range, or under protection its key list, holds
+// position p) writes it before it stages any tile -- the packed copy (BF16:
+// the row), and under protection, for a token protected after the step, its
+// bf16 row into ring row p or sink + (p - sink) mod recent of the sequence's
+// buffer (skipped for a buffer index outside [0, num_prot)).  One 16-byte
+// piece per lane and round (72 per token; a group's 8 lanes stay together,
+// as the quantizer needs); the wave's stores land before its first staging
+// load.
+template <int KIND, bool kProt, class Reads>
+__device__ __forceinline__ void narrow_append(const DecodeArgs& a, int b, int L, Reads reads, int lane) {
+    using C = NCfg<KIND>;
+    bool any = false;
+    for (int i = 0; i < a.s_q; ++i) {
+        const int pos = L - a.s_q + i;
+        if (pos >= 0 && reads(pos)) any = true;
+    }
+    if (!any) return;
+    const int64_t num_slots = a.num_pages * a.g.page_size;
+    for (int piece = lane; piece < 72 * a.s_q; piece += 64) {
+        const int i = piece / 72, r = piece % 72;
+        const int pos = L - a.s_q + i;
+        if (pos < 0 || !reads(pos)) continue;
+        const int64_t tok = static_cast<int64_t>(b) * a.s_q + i;
+        const int64_t slot = a.new_slots[tok];
+        if (slot < 0 || slot >= num_slots) continue;
+        uint8_t* base = const_cast<uint8_t*>(a.cache) + slot / a.g.page_size * a.g.page_bytes;
+        const int64_t off = slot % a.g.page_size;
+        const bool rope = r >= 64;
+        const uint16_t* src = rope ? a.new_k + tok * a.new_k_stride + (r - 64) * 8
+                                   : a.new_c + tok * a.new_c_stride + r * 8;
+        const uint4 raw = *reinterpret_cast<const uint4*>(src);
+        if constexpr (C::lowbit) {
+            wc::quantize_store<C::cbits, C::pmeta>(raw, rope, r >> 3, r & 7, base, off, a.g);
+            if constexpr (kProt) {
+                const int64_t ps = a.prot_slot[b];
+                if ((pos < a.sink || pos >= L - a.recent) && ps >= 0 && ps < a.num_prot) {
+                    const int prow = pos < a.sink ? pos : a.sink + (pos - a.sink) % a.recent;
+                    uint8_t* dst = const_cast<uint8_t*>(a.prot) + (ps * (a.sink + a.recent) + prow) * 1152 + 16 * r;
+                    *reinterpret_cast<uint4*>(dst) = raw;
+                }
+            }
+        } else {
+            *reinterpret_cast<uint4*>(base + off * 1152 + r * 16) = raw;
+        }
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 // ---------------------------------------------------------------------------
@@ -562,6 +614,8 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
             t_end = min(split * a.split_tokens + a.split_tokens, L);
         }
         const int lim = row_ok ? min(L - a.s_q + qi + 1, t_end) : t_begin;
+        if (a.new_c != nullptr)
+            narrow_append<KIND, false>(a, b, L, [&](int pos) { return pos >= t_begin && pos < t_end; }, lane);
         run(std::integral_constant<int, KIND>{}, std::false_type{}, t_begin, t_end, t_begin, lim);
     } else {
         // the tile list of mla_plan_splits_protected (32-key list tiles)
@@ -575,6 +629,20 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
         if (a.split_tokens != 0) {
             u0 = split * (a.split_tokens / 32);
             u1 = min(u0 + a.split_tokens / 32, n_list);
+        }
+        if constexpr (NCfg<KIND>::lowbit) {
+            if (a.new_c != nullptr) {
+                // list tile of position p: a packed position by its tile (from the
+                // tile holding token `sink`), a protected one by its index among
+                // the protected rows
+                const int nsink = min(sink, L), r0 = max(sink, L - recent);
+                auto reads = [&](int pos) {
+                    const bool prot = pos < sink || pos >= L - recent;
+                    const int u = prot ? n_pk + (min(pos, nsink) + max(0, pos - r0)) / 32 : pos / 32 - pk0;
+                    return u >= u0 && u < u1;
+                };
+                narrow_append<KIND, true>(a, b, L, reads, lane);
+            }
         }
         if (u0 < n_pk) {
             const int tb = 32 * (pk0 + u0);

@@ -34,11 +34,8 @@ struct AppendArgs {
     // BF16 protection writes (lowbit_append_kernel<CBITS, true> only)
     uint8_t* prot;
     int64_t num_prot;
-    const int32_t* token_seq;   // [n] sequence of each token (nullptr: token t is query
-                                //     token t % s_q of sequence t / s_q, the step's append)
-    const int32_t* positions;   // [n] position of each token in its sequence (nullptr with
-                                //     token_seq: seq_lens[b] - s_q + t % s_q)
-    int32_t s_q;
+    const int32_t* token_seq;   // [n] sequence of each token
+    const int32_t* positions;   // [n] position of each token in its sequence
     const int32_t* seq_lens;    // [B] lengths after the append
     const int32_t* prot_slot;   // [B] buffer of each sequence
     int32_t B;

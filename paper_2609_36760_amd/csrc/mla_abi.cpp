@@ -236,30 +236,12 @@ int decode_common(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat,
                                                  : (paper ? mla::KIND_C2R4P : mla::KIND_C2R4);
     const bool narrow = s_q * H <= mla::kNarrowRows;
     if (nt != nullptr && B > 0) {
-        if (narrow) {
-            // few query rows: the writer runs as its own launch first (under
-            // protection the protected writer, the step's tokens implied)
-            mla::AppendArgs w{};
-            if (pd != nullptr) {
-                w.prot = static_cast<uint8_t*>(const_cast<void*>(pd->prot));
-                w.num_prot = pd->num_prot;
-                w.seq_lens = seq_lens;
-                w.prot_slot = pd->prot_slot;
-                w.B = B;
-                w.s_q = s_q;
-                w.sink = pd->policy->sink;
-                w.recent = pd->policy->recent;
-            }
-            st = append_common(f, lowbit, nt->c_kv, nt->c_kv_stride, nt->k_rope, nt->k_rope_stride,
-                               nt->slot_mapping, B * s_q, const_cast<void*>(cache), num_pages, stream, w);
-            if (st != MLA_OK) return st;
-        } else {
-            a.new_c = nt->c_kv;
-            a.new_c_stride = nt->c_kv_stride;
-            a.new_k = nt->k_rope;
-            a.new_k_stride = nt->k_rope_stride;
-            a.new_slots = nt->slot_mapping;
-        }
+        // the workgroups that read a new token write it inside the decode launch
+        a.new_c = nt->c_kv;
+        a.new_c_stride = nt->c_kv_stride;
+        a.new_k = nt->k_rope;
+        a.new_k_stride = nt->k_rope_stride;
+        a.new_slots = nt->slot_mapping;
     }
     if (pd == nullptr)
         return hip_status(narrow ? mla::launch_decode_narrow(kind, a, stream) : mla::launch_decode(kind, a, stream));

@@ -39,11 +39,10 @@ __global__ __launch_bounds__(kThreads) void lowbit_append_kernel(AppendArgs a) {
     const uint4 raw = *reinterpret_cast<const uint4*>(src);
 
     if constexpr (kProt) {
-        const bool implied = a.token_seq == nullptr;       // the step's tokens, [B][s_q]
-        const int bseq = implied ? static_cast<int>(token / a.s_q) : a.token_seq[token];
+        const int bseq = a.token_seq[token];
         if (bseq >= 0 && bseq < a.B) {
+            const int p = a.positions[token];
             const int L = a.seq_lens[bseq];
-            const int p = implied ? L - a.s_q + static_cast<int>(token % a.s_q) : a.positions[token];
             const int64_t ps = a.prot_slot[bseq];
             // p >= L - recent with p < L implies recent >= 1
             if (p >= 0 && p < L && (p < a.sink || p >= L - a.recent) && ps >= 0 && ps < a.num_prot) {

@@ -223,7 +223,7 @@ int main() {
                                                pslot, 0, nullptr, 0, out, lse, nullptr, nullptr, nullptr,
                                                nullptr) == MLA_EINVAL);
 
-        // append-and-decode: the writer inside the wide launch, its own launch for narrow shapes
+        // append-and-decode: the writer inside the decode launch (wide and narrow)
         const auto* c = static_cast<const uint16_t*>(dev(23));
         const auto* k = static_cast<const uint16_t*>(dev(24));
         const auto* slots = static_cast<const int64_t*>(dev(25));
@@ -235,7 +235,20 @@ int main() {
         CHECK(mla_lowbit_append_decode_attn(&f, c, 512, k, 64, slots, ql, qr, const_cast<void*>(cache), 4, bt, 4, sl,
                                             2, 1, 16, 0.1f, 0, nullptr, 0, out, lse, nullptr, nullptr, nullptr,
                                             nullptr) == MLA_OK);
-        CHECK(g_append_calls == before + 1 && g_last_narrow && g_last_append.n == 2);
+        CHECK(g_append_calls == before && g_last_narrow && g_last_decode.new_c == c && g_last_decode.new_k == k);
+        // the same under protection: one launch, the protection arguments and the new tokens together
+        auto* wprot = dev(21);
+        for (int heads : {128, 16}) {
+            CHECK(mla_lowbit_append_decode_attn_protected(&f, &pol, c, 512, k, 64, slots, ql, qr, const_cast<void*>(cache),
+                                                          4, bt, 4, sl, 2, 1, heads, 0.1f, wprot, 2, pslot, 0, nullptr,
+                                                          0, out, lse, nullptr, nullptr, nullptr, nullptr) == MLA_OK);
+            CHECK(g_append_calls == before && g_last_protected && g_last_narrow == (heads == 16));
+            CHECK(g_last_decode.new_c == c && g_last_decode.new_slots == slots && g_last_decode.prot == wprot &&
+                  g_last_decode.sink == 4 && g_last_decode.recent == 128 && g_last_decode.num_prot == 2);
+        }
+        CHECK(mla_lowbit_append_decode_attn_protected(&f, &pol, c, 512, k, 64, slots, ql, qr, const_cast<void*>(cache),
+                                                      4, bt, 4, sl, 2, 1, 128, 0.1f, nullptr, 2, pslot, 0, nullptr, 0,
+                                                      out, lse, nullptr, nullptr, nullptr, nullptr) == MLA_EINVAL);
 
         // timing hook: consumed by the next decode dispatch only
         CHECK(mla_time_next_decode_launch(reinterpret_cast<hipEvent_t>(dev(30)), nullptr) == MLA_EINVAL);

@@ -7,8 +7,8 @@ launch runs the same quantizer, and the decode reads the same bytes.  Cases
 cover new tokens whose tile is staged in the prologue (short key ranges) and
 later (long ranges), a split boundary between the two new tokens of a
 sequence, two row blocks per work item (s_q = 2, 128 heads: both write the
-same bytes), 4-bit, 2-bit and BF16 caches, the paper's metadata, and a
-16-head shape (the writer then runs as its own launch).
+same bytes), 4-bit, 2-bit and BF16 caches, the paper's metadata, and the
+16-row kernel (16 and 32 rows; s_q = 2 at 16 heads: two row blocks).
 """
 import numpy as np
 import pytest
@@ -29,6 +29,10 @@ CASES = [
     ("bf16_sq1_split64", 128, 1, [1, 33, 300], "bf16", 16, "fp16", 64),
     ("bf16_sq2_nosplit", 128, 2, [2, 97, 260], "bf16", 16, "fp16", 0),
     ("c4_h16_narrow", 16, 1, [7, 256, 333], "lowbit", 4, "fp16", 64),
+    ("c4_h16_sq2_split32_edge", 16, 2, [2, 17, 33, 65, 300], "lowbit", 4, "fp16", 32),
+    ("c2_h16_sq1_nosplit", 16, 1, [5, 96, 290], "lowbit", 2, "fp16", 0),
+    ("bf16_h16_sq2_split64", 16, 2, [2, 33, 300], "bf16", 16, "fp16", 64),
+    ("c4_paper_h32_sq1_split32", 32, 1, [3, 130, 400], "lowbit", 4, "paper", 32),
 ]
 
 
@@ -63,6 +67,9 @@ PROTECTED = [
     ("prot_c4_h128_sq2_recent1_split32", 4, "fp16", 128, 2, 32, (4, 1), [2, 6, 40, 70], 4),
     ("prot_c4_h128_sq1_sinkonly_split32", 4, "fp16", 128, 1, 32, (4, 0), [1, 3, 5, 70], 4),
     ("prot_c4_h16_sq2_split32", 4, "fp16", 16, 2, 32, (4, 128), [2, 100, 129, 133], 4),
+    ("prot_c2_h16_sq1_split32", 2, "fp16", 16, 1, 32, (4, 16), [3, 20, 21, 90], 6),
+    ("prot_c4_paper_h32_sq1_split64", 4, "paper", 32, 1, 64, (4, 128), [1, 100, 129, 200], 4),
+    ("prot_c4_h16_sq2_recent1_split32", 4, "fp16", 16, 2, 32, (4, 1), [2, 6, 40, 70], 4),
 ]
 
 
@@ -75,8 +82,7 @@ def test_protected_append_decode_matches_separate_calls(case):
     tiles and later, sequences still entirely protected, a protected phase
     that starts a work item, two row blocks (s_q = 2 at 128 heads), a one-row
     window (the older new token read packed), sink rows only, INT2, the
-    paper's metadata, and 16 heads (the protected writer then runs as its own
-    launch)."""
+    paper's metadata, and the 16-row kernel (16 and 32 rows)."""
     import torch
 
     from paper_2609_36760_amd import _binding as mb
