@@ -269,18 +269,32 @@ __global__ __launch_bounds__(64) void narrow_kernel(DecodeArgs a) {
 
     const int P = a.g.page_size;
     int b, split = 0;
+    int Lraw;
     if (a.split_tokens == 0) {
         b = w;
+        Lraw = a.seq_lens[b];
     } else {
-        int lo = 0, hi = a.B;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (a.split_indptr[mid] <= w) lo = mid; else hi = mid - 1;
+        // the last b with split_indptr[b] <= w, counted 64 entries at a time
+        // with the lengths loaded alongside: one round of loads instead of a
+        // chain of dependent ones (as in decode_attn.hip)
+        int cnt = 0, start = 0;
+        Lraw = 0;
+        for (int base = 0; base <= a.B; base += 64) {
+            const int idx = base + lane;
+            const int ip = idx <= a.B ? a.split_indptr[idx] : 0x7FFFFFFF;
+            const int sl = idx < a.B ? a.seq_lens[idx] : 0;
+            const int c = __builtin_popcountll(__builtin_amdgcn_ballot_w64(ip <= w));
+            const int last = cnt + c - 1 - base;     // lane of the last such entry in this chunk
+            if (c > 0 && last >= 0 && last < 64) {
+                start = __builtin_amdgcn_readlane(ip, last);
+                Lraw = __builtin_amdgcn_readlane(sl, last);
+            }
+            cnt += c;
         }
-        b = lo < a.B ? lo : a.B - 1;
-        split = w - a.split_indptr[b];
+        b = min(cnt - 1, a.B - 1);
+        split = w - start;
     }
-    const int L = min(max(a.seq_lens[b], 0), a.max_pages * P);
+    const int L = min(max(Lraw, 0), a.max_pages * P);
     const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_pages;
 
     const int row = rb * kRows + li;
