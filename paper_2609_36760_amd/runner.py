@@ -27,7 +27,7 @@ class DecodeRun:
     def __init__(self, w: syn.Workload, layer: int = 0, kind: str = "lowbit", device: str = "cuda",
                  split_tokens: int | None = None, seq_lens=None, threads: int = 16, prefill: bool = True,
                  token_cache: dict | None = None, protect=None, prot_slots=None, meta: str = "fp16",
-                 device_tokens: bool = False, inputs=None):
+                 device_tokens: bool = False, inputs=None, page_size: int = syn.PAGE):
         """``protect``: an ``mla_protect_policy`` to keep sink/recent tokens in
         bf16 (low-bit caches only); ``prot_slots``: the protection buffer of
         each sequence (default: buffer b for sequence b); ``meta``: "fp16"
@@ -41,7 +41,8 @@ class DecodeRun:
         ``q_rope [B, s_q, H, 64]`` bf16 bit patterns.  With explicit inputs,
         ``seq_lens`` may start the sequences at a prefix of their tokens:
         pages are allocated for all of them and :meth:`advance` moves the
-        sequences on, step by step."""
+        sequences on, step by step.  ``page_size``: tokens per cache page (a
+        multiple of 32)."""
         if inputs is not None and device_tokens:
             raise ValueError("explicit inputs are host arrays")
         self.inputs = inputs
@@ -55,7 +56,8 @@ class DecodeRun:
         if meta not in ("fp16", "paper"):
             raise ValueError(meta)
         self.meta = meta
-        self.fmt = mb.cache_format(c_bits=self.c_bits,
+        self.page_size = page_size
+        self.fmt = mb.cache_format(c_bits=self.c_bits, page_size=page_size,
                                    meta=mb.MLA_META_PAPER if meta == "paper" else mb.MLA_META_FP16)
         self.B, self.H, self.s_q = w.B, w.H, w.s_q
         self.tau = w.tau
@@ -69,7 +71,7 @@ class DecodeRun:
             capacity = lens
         self.lens = lens
         self.capacity = capacity
-        bt, num_pages = syn.page_table(w, capacity, layer)
+        bt, num_pages = syn.page_table(w, capacity, layer, page=page_size)
         self.block_table_host = bt
         self.num_pages = num_pages
         self.page_bytes = (mb.mla_lowbit_page_bytes(self.fmt) if kind == "lowbit"
@@ -129,7 +131,7 @@ class DecodeRun:
         """Slots, positions and host rows of the step's new tokens (the last s_q
         positions of every sequence)."""
         lens, bt, device = self.lens, self.block_table_host, self.device
-        new_slots = [syn.slots_of(bt[b], np.arange(int(lens[b]) - self.s_q, int(lens[b]))) for b in range(self.B)]
+        new_slots = [syn.slots_of(bt[b], np.arange(int(lens[b]) - self.s_q, int(lens[b])), self.page_size) for b in range(self.B)]
         self.new_slots = _dev(np.concatenate(new_slots), device)
         if not self.device_tokens:
             new_c, new_k = [], []
@@ -187,7 +189,7 @@ class DecodeRun:
             new_c.append(c[hist:].clone())
             new_k.append(k[hist:].clone())
             if prefill and hist > 0:
-                slots = _dev(syn.slots_of(self.block_table_host[b], np.arange(hist)), self.device)
+                slots = _dev(syn.slots_of(self.block_table_host[b], np.arange(hist), self.page_size), self.device)
                 seq = torch.full((hist,), b, dtype=torch.int32, device=self.device)
                 pos = torch.arange(hist, dtype=torch.int32, device=self.device)
                 self._append(c[:hist].view(torch.int16), k[:hist].view(torch.int16), slots, seq, pos)
@@ -239,7 +241,7 @@ class DecodeRun:
                 continue
             pend_c.append(c)
             pend_k.append(k)
-            pend_s.append(syn.slots_of(self.block_table_host[b], np.arange(n)))
+            pend_s.append(syn.slots_of(self.block_table_host[b], np.arange(n), self.page_size))
             pend_b.append(np.full(n, b, np.int32))
             pend_p.append(np.arange(n, dtype=np.int32))
             pend_n += n

@@ -144,12 +144,13 @@ def queries(w: Workload, layer: int = 0, batch=None):
     return ql, qr
 
 
-def page_table(w: Workload, lens: np.ndarray, layer: int = 0):
-    """Seeded page permutation: ``(block_table [B, max_pages] int32, num_pages)``.
+def page_table(w: Workload, lens: np.ndarray, layer: int = 0, page: int = PAGE):
+    """Seeded page permutation of ``page``-token pages:
+    ``(block_table [B, max_pages] int32, num_pages)``.
 
     Unused table entries are 0 (never read: they lie beyond ``seq_lens``).
     """
-    pages = (np.asarray(lens, np.int64) + PAGE - 1) // PAGE
+    pages = (np.asarray(lens, np.int64) + page - 1) // page
     total = int(pages.sum())
     perm = _rng(w.cfg, 6, layer).permutation(total).astype(np.int32)
     mp = int(pages.max())
@@ -161,10 +162,10 @@ def page_table(w: Workload, lens: np.ndarray, layer: int = 0):
     return bt, total
 
 
-def slots_of(block_table_row: np.ndarray, positions: np.ndarray) -> np.ndarray:
-    """Slot ``page * 64 + offset`` of each token position of one sequence."""
+def slots_of(block_table_row: np.ndarray, positions: np.ndarray, page: int = PAGE) -> np.ndarray:
+    """Slot ``page_id * page + offset`` of each token position of one sequence."""
     positions = np.asarray(positions, np.int64)
-    return block_table_row[positions // PAGE].astype(np.int64) * PAGE + positions % PAGE
+    return block_table_row[positions // page].astype(np.int64) * page + positions % page
 
 
 def device_sequence_tokens(w: Workload, layer: int, b: int, L: int, device: str = "cuda"):

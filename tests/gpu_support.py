@@ -63,7 +63,7 @@ def half_ulp_bf16(y) -> np.ndarray:
 
 
 def oracle_format(run) -> pc.CacheFormat:
-    return pc.CacheFormat(c_bits=run.c_bits, r_bits=run.r_bits, meta=run.meta)
+    return pc.CacheFormat(c_bits=run.c_bits, r_bits=run.r_bits, meta=run.meta, page_size=run.page_size)
 
 
 def gpu_pages(run, b: int) -> np.ndarray:
@@ -71,7 +71,8 @@ def gpu_pages(run, b: int) -> np.ndarray:
     (``[n_pages, page_bytes]`` uint8)."""
     import torch
     L = int(run.lens[b])
-    ids = run.block_table_host[b][: (L + PAGE - 1) // PAGE].astype(np.int64)
+    P = run.page_size
+    ids = run.block_table_host[b][: (L + P - 1) // P].astype(np.int64)
     pages = run.cache.view(run.num_pages, run.page_bytes)[torch.from_numpy(ids).to(run.cache.device)]
     return pages.cpu().numpy()
 
