@@ -3,7 +3,8 @@
 Small cases compare every output of every row with the oracle (exact softmax
 in fp64 over the oracle's own reconstruction of the same cache); they span
 several tiles, ragged tails, one- and two-token queries, split and unsplit
-launches, 4-bit and 2-bit content, the BF16 cache and 16 to 256 query rows.
+launches, 4-bit and 2-bit content, the BF16 cache and 16 to 512 query rows
+(one to four 128-row blocks per work item, the last one part-filled).
 The full-size workloads run in the launch configuration the benchmark times
 and are compared on sampled sequences and heads.
 """
@@ -41,6 +42,13 @@ SMALL = [
     ("bf16_h128_sq1_split64", 128, 1, [1, 33, 300], "bf16", 64),
     ("bf16_h128_sq2_nosplit", 128, 2, [2, 97, 260], "bf16", 0),
     ("bf16_h16_sq1_nosplit", 16, 1, [5, 256], "bf16", 0),
+    # row counts: 32 rows over two 16-row waves, part-filled and several
+    # 128-row blocks per work item
+    ("c4_h32_sq1_split32", 32, 1, [1, 45, 200], 4, 32),
+    ("c4_h32_sq2_nosplit", 32, 2, [2, 64, 150], 4, 0),
+    ("c4_h80_sq2_split64", 80, 2, [2, 99, 230], 4, 64),
+    ("c2_h256_sq2_split64", 256, 2, [2, 70, 201], 2, 64),
+    ("bf16_h256_sq1_nosplit", 256, 1, [1, 130], "bf16", 0),
 ]
 
 

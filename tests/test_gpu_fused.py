@@ -7,8 +7,9 @@ launch runs the same quantizer, and the decode reads the same bytes.  Cases
 cover new tokens whose tile is staged in the prologue (short key ranges) and
 later (long ranges), a split boundary between the two new tokens of a
 sequence, two row blocks per work item (s_q = 2, 128 heads: both write the
-same bytes), 4-bit, 2-bit and BF16 caches, the paper's metadata, and the
-16-row kernel (16 and 32 rows; s_q = 2 at 16 heads: two row blocks).
+same bytes; four at 256 heads, and a part-filled second one at 80), 4-bit,
+2-bit and BF16 caches, the paper's metadata, and the 16-row kernel (16 and 32
+rows; s_q = 2 at 16 heads: two row blocks).
 """
 import numpy as np
 import pytest
@@ -33,6 +34,10 @@ CASES = [
     ("c2_h16_sq1_nosplit", 16, 1, [5, 96, 290], "lowbit", 2, "fp16", 0),
     ("bf16_h16_sq2_split64", 16, 2, [2, 33, 300], "bf16", 16, "fp16", 64),
     ("c4_paper_h32_sq1_split32", 32, 1, [3, 130, 400], "lowbit", 4, "paper", 32),
+    ("c4_h256_sq2_split64", 256, 2, [2, 65, 199], "lowbit", 4, "fp16", 64),
+    ("c2_h80_sq2_nosplit", 80, 2, [2, 131, 260], "lowbit", 2, "fp16", 0),
+    ("bf16_h256_sq2_split32", 256, 2, [2, 33, 100], "bf16", 16, "fp16", 32),
+    ("c4_h32_sq1_split64", 32, 1, [1, 64, 65, 200], "lowbit", 4, "fp16", 64),
 ]
 
 
@@ -70,6 +75,7 @@ PROTECTED = [
     ("prot_c2_h16_sq1_split32", 2, "fp16", 16, 1, 32, (4, 16), [3, 20, 21, 90], 6),
     ("prot_c4_paper_h32_sq1_split64", 4, "paper", 32, 1, 64, (4, 128), [1, 100, 129, 200], 4),
     ("prot_c4_h16_sq2_recent1_split32", 4, "fp16", 16, 2, 32, (4, 1), [2, 6, 40, 70], 4),
+    ("prot_c4_h256_sq2_split64", 4, "fp16", 256, 2, 64, (4, 128), [2, 126, 130, 200], 4),
 ]
 
 
