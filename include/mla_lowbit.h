@@ -28,6 +28,13 @@
  *       MLA_EINVAL  a null pointer, a negative size or an ill-formed format
  *       MLA_ENOTSUP well-formed, but a shape the library does not implement
  *       MLA_EHIP    a HIP launch failed; mla_last_hip_error() gives the code
+ *   - Launch sizes.  A dispatch counts its work items in 32 bits, so shapes
+ *     whose launch would need more are refused with MLA_ENOTSUP: an append of
+ *     more than 2^25 tokens in one call (also B * s_q new tokens of an
+ *     append-and-decode call); a decode whose work items (B unsplit, else
+ *     num_splits), rounded up to a multiple of 8, times ceil(s_q * H / 128)
+ *     exceed 2^24 - 1 (the 16-row kernel, s_q * H <= 32: 2^26 - 1 times
+ *     ceil(s_q * H / 16)); a combine of more than 2^24 - 8 rows (B * s_q * H).
  *   - Device-resident values (page ids, sequence lengths, split offsets) are
  *     not readable by the host without a synchronization and are preconditions:
  *     s_q <= seq_lens[b] <= max_pages_per_seq * page_size, 0 <= page id <

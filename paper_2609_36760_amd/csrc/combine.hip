@@ -28,6 +28,7 @@ namespace {
 
 constexpr int kDc = 512;
 constexpr int kWaves = 4;         // waves (and rows) per workgroup
+static_assert(64 * kWaves == kCombineThreads, "launch shape the host checks");
 constexpr int kShare = 16;        // splits per sequence from which the waves share a row
 // kBatch: splits whose loads are in flight together (4 when sequences have
 // at most 4 splits on average, so that no load re-reads a split, else 8)

@@ -84,6 +84,7 @@ using namespace kc;
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRowsPerBlock = 32 * kWaves;
+static_assert(kThreads == kDecodeThreads && kRowsPerBlock == kDecodeRowsPerBlock, "launch shape the host checks");
 constexpr int kTile = 32;                       // tokens per tile
 constexpr int kDc = 512;
 constexpr int kDk = 576;                        // d_c + d_r
@@ -1256,9 +1257,7 @@ void decode_kernel(DecodeArgs a) {
 hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream) {
     if (a.num_work == 0) return hipSuccess;
     const LaunchEvents ev = take_launch_events();
-    const int rows = a.s_q * a.H;
-    const int RB = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
-    const int blocks = ((a.num_work + 7) / 8) * 8 * RB;
+    const int64_t blocks = decode_workgroups(a.num_work, static_cast<int64_t>(a.s_q) * a.H, kRowsPerBlock);
     const dim3 grid(static_cast<unsigned>(blocks)), block(kThreads);
     switch (kind) {
         case KIND_C4R4: dispatch_decode(decode_kernel<KIND_C4R4, false>, grid, block, stream, ev, a); break;
@@ -1273,9 +1272,7 @@ hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream
 hipError_t launch_decode_protected(CacheKind kind, const DecodeArgs& a, hipStream_t stream) {
     if (a.num_work == 0) return hipSuccess;
     const LaunchEvents ev = take_launch_events();
-    const int rows = a.s_q * a.H;
-    const int RB = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
-    const int blocks = ((a.num_work + 7) / 8) * 8 * RB;
+    const int64_t blocks = decode_workgroups(a.num_work, static_cast<int64_t>(a.s_q) * a.H, kRowsPerBlock);
     const dim3 grid(static_cast<unsigned>(blocks)), block(kThreads);
     switch (kind) {
         case KIND_C4R4: dispatch_decode(decode_kernel<KIND_C4R4, true>, grid, block, stream, ev, a); break;

@@ -51,6 +51,7 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kRows = 16;           // query rows per workgroup
+static_assert(kRows == kNarrowRowsPerBlock, "launch shape the host checks");
 constexpr int kTok = 16;            // tokens per tile
 constexpr int kQSteps = 18;         // 576 channels / 32 per k-step
 constexpr int kDc = 512;
@@ -713,8 +714,9 @@ template <bool kProt>
 hipError_t launch(CacheKind kind, const DecodeArgs& a, hipStream_t stream) {
     if (a.num_work == 0) return hipSuccess;
     const LaunchEvents ev = take_launch_events();
-    const int RB = (a.s_q * a.H + kRows - 1) / kRows;
-    const dim3 grid(static_cast<unsigned>(((a.num_work + 7) / 8) * 8 * RB)), block(64);
+    static_assert(kNarrowThreads == 64, "one wave per workgroup");
+    const int64_t blocks = decode_workgroups(a.num_work, static_cast<int64_t>(a.s_q) * a.H, kRows);
+    const dim3 grid(static_cast<unsigned>(blocks)), block(kNarrowThreads);
     switch (kind) {
         case KIND_C4R4: dispatch_decode(narrow_kernel<KIND_C4R4, kProt>, grid, block, stream, ev, a); break;
         case KIND_C2R4: dispatch_decode(narrow_kernel<KIND_C2R4, kProt>, grid, block, stream, ev, a); break;

@@ -103,6 +103,28 @@ hipError_t launch_decode(CacheKind kind, const DecodeArgs& a, hipStream_t stream
 hipError_t launch_decode_protected(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
 // The same computation for few query rows (s_q * H <= kNarrowRows): 16 rows per one-wave workgroup.
 constexpr int kNarrowRows = 32;
+
+// Launch shapes, for the host's size checks (each kernel file asserts its own
+// constants against these).  A dispatch packet holds the launch's work-item
+// count in 32 bits, so a launch of more than kMaxDispatchItems work items
+// cannot be expressed: the host refuses such shapes before any HIP call.
+constexpr int64_t kMaxDispatchItems = 0xFFFFFFFFll;
+constexpr int kDecodeThreads = 256;          // decode_attn.hip: 4 waves per workgroup
+constexpr int kDecodeRowsPerBlock = 128;     // query rows per workgroup
+constexpr int kNarrowThreads = 64;           // decode_narrow.hip: one wave per workgroup
+constexpr int kNarrowRowsPerBlock = 16;
+constexpr int kWorkGroupRound = 8;           // work items padded to a multiple of the 8 XCDs
+constexpr int kCombineThreads = 256;         // combine.hip: at most one row per workgroup
+constexpr int kAppendThreadsPerToken = 72;   // quant_append.hip: 9 groups x 8 lanes
+constexpr int64_t kMaxAppendTokens = int64_t(1) << 25;
+static_assert(kMaxAppendTokens * kAppendThreadsPerToken + 256 <= kMaxDispatchItems, "append launch size");
+
+// Work items of a launch over the split (or unsplit) work list: padded to the
+// XCD round, times the row blocks; the caller multiplies by the threads.
+constexpr int64_t decode_workgroups(int64_t num_work, int64_t rows, int64_t rows_per_block) {
+    return (num_work + kWorkGroupRound - 1) / kWorkGroupRound * kWorkGroupRound *
+           ((rows + rows_per_block - 1) / rows_per_block);
+}
 hipError_t launch_decode_narrow(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_decode_narrow_protected(CacheKind kind, const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_lowbit_append_protected(const AppendArgs& a, hipStream_t stream);

@@ -118,6 +118,7 @@ int check_append(const uint16_t* c_kv, int64_t c_kv_stride, const uint16_t* k_ro
                  const int64_t* slot_mapping, int32_t n, const void* cache, int64_t num_pages) {
     if (n < 0 || num_pages < 0) return MLA_EINVAL;
     if (n == 0) return MLA_OK;
+    if (n > mla::kMaxAppendTokens) return MLA_ENOTSUP;   // the launch would not fit one dispatch
     if (c_kv == nullptr || k_rope == nullptr || slot_mapping == nullptr || cache == nullptr) return MLA_EINVAL;
     if (num_pages == 0) return MLA_EINVAL;
     if (c_kv_stride < kDc || k_rope_stride < kDr) return MLA_EINVAL;
@@ -155,6 +156,17 @@ struct NewTokens {
     int64_t k_rope_stride;
     const int64_t* slot_mapping;
 };
+
+// Whether the decode launch over num_work work items fits one dispatch (its
+// work-item count is 32 bits): the wide kernel's 256-thread workgroups of 128
+// rows, or the 16-row kernel's one-wave workgroups when s_q * H <= 32.
+bool decode_fits(int64_t num_work, int32_t s_q, int32_t H) {
+    const int64_t rows = static_cast<int64_t>(s_q) * H;
+    const bool narrow = rows <= mla::kNarrowRows;
+    const int64_t groups = mla::decode_workgroups(num_work, rows, narrow ? mla::kNarrowRowsPerBlock
+                                                                         : mla::kDecodeRowsPerBlock);
+    return groups * (narrow ? mla::kNarrowThreads : mla::kDecodeThreads) <= mla::kMaxDispatchItems;
+}
 
 // Host validation of a decode call (no HIP call); part_* are checked only when
 // check_parts is set (the allocation-free entry point supplies its own).
@@ -196,6 +208,7 @@ int check_decode(const mla_cache_format* f, bool lowbit, const uint16_t* q_lat, 
             if (!aligned(part_o, 16)) return MLA_ENOTSUP;
         }
     }
+    if (!decode_fits(split_tokens == 0 ? B : num_splits, s_q, H)) return MLA_ENOTSUP;
     return MLA_OK;
 }
 
@@ -274,6 +287,8 @@ static int append_decode(const mla_cache_format* f, bool lowbit, const uint16_t*
     int st = lowbit ? check_lowbit_format(f) : check_shape(f);
     if (st != MLA_OK) return st;
     if (B < 0 || s_q < 0) return MLA_EINVAL;
+    if (s_q != 1 && s_q != 2) return MLA_EINVAL;
+    if (static_cast<int64_t>(B) * s_q > mla::kMaxAppendTokens) return MLA_ENOTSUP;
     st = check_append(c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, B * s_q, cache, num_pages);
     if (st != MLA_OK) return st;
     const NewTokens nt{c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping};
@@ -407,6 +422,8 @@ int mla_lowbit_append_decode_attn_protected(const mla_cache_format* f, const mla
     st = check_policy(p);
     if (st != MLA_OK) return st;
     if (B < 0 || s_q < 0) return MLA_EINVAL;
+    if (s_q != 1 && s_q != 2) return MLA_EINVAL;
+    if (static_cast<int64_t>(B) * s_q > mla::kMaxAppendTokens) return MLA_ENOTSUP;
     st = check_append(c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping, B * s_q, cache, num_pages);
     if (st != MLA_OK) return st;
     const NewTokens nt{c_kv, c_kv_stride, k_rope, k_rope_stride, slot_mapping};
@@ -515,6 +532,11 @@ int mla_splitkv_combine(const float* part_m, const float* part_s, const uint16_t
     if (part_m == nullptr || part_s == nullptr || part_o == nullptr || split_indptr == nullptr || out == nullptr)
         return MLA_EINVAL;
     if (!aligned(part_o, 16) || !aligned(out, 16)) return MLA_ENOTSUP;
+    // at most one row per 256-thread workgroup, workgroups padded to a multiple of 8
+    const int64_t rows = static_cast<int64_t>(B) * s_q * H;
+    if ((rows + mla::kWorkGroupRound - 1) / mla::kWorkGroupRound * mla::kWorkGroupRound * mla::kCombineThreads >
+        mla::kMaxDispatchItems)
+        return MLA_ENOTSUP;
     mla::CombineArgs a{};
     a.part_m = part_m;
     a.part_s = part_s;

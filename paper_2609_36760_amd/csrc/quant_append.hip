@@ -21,6 +21,7 @@ using wc::kGroup;
 using wc::kGroupsPerToken;
 using wc::kLanesPerGroup;
 constexpr int kThreads = 256;
+static_assert(kGroupsPerToken * kLanesPerGroup == kAppendThreadsPerToken, "launch shape the host checks");
 
 template <int CBITS, bool kProt, bool kPaper>
 __global__ __launch_bounds__(kThreads) void lowbit_append_kernel(AppendArgs a) {
@@ -61,7 +62,8 @@ __global__ __launch_bounds__(kThreads) void lowbit_append_kernel(AppendArgs a) {
 // BF16 comparison cache: row = [c_kv (512) | k_rope (64)] bf16; 72 lanes per
 // token, 16 bytes each.
 __global__ __launch_bounds__(kThreads) void bf16_append_kernel(AppendArgs a) {
-    constexpr int kLanesPerToken = 72;
+    constexpr int kLanesPerToken = 72;     // 64 content + 8 RoPE pieces of 16 bytes
+    static_assert(kLanesPerToken == kAppendThreadsPerToken, "launch shape the host checks");
     const int64_t tid = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
     const int64_t token = tid / kLanesPerToken;
     const int lane = static_cast<int>(tid % kLanesPerToken);
@@ -106,7 +108,7 @@ hipError_t launch_lowbit_append_protected(const AppendArgs& a, hipStream_t strea
 
 hipError_t launch_bf16_append(const AppendArgs& a, hipStream_t stream) {
     if (a.n == 0) return hipSuccess;
-    const int64_t threads = static_cast<int64_t>(a.n) * 72;
+    const int64_t threads = static_cast<int64_t>(a.n) * kAppendThreadsPerToken;
     const dim3 grid(static_cast<unsigned>((threads + kThreads - 1) / kThreads));
     hipLaunchKernelGGL(bf16_append_kernel, grid, dim3(kThreads), 0, stream, a);
     return hipGetLastError();

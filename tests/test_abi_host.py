@@ -295,3 +295,38 @@ def test_noalloc_rejects_more_partials_than_its_storage(mb):
     st = lib.mla_lowbit_decode_attn_noalloc(ctypes.byref(fmt), fake, fake, fake, 4, fake, 4, fake, 8, 3, 128, 0.1,
                                             64, fake, 4, fake, fake, None)
     assert st == mb.MLA_EINVAL
+
+
+# Launch sizes past a dispatch's 32-bit work-item count are refused on the
+# host (only the refusing side is exercised: an accepted call would launch).
+_SPLIT = dict(split_tokens=64, split_indptr=16, part_m=16, part_s=16, part_o=16)
+
+
+@pytest.mark.parametrize("over", [
+    dict(_SPLIT, num_splits=2 ** 24 - 7),              # 2^24 workgroups x 256 threads = 2^32
+    dict(_SPLIT, num_splits=2 ** 23 - 7, s_q=2),       # two 128-row blocks
+    dict(_SPLIT, num_splits=2 ** 23, H=256),
+    dict(B=2 ** 24),                                   # unsplit: one work item per sequence
+    dict(_SPLIT, num_splits=2 ** 26 - 7, H=16),        # 16-row kernel: 64-thread workgroups
+    dict(_SPLIT, num_splits=2 ** 25 - 7, H=32),        # two 16-row blocks
+    dict(_SPLIT, num_splits=2 ** 31 - 1),
+    dict(_SPLIT, num_splits=2 ** 20, H=2 ** 30),       # rows beyond 32 bits
+])
+def test_decode_refuses_launches_past_one_dispatch(mb, over):
+    assert _decode_status(mb, **over) == 2
+
+
+def test_append_and_combine_refuse_launches_past_one_dispatch(mb):
+    lib = mb.library()
+    fmt = mb.cache_format()
+    f = ctypes.byref(fmt)
+    for fn in (lib.mla_lowbit_quant_append, lib.mla_bf16_append):
+        assert fn(f, 16, 512, 16, 64, 16, 2 ** 25 + 1, 256, 1, None) == 2
+        assert fn(f, 16, 512, 16, 64, 16, 2 ** 31 - 1, 256, 1, None) == 2
+    # rows = B * s_q * H: 2^24 - 7 rounds up to 2^24 workgroups of 256 threads
+    assert lib.mla_splitkv_combine(16, 16, 16, 16, 2 ** 17, 2 ** 17, 1, 128, 512, 16, None, None) == 2
+    assert lib.mla_splitkv_combine(16, 16, 16, 16, 2 ** 20, 2 ** 16, 2, 128, 512, 16, None, None) == 2
+    # the new tokens of an append-and-decode call
+    assert _append_decode_status(mb, B=2 ** 24 + 1, s_q=2) == 2
+    assert _prot_append_decode_status(mb, B=2 ** 25 + 1) == 2
+    assert lib.mla_last_hip_error() == 0
