@@ -377,6 +377,62 @@ def cpu_baseline(budget_s: float = 15.0):
                       f"{blas} BLAS threads of {os.cpu_count()} host CPUs (input generation excluded)"}
 
 
+ORACLE_CONFIGS = (("tiny_b1_h16_256", 0), ("dsv3_b32_h128_4k_c4r4", 0), ("int2_b64_h128_32k_c2r4", 0),
+                  ("splitkv_b8_h128_128k_c4r4", 0), ("ragged_b96_h128_sq2_mixed", 0),
+                  ("ragged_b96_h128_sq2_mixed", 1), (MAIN, 0))
+
+
+def cpu_baseline_configs():
+    """The CPU baseline over every full-size configuration in full: the oracle,
+    as it stands, on every sequence -- (i) the fp32 quantize and pack of every
+    cached token (Appendix C.4), (ii) the dequantization and fp64 attention of
+    every row (Sec. 2.1), through per-split partials and their global merge
+    (Appendix C.5) where the configuration splits its keys.  Wall time per
+    configuration on the host's cores; inputs drawn outside the timed parts."""
+    from oracle import attention as at
+    from oracle import paged_cache as pc
+    from paper_2609_36760_amd import synthetic as syn
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        blas = 1
+    rows = []
+    for name, layer in ORACLE_CONFIGS:
+        w = syn.WORKLOADS[name]
+        fmt = pc.CacheFormat(c_bits=w.layers[layer][0], r_bits=w.layers[layer][1])
+        lens = syn.seq_lens(w)
+        t_pack = t_attn = 0.0
+        for b in range(w.B):
+            L = int(lens[b])
+            c, k = syn.sequence_tokens(w, layer, b, L)
+            ql, qr = syn.queries(w, layer, batch=[b])
+            t0 = time.perf_counter()
+            blocks = pc.encode_tokens(fmt, c, k)
+            t1 = time.perf_counter()
+            c_hat, kr_hat = pc.decode_blocks(fmt, blocks)
+            if w.split_tokens:
+                R = w.s_q * w.H
+                bounds = [(a, min(a + w.split_tokens, L)) for a in range(0, L, w.split_tokens)]
+                m, s_, o = at.chunk_partials(at.bf16_bits_to_f64(ql[0]).reshape(R, -1),
+                                             at.bf16_bits_to_f64(qr[0]).reshape(R, -1), c_hat, kr_hat, w.tau,
+                                             at.decode_limits(L, w.s_q, w.H), bounds)
+                at.merge(m, s_, o)
+            else:
+                at.decode_sequence(ql[0], qr[0], c_hat, kr_hat, w.tau)
+            t2 = time.perf_counter()
+            t_pack += t1 - t0
+            t_attn += t2 - t1
+        tokens = int(lens.sum())
+        rows.append({"workload": name, "layer": layer, "sequences": int(w.B), "cached_tokens": tokens,
+                     "rows": int(w.B * w.s_q * w.H), "splits": w.split_tokens or None,
+                     "quantize_pack_s": round(t_pack, 2), "dequant_attention_merge_s": round(t_attn, 2),
+                     "decode_tokens_per_s": round(w.B * w.s_q / (t_pack + t_attn), 3)})
+        print(f"[oracle {name} layer {layer}] pack {t_pack:.1f} s, attention {t_attn:.1f} s "
+              f"({tokens} tokens)", file=sys.stderr, flush=True)
+    return {"kind": "oracle", "cores": blas, "host_cpus": os.cpu_count(), "configs": rows}
+
+
 def measured_traffic(workload: str):
     """HBM bytes per launch of the low-bit decode kernel on ``workload`` from
     the recorded FETCH_SIZE / WRITE_SIZE counter runs, each scaled by what the
@@ -537,6 +593,8 @@ def main():
                     help="first copy a 256 MiB buffer once (reference for HBM traffic counters)")
     ap.add_argument("--paper-grid", action="store_true",
                     help="instead of the step benchmark: the paper's 16-head attention latency grid")
+    ap.add_argument("--oracle-configs", action="store_true",
+                    help="time the CPU oracle on every full-size configuration in full (no GPU use) and exit")
     ap.add_argument("--configs", action="store_true",
                     help="report the full-size correctness configurations instead (one JSON line)")
     ap.add_argument("--config-steps", type=int, default=100)
@@ -550,6 +608,9 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no multi-GPU path; "
               "the per-GPU kernel is the whole workload.", file=sys.stderr)
         sys.exit(2)
+    if args.oracle_configs:
+        print(json.dumps({"oracle_configs": cpu_baseline_configs()}), flush=True)
+        return
     import torch
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
